@@ -1,0 +1,190 @@
+/*
+ * moe.h -- C ABI of the MI355X (gfx950) routed-expert FP8 MoE FFN library.
+ *
+ * One routed-expert MoE layer of a DeepSeek-V3-style model with FP8 e4m3
+ * expert weights carrying fp32 scales per 128x128 weight block:
+ *
+ *   moe_quant_act   activations bf16 -> e4m3 per token per 128 channels
+ *   moe_permute     top-k routing -> per-expert token lists
+ *   moe_expert_ffn  per expert: gate and up projections, SiLU(gate)*up,
+ *                   re-quantization, down projection (FP8 x FP8, fp32
+ *                   accumulation, one scale per 128-K block)
+ *   moe_combine     routing-weighted fp32 sum of the k expert rows -> bf16
+ *   moe_ffn_streamed  the whole layer with the expert weights resident in
+ *                   pinned host memory, copied block by block into a device
+ *                   ring of expert slots on a copy stream while the compute
+ *                   stream runs the experts whose weights have landed
+ *
+ * Conventions (all entry points):
+ *   - Every pointer is owned by the caller.  "device" pointers are HIP device
+ *     memory of the current device; "pinned host" pointers come from
+ *     hipHostMalloc (or torch pin_memory).  The library never allocates,
+ *     frees or synchronizes the host on these calls; all work is enqueued on
+ *     the given stream(s) in order.
+ *   - Layouts are row-major and contiguous.  Weights are [out, in] (the
+ *     reduction dimension K contiguous); weight scales are
+ *     [out/128, in/128]; activation scales are [rows, cols/128].
+ *   - All feature dimensions must be multiples of 128 (the FP8 scale block),
+ *     else MOE_ERR_UNSUPPORTED_SHAPE.  Argument errors are returned before
+ *     anything is enqueued.  Launch failures return MOE_ERR_HIP (details in
+ *     moe_last_error()).  Data errors found on the device (an expert id out
+ *     of range or repeated within a token) are OR-ed into *dev_status.
+ *   - Inputs must be finite.  Calls on distinct streams are thread-safe.
+ */
+#ifndef MOE_FP8_MI355X_H
+#define MOE_FP8_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_BLOCK 128
+
+typedef enum {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = -1,
+  MOE_ERR_UNSUPPORTED_SHAPE = -2,
+  MOE_ERR_WORKSPACE = -3,
+  MOE_ERR_HIP = -4
+} moe_status_t;
+
+/* Bits OR-ed into the optional device status word by moe_permute. */
+#define MOE_DEV_BAD_EXPERT_ID 1  /* an id outside [0, n_experts) */
+#define MOE_DEV_DUP_EXPERT_ID 2  /* the same id twice in one token's top-k */
+
+/* Kernel family used by moe_expert_ffn.  AUTO picks DECODE for
+ * tokens <= MOE_DECODE_MAX_TOKENS, else PREFILL; both compute the same
+ * definition. */
+typedef enum {
+  MOE_REGIME_AUTO = 0,
+  MOE_REGIME_DECODE = 1,  /* weight-streaming FP8 MFMA GEMV, tokens <= 64 */
+  MOE_REGIME_PREFILL = 2  /* LDS-tiled block-scaled FP8 MFMA grouped GEMM */
+} moe_regime_t;
+
+#define MOE_DECODE_MAX_TOKENS 64
+
+typedef struct {
+  int32_t hidden;    /* H: model width, multiple of 128 */
+  int32_t inter;     /* I: expert intermediate width, multiple of 128 */
+  int32_t n_experts; /* E: routed experts in the layer, 1..1024 */
+  int32_t topk;      /* k: experts per token, 1..min(E, 32) */
+} moe_dims_t;
+
+/* Human-readable name of a status code (static storage). */
+const char* moe_status_string(moe_status_t status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* moe_last_error(void);
+
+/*
+ * Activation quantization (FP8 Block Scaling Format: activations are
+ * quantized to FP8 before the FP8 GEMM; 128-element scale blocks as in the
+ * Tiling and Scale-Block Optimizations of the FP8 GEMV kernel).
+ *
+ * For each row r and each block b of 128 consecutive columns:
+ *   a = max |x[r, 128b .. 128b+127]|, s[r,b] = a / 448 (fp32, correctly
+ *   rounded), q = e4m3 code nearest to x / s (correctly rounded fp32
+ *   division; ties to the even code; |x/s| > 448 saturates to 448; the sign
+ *   of zero is kept).  An all-zero block gives s = 0 and signed-zero codes.
+ *
+ * x_bf16: device [rows, cols] bf16 bit patterns.  q: device [rows, cols]
+ * e4m3 codes.  s: device [rows, cols/128] fp32.  rows >= 0 (0 enqueues
+ * nothing); cols a positive multiple of 128.
+ */
+moe_status_t moe_quant_act(const uint16_t* x_bf16, int32_t rows, int32_t cols,
+                           uint8_t* q, float* s, hipStream_t stream);
+
+/* Same rule over fp32 rows (used for the expert intermediate h). */
+moe_status_t moe_quant_rows_f32(const float* x, int32_t rows, int32_t cols,
+                                uint8_t* q, float* s, hipStream_t stream);
+
+/*
+ * Weight quantization to the DeepSeek-V3 FP8 storage format (FP8 Block
+ * Scaling Format): per 128x128 block of each [rows, cols] matrix the same
+ * rule as moe_quant_act with a = max over the 16384 block elements.
+ *
+ * w: device fp32 [n_mats, rows, cols].  q: device e4m3 [n_mats, rows, cols].
+ * s: device fp32 [n_mats, rows/128, cols/128].  rows, cols multiples of 128.
+ * This is offline weight preparation, not part of a layer call.
+ */
+moe_status_t moe_quant_weight(const float* w, int32_t n_mats, int32_t rows, int32_t cols,
+                              uint8_t* q, float* s, hipStream_t stream);
+
+/*
+ * Token -> expert permutation (tokens are gated and sorted by expert into
+ * per-expert token lists: Multi-GPU Parallelism and the standard EP
+ * workflow of Distributed Stream-loading Prefill).
+ *
+ * Flat slot f = t*k + j holds expert topk_ids[t*k + j].  The slots are
+ * stably sorted by expert id (ties by f):
+ *   expert_offsets[e] = number of slots with id < e  (expert_offsets[E] = T*k)
+ *   sorted_src[p]     = the slot f at sorted position p
+ *   dest_row[f]       = the sorted position p of slot f
+ * The result is unique, computed without order-dependent atomics, and
+ * identical run to run.
+ *
+ * topk_ids: device int32 [T, k].  expert_offsets: device int32 [E+1].
+ * sorted_src, dest_row: device int32 [T*k].  dev_status: device int32 or
+ * NULL; bits MOE_DEV_* are OR-ed in when ids are bad (outputs are then
+ * unspecified but every write stays in bounds).  ws: device workspace of at
+ * least moe_permute_workspace(T, k, E) bytes.  T >= 0, 1 <= k <= min(E,32),
+ * 1 <= E <= 1024.
+ */
+size_t moe_permute_workspace(int32_t T, int32_t k, int32_t E);
+moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                         int32_t* expert_offsets, int32_t* sorted_src, int32_t* dest_row,
+                         int32_t* dev_status, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Routed expert FFN over the expert-sorted rows (Fine-grained CPU
+ * Parallelism for MoE Inference: gate and up are independent, SiLU(gate)
+ * times up is fused into stage one, then down; FP8 x FP8 GEMMs with fp32
+ * accumulation and one fp32 scale per 128-K block).
+ *
+ * Row p (0 <= p < T*k) belongs to token t = sorted_src[p] / k and to the
+ * expert e with expert_offsets[e] <= p < expert_offsets[e+1].  For each n:
+ *   G[p,n] = sum_b (sx[t,b] * s_gate[e,n/128,b]) * sum_{i in b} qx[t,i] w_gate[e,n,i]
+ *   U[p,n] likewise with w_up, s_up
+ *   h = G * sigmoid(G) * U (fp32), quantized per row per 128 -> qh, sh
+ *   y_rows[p,m] = sum_b (sh[p,b] * s_down[e,m/128,b]) * sum_{i in b} qh[p,i] w_down[e,m,i]
+ *
+ * qx: device e4m3 [T, H]; sx: device fp32 [T, H/128] (from moe_quant_act).
+ * w_gate, w_up: device e4m3 [E, I, H]; s_gate, s_up: fp32 [E, I/128, H/128].
+ * w_down: device e4m3 [E, H, I]; s_down: fp32 [E, H/128, I/128].
+ * y_rows: device fp32 [T*k, H] in expert-sorted order.
+ * ws: device workspace of moe_expert_ffn_workspace(dims, T, regime) bytes.
+ * regime: see moe_regime_t; DECODE requires T <= MOE_DECODE_MAX_TOKENS.
+ */
+size_t moe_expert_ffn_workspace(moe_dims_t dims, int32_t T, moe_regime_t regime);
+moe_status_t moe_expert_ffn(moe_dims_t dims, int32_t T, moe_regime_t regime,
+                            const uint8_t* qx, const float* sx,
+                            const int32_t* expert_offsets, const int32_t* sorted_src,
+                            const uint8_t* w_gate, const float* s_gate,
+                            const uint8_t* w_up, const float* s_up,
+                            const uint8_t* w_down, const float* s_down,
+                            float* y_rows, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Router-weighted combine (Operator Fusion for Quantized Inference: the
+ * expert outputs are accumulated with the router weights in F32 and
+ * converted back to the hidden type):
+ *   out[t,n] = bf16_rne( sum_{j=0..k-1} topk_w[t,j] * y_rows[dest_row[t*k+j], n] )
+ * summed in fp32 in slot order from +0.0.
+ *
+ * y_rows: device fp32 [T*k, H]; dest_row: device int32 [T*k];
+ * topk_w: device fp32 [T, k]; out_bf16: device [T, H] bf16 bit patterns.
+ */
+moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const float* topk_w,
+                         int32_t T, int32_t k, int32_t H, uint16_t* out_bf16,
+                         hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_FP8_MI355X_H */

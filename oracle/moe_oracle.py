@@ -41,7 +41,9 @@ accumulation over blocks (ascending) are fp32.  Inputs must be finite.
 """
 from __future__ import annotations
 
+import concurrent.futures as _cf
 import math
+import os
 
 import numpy as np
 
@@ -83,9 +85,28 @@ def e4m3_encode(v: np.ndarray) -> np.ndarray:
 
     Nearest representable value, ties to the even code (the code whose
     mantissa LSB is 0), |v| > 448 saturates to 448, sign kept (so -0 and
-    negative values that round to zero give 0x80).
+    negative values that round to zero give 0x80).  Large arrays are split
+    into chunks handled on a thread pool; each element is independent.
     """
     v = np.asarray(v, dtype=np.float32)
+    if v.size > _PAR_MIN:
+        flat = v.reshape(-1)
+        out = np.empty(flat.shape, dtype=np.uint8)
+        step = _PAR_MIN
+
+        def work(i0):
+            out[i0:i0 + step] = _encode_chunk(flat[i0:i0 + step])
+
+        with _cf.ThreadPoolExecutor(max_workers=os.cpu_count() or 1) as ex:
+            list(ex.map(work, range(0, flat.size, step)))
+        return out.reshape(v.shape)
+    return _encode_chunk(v)
+
+
+_PAR_MIN = 1 << 20
+
+
+def _encode_chunk(v: np.ndarray) -> np.ndarray:
     sign = (np.signbit(v).astype(np.uint8) << 7).astype(np.uint8)
     a = np.minimum(np.abs(v.astype(np.float64)), E4M3_MAX)
     hi = np.searchsorted(_E4M3_POS, a, side="left")       # first value >= a

@@ -1,0 +1,113 @@
+"""MI355X (gfx950) routed-expert FP8 MoE FFN.
+
+Thin Python binding of libmoe.so (the C ABI in include/moe.h).  Functions
+carry the C names and only marshal arguments: every step of the layer runs
+in the library's HIP kernels.  torch tensors supply device memory and
+streams; nothing here computes.  If libmoe.so is missing the import fails:
+build it with ``python -m paper_2606_10493_amd.build``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+from ._lib import (  # noqa: F401
+    LIB_PATH, MoEError, lib, MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED_SHAPE,
+    MOE_ERR_WORKSPACE, MOE_ERR_HIP, MOE_REGIME_AUTO, MOE_REGIME_DECODE, MOE_REGIME_PREFILL,
+    MOE_DEV_BAD_EXPERT_ID, MOE_DEV_DUP_EXPERT_ID, MOE_DECODE_MAX_TOKENS, MoeDims, EXPORTED_SYMBOLS,
+)
+from ._lib import check as _check
+
+
+def _ptr(t):
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def _need(t, dtype_bytes, name):
+    if t is not None:
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a device tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if t.element_size() != dtype_bytes:
+            raise ValueError(f"{name} has element size {t.element_size()}, expected {dtype_bytes}")
+
+
+def moe_status_string(status: int) -> str:
+    return lib.moe_status_string(status).decode()
+
+
+def moe_last_error() -> str:
+    return lib.moe_last_error().decode()
+
+
+def moe_quant_act(x_bf16, q, s, stream=None):
+    """x_bf16 [rows, cols] (bf16 or 16-bit view) -> q uint8 [rows, cols], s fp32 [rows, cols/128]."""
+    _need(x_bf16, 2, "x_bf16"); _need(q, 1, "q"); _need(s, 4, "s")
+    rows, cols = x_bf16.shape
+    _check(lib.moe_quant_act(_ptr(x_bf16), rows, cols, _ptr(q), _ptr(s), _stream(stream)))
+
+
+def moe_quant_rows_f32(x, q, s, stream=None):
+    _need(x, 4, "x"); _need(q, 1, "q"); _need(s, 4, "s")
+    rows, cols = x.shape
+    _check(lib.moe_quant_rows_f32(_ptr(x), rows, cols, _ptr(q), _ptr(s), _stream(stream)))
+
+
+def moe_quant_weight(w, q, s, stream=None):
+    """w fp32 [n_mats, rows, cols] (or [rows, cols]) -> q uint8 same shape, s fp32 [.., rows/128, cols/128]."""
+    _need(w, 4, "w"); _need(q, 1, "q"); _need(s, 4, "s")
+    shape = w.shape if w.dim() == 3 else (1, *w.shape)
+    _check(lib.moe_quant_weight(_ptr(w), shape[0], shape[1], shape[2], _ptr(q), _ptr(s), _stream(stream)))
+
+
+def moe_permute_workspace(T: int, k: int, E: int) -> int:
+    return int(lib.moe_permute_workspace(T, k, E))
+
+
+def moe_permute(topk_ids, n_experts, expert_offsets, sorted_src, dest_row, dev_status=None, ws=None,
+                stream=None):
+    _need(topk_ids, 4, "topk_ids"); _need(expert_offsets, 4, "expert_offsets")
+    _need(sorted_src, 4, "sorted_src"); _need(dest_row, 4, "dest_row")
+    _need(dev_status, 4, "dev_status"); _need(ws, 1, "ws")
+    T, k = topk_ids.shape
+    _check(lib.moe_permute(_ptr(topk_ids), T, k, n_experts, _ptr(expert_offsets), _ptr(sorted_src),
+                           _ptr(dest_row), _ptr(dev_status), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def moe_expert_ffn_workspace(dims: MoeDims, T: int, regime: int = MOE_REGIME_AUTO) -> int:
+    return int(lib.moe_expert_ffn_workspace(dims, T, regime))
+
+
+def moe_expert_ffn(dims: MoeDims, T: int, regime: int, qx, sx, expert_offsets, sorted_src,
+                   w_gate, s_gate, w_up, s_up, w_down, s_down, y_rows, ws, stream=None):
+    for t, nb, n in ((qx, 1, "qx"), (sx, 4, "sx"), (expert_offsets, 4, "expert_offsets"),
+                     (sorted_src, 4, "sorted_src"), (w_gate, 1, "w_gate"), (s_gate, 4, "s_gate"),
+                     (w_up, 1, "w_up"), (s_up, 4, "s_up"), (w_down, 1, "w_down"), (s_down, 4, "s_down"),
+                     (y_rows, 4, "y_rows"), (ws, 1, "ws")):
+        _need(t, nb, n)
+    _check(lib.moe_expert_ffn(dims, T, regime, _ptr(qx), _ptr(sx), _ptr(expert_offsets), _ptr(sorted_src),
+                              _ptr(w_gate), _ptr(s_gate), _ptr(w_up), _ptr(s_up), _ptr(w_down),
+                              _ptr(s_down), _ptr(y_rows), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def moe_combine(y_rows, dest_row, topk_w, out_bf16, stream=None):
+    _need(y_rows, 4, "y_rows"); _need(dest_row, 4, "dest_row"); _need(topk_w, 4, "topk_w")
+    _need(out_bf16, 2, "out_bf16")
+    T, k = topk_w.shape
+    H = out_bf16.shape[1]
+    _check(lib.moe_combine(_ptr(y_rows), _ptr(dest_row), _ptr(topk_w), T, k, H, _ptr(out_bf16),
+                           _stream(stream)))
+
+
+from .layer import MoELayerBuffers, run_layer  # noqa: E402,F401

@@ -1,0 +1,127 @@
+// C ABI glue: status strings, per-thread error detail, workspace sizing and
+// the regime dispatch of moe_expert_ffn.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "common.h"
+
+namespace moe {
+
+static thread_local char g_last_error[512] = "";
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+}
+
+moe_status_t fail(moe_status_t st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+moe_status_t check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(MOE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return MOE_OK;
+}
+
+moe_status_t run_ffn_decode(const moe_dims_t& d, int32_t T, const uint8_t* qx, const float* sx,
+                            const int32_t* offsets, const int32_t* sorted_src, const uint8_t* w_gate,
+                            const float* s_gate, const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
+                            const float* s_down, float* y_rows, float* h, uint8_t* qh, float* sh,
+                            hipStream_t stream);
+
+moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, const float* sx,
+                             const int32_t* offsets, const int32_t* sorted_src, const uint8_t* w_gate,
+                             const float* s_gate, const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
+                             const float* s_down, float* y_rows, uint8_t* qh, float* sh, int32_t* tiles,
+                             hipStream_t stream);
+
+size_t prefill_tile_workspace(const moe_dims_t& d, int32_t T);
+
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+moe_regime_t resolve(moe_regime_t r, int32_t T) {
+  if (r == MOE_REGIME_AUTO) return T <= MOE_DECODE_MAX_TOKENS ? MOE_REGIME_DECODE : MOE_REGIME_PREFILL;
+  return r;
+}
+
+moe_status_t check_dims(const moe_dims_t& d, const char* who) {
+  if (d.hidden <= 0 || d.inter <= 0 || d.n_experts < 1 || d.n_experts > 1024 || d.topk < 1 || d.topk > 32 ||
+      d.topk > d.n_experts)
+    return fail(MOE_ERR_INVALID_ARG, "%s: dims H=%d I=%d E=%d k=%d", who, d.hidden, d.inter, d.n_experts, d.topk);
+  if (d.hidden % kBlock || d.inter % kBlock)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "%s: H=%d, I=%d must be multiples of 128", who, d.hidden, d.inter);
+  return MOE_OK;
+}
+
+}  // namespace
+}  // namespace moe
+
+using namespace moe;
+
+extern "C" const char* moe_status_string(moe_status_t s) {
+  switch (s) {
+    case MOE_OK: return "MOE_OK";
+    case MOE_ERR_INVALID_ARG: return "MOE_ERR_INVALID_ARG";
+    case MOE_ERR_UNSUPPORTED_SHAPE: return "MOE_ERR_UNSUPPORTED_SHAPE";
+    case MOE_ERR_WORKSPACE: return "MOE_ERR_WORKSPACE";
+    case MOE_ERR_HIP: return "MOE_ERR_HIP";
+  }
+  return "MOE_ERR_UNKNOWN";
+}
+
+extern "C" const char* moe_last_error(void) { return g_last_error; }
+
+extern "C" size_t moe_expert_ffn_workspace(moe_dims_t d, int32_t T, moe_regime_t regime) {
+  if (T < 0 || d.hidden <= 0 || d.inter <= 0 || d.topk <= 0 || d.n_experts <= 0) return 0;
+  const size_t R = (size_t)T * d.topk;
+  const size_t qh = align256(R * d.inter);
+  const size_t sh = align256(R * (d.inter / kBlock) * sizeof(float));
+  if (resolve(regime, T) == MOE_REGIME_DECODE) return qh + sh + align256(R * d.inter * sizeof(float));
+  return qh + sh + align256(prefill_tile_workspace(d, T));
+}
+
+extern "C" moe_status_t moe_expert_ffn(moe_dims_t d, int32_t T, moe_regime_t regime, const uint8_t* qx,
+                                       const float* sx, const int32_t* expert_offsets, const int32_t* sorted_src,
+                                       const uint8_t* w_gate, const float* s_gate, const uint8_t* w_up,
+                                       const float* s_up, const uint8_t* w_down, const float* s_down, float* y_rows,
+                                       void* ws, size_t ws_bytes, hipStream_t stream) {
+  moe_status_t st = check_dims(d, "moe_expert_ffn");
+  if (st != MOE_OK) return st;
+  if (T < 0) return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn: T=%d", T);
+  if (regime != MOE_REGIME_AUTO && regime != MOE_REGIME_DECODE && regime != MOE_REGIME_PREFILL)
+    return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn: regime=%d", (int)regime);
+  const moe_regime_t rg = resolve(regime, T);
+  if (rg == MOE_REGIME_DECODE && T > MOE_DECODE_MAX_TOKENS)
+    return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn: decode regime needs T <= %d (T=%d)", MOE_DECODE_MAX_TOKENS, T);
+  if ((int64_t)T * d.topk > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_expert_ffn: T*k overflows");
+  if (T == 0) return MOE_OK;
+  if (!qx || !sx || !expert_offsets || !sorted_src || !w_gate || !s_gate || !w_up || !s_up || !w_down || !s_down ||
+      !y_rows)
+    return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn: null pointer");
+  if (!aligned(qx, 16) || !aligned(w_gate, 16) || !aligned(w_up, 16) || !aligned(w_down, 16) ||
+      !aligned(y_rows, 16) || !aligned(sx, 4))
+    return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn: misaligned pointer (16 bytes needed)");
+  const size_t need = moe_expert_ffn_workspace(d, T, rg);
+  if (!ws || ws_bytes < need)
+    return fail(MOE_ERR_WORKSPACE, "moe_expert_ffn: workspace %zu bytes < %zu", ws_bytes, need);
+  if (!aligned(ws, 256)) return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn: workspace must be 256-byte aligned");
+  const size_t R = (size_t)T * d.topk;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  uint8_t* qh = base;
+  float* sh = reinterpret_cast<float*>(base + align256(R * d.inter));
+  uint8_t* rest = reinterpret_cast<uint8_t*>(sh) + align256(R * (d.inter / kBlock) * sizeof(float));
+  if (rg == MOE_REGIME_DECODE)
+    return run_ffn_decode(d, T, qx, sx, expert_offsets, sorted_src, w_gate, s_gate, w_up, s_up, w_down, s_down,
+                          y_rows, reinterpret_cast<float*>(rest), qh, sh, stream);
+  return run_ffn_prefill(d, T, qx, sx, expert_offsets, sorted_src, w_gate, s_gate, w_up, s_up, w_down, s_down, y_rows,
+                         qh, sh, reinterpret_cast<int32_t*>(rest), stream);
+}

@@ -1,0 +1,94 @@
+// Shared device helpers and host error plumbing of the MoE FP8 library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "moe.h"
+
+namespace moe {
+
+constexpr int kBlock = MOE_BLOCK;   // FP8 scale block (elements along K)
+constexpr float kE4M3Max = 448.0f;  // largest finite e4m3 magnitude
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// fp32 -> e4m3 code (OCP E4M3: bias 7, no infinities, max 448), round to
+// nearest with ties to the even code, |v| >= 448 saturates to 448, the sign
+// of zero is kept.  Written from the IEEE-754 binary32 layout:
+//   * |v| < 2^-6 (e4m3 subnormals, spacing 2^-9): code = rne(|v| * 2^9),
+//     the product is exact and 8 is the smallest normal (code 0x08);
+//   * otherwise re-bias the exponent (127 -> 7) and round the 23-bit
+//     mantissa to 3 bits by adding 0x7FFFF plus the kept LSB before dropping
+//     20 bits; a mantissa carry moves into the exponent field by itself.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t encode_e4m3(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const uint32_t sign = (u >> 24) & 0x80u;
+  const uint32_t a = u & 0x7fffffffu;
+  const float fa = __uint_as_float(a);
+  uint32_t code;
+  if (!(fa < kE4M3Max)) {
+    code = 0x7eu;
+  } else if (a < 0x3c800000u) {  // 2^-6
+    code = (uint32_t)__builtin_rintf(fa * 512.0f);
+  } else {
+    const uint32_t r = a + 0x7ffffu + ((a >> 20) & 1u);
+    code = (r >> 20) - (120u << 3);
+  }
+  return code | sign;
+}
+
+// Quantize one value given the block scale s (s == 0: all-zero block, keep
+// the sign only).  x / s is the correctly rounded fp32 quotient (the library
+// is built with correctly rounded fp32 division).
+__device__ __forceinline__ uint32_t quantize_e4m3(float x, float s) {
+  if (s > 0.0f) return encode_e4m3(x / s);
+  return (__float_as_uint(x) >> 24) & 0x80u;
+}
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// FP8 x FP8 MFMA over one 128-element K block: D[16x16] = A[16x128] * B[128x16].
+// Lane l supplies row (l & 15) of A and column (l & 15) of B, 32 bytes each,
+// taken from the same 32-byte K range for A and B; the instruction's internal
+// order of K does not change the dot products because A and B share it.
+// The E8M0 block scales of the instruction are left at 127 (= 1.0); the fp32
+// scales are applied to the result.
+__device__ __forceinline__ v4f mfma_f8_16x16x128(const v8i& a, const v8i& b) {
+  const v4f zero = {0.f, 0.f, 0.f, 0.f};
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, zero, 0, 0, 0, 127, 0, 127);
+}
+
+__device__ __forceinline__ v8i load_v8i(const uint8_t* p) {
+  const uint4 lo = *reinterpret_cast<const uint4*>(p);
+  const uint4 hi = *reinterpret_cast<const uint4*>(p + 16);
+  v8i r;
+  r[0] = lo.x; r[1] = lo.y; r[2] = lo.z; r[3] = lo.w;
+  r[4] = hi.x; r[5] = hi.y; r[6] = hi.z; r[7] = hi.w;
+  return r;
+}
+
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  return (g * (1.0f / (1.0f + expf(-g)))) * u;
+}
+
+// ----------------------------------------------------------------- host side
+void set_error(const char* fmt, ...);
+moe_status_t fail(moe_status_t st, const char* fmt, ...);
+moe_status_t check_launch(const char* what);
+
+inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace moe

@@ -1,0 +1,290 @@
+// Token -> expert permutation: a stable counting sort of the flat slots
+// f = t*k + j by expert id (tokens gated and sorted by expert into per-expert
+// token lists, as in the standard expert-parallel workflow of the paper).
+//
+// A token lists each expert at most once, so within one expert the stable
+// order by f is the order by token.  Each 256-token chunk therefore builds,
+// in LDS, one 256-bit token mask per expert (4 x 64-bit words, set with an
+// order-independent atomic OR).  The rank of (t, e) inside the chunk is the
+// number of set bits below t in e's mask, so the scatter is exact and
+// deterministic without any order-dependent atomics.
+//
+// Slots whose id is out of range, or repeats an earlier slot's id in the
+// same token, are reported in the device status word and parked after all
+// valid rows (positions expert_offsets[E] .. T*k-1, in slot order), so the
+// outputs stay a bijection and every later index stays in bounds.
+//
+//   one chunk  (T <= 256): permute_small_kernel does count, scan and scatter.
+//   several chunks: permute_count_kernel -> permute_scan_kernel -> permute_scatter_kernel.
+#include "common.h"
+
+namespace moe {
+
+namespace {
+
+constexpr int kChunk = 256;      // tokens per workgroup (one per thread)
+constexpr int kMaxExperts = 1024;
+constexpr int kMaxTopk = 32;
+
+struct SlotCheck {
+  int expert;
+  uint32_t err;  // MOE_DEV_* bits, 0 if the slot is valid
+};
+
+__device__ __forceinline__ SlotCheck check_slot(const int32_t* __restrict__ ids, int64_t tok_base, int j, int E) {
+  SlotCheck r;
+  r.expert = ids[tok_base + j];
+  r.err = 0;
+  if (r.expert < 0 || r.expert >= E) {
+    r.err = MOE_DEV_BAD_EXPERT_ID;
+    return r;
+  }
+  for (int i = 0; i < j; ++i)
+    if (ids[tok_base + i] == r.expert) r.err = MOE_DEV_DUP_EXPERT_ID;
+  return r;
+}
+
+// Fill the per-expert token masks of one chunk; returns this thread's error bits.
+__device__ __forceinline__ uint32_t build_masks(unsigned long long* mask, int* bad_count, const int32_t* ids,
+                                                int64_t t, int64_t T, int k, int E) {
+  uint32_t err = 0;
+  if (t < T) {
+    const int64_t base = t * k;
+    const unsigned long long bit = 1ull << (threadIdx.x & 63);
+    const int word = threadIdx.x >> 6;
+    for (int j = 0; j < k; ++j) {
+      const SlotCheck s = check_slot(ids, base, j, E);
+      if (s.err == 0) {
+        atomicOr(&mask[s.expert * 4 + word], bit);
+      } else {
+        err |= s.err;
+        atomicAdd(bad_count, 1);
+      }
+    }
+  }
+  return err;
+}
+
+__device__ __forceinline__ int rank_in_chunk(const unsigned long long* mask, int e) {
+  const int word = threadIdx.x >> 6;
+  const unsigned long long below = (1ull << (threadIdx.x & 63)) - 1ull;
+  int r = __popcll(mask[e * 4 + word] & below);
+  for (int w = 0; w < word; ++w) r += __popcll(mask[e * 4 + w]);
+  return r;
+}
+
+__device__ __forceinline__ int mask_count(const unsigned long long* mask, int e) {
+  return __popcll(mask[e * 4]) + __popcll(mask[e * 4 + 1]) + __popcll(mask[e * 4 + 2]) + __popcll(mask[e * 4 + 3]);
+}
+
+__device__ __forceinline__ void report(int32_t* dev_status, uint32_t err) {
+  // Any-lane OR, then one atomic per wave.
+  for (int m = 32; m >= 1; m >>= 1) err |= (uint32_t)__shfl_xor((int)err, m, 64);
+  if (dev_status && err && (threadIdx.x & 63) == 0) atomicOr(dev_status, (int)err);
+}
+
+// Valid slots of this chunk go to base_e + rank; invalid ones, in slot order,
+// to bad_base + running index (walked by one thread: the error path only).
+__device__ __forceinline__ void scatter_chunk(const unsigned long long* mask, const int32_t* ids, int64_t chunk0,
+                                              int64_t T, int k, int E, const int32_t* base_of_e, int32_t bad_base,
+                                              int bad_count, int32_t* sorted_src, int32_t* dest_row) {
+  const int64_t t = chunk0 + threadIdx.x;
+  if (t < T) {
+    const int64_t tb = t * k;
+    for (int j = 0; j < k; ++j) {
+      const SlotCheck s = check_slot(ids, tb, j, E);
+      if (s.err) continue;
+      const int32_t p = base_of_e[s.expert] + rank_in_chunk(mask, s.expert);
+      dest_row[tb + j] = p;
+      sorted_src[p] = (int32_t)(tb + j);
+    }
+  }
+  if (bad_count > 0 && threadIdx.x == 0) {
+    int32_t p = bad_base;
+    const int64_t t1 = min(T, chunk0 + kChunk);
+    for (int64_t tt = chunk0; tt < t1; ++tt)
+      for (int j = 0; j < k; ++j) {
+        const SlotCheck s = check_slot(ids, tt * k, j, E);
+        if (!s.err) continue;
+        dest_row[tt * k + j] = p;
+        sorted_src[p] = (int32_t)(tt * k + j);
+        ++p;
+      }
+  }
+}
+
+// Exclusive scan of v over a 256-thread block (LDS, Hillis-Steele).
+__device__ __forceinline__ int block_exclusive_scan256(int v, int* tmp, int* total) {
+  const int t = threadIdx.x;
+  tmp[t] = v;
+  __syncthreads();
+  for (int d = 1; d < 256; d <<= 1) {
+    const int add = (t >= d) ? tmp[t - d] : 0;
+    __syncthreads();
+    tmp[t] += add;
+    __syncthreads();
+  }
+  const int incl = tmp[t];
+  *total = tmp[255];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                            int32_t* __restrict__ offsets,
+                                                            int32_t* __restrict__ sorted_src,
+                                                            int32_t* __restrict__ dest_row,
+                                                            int32_t* __restrict__ dev_status) {
+  __shared__ unsigned long long mask[kMaxExperts * 4];
+  __shared__ int start[kMaxExperts];
+  __shared__ int tmp[256];
+  __shared__ int bad_count;
+  for (int i = threadIdx.x; i < E * 4; i += 256) mask[i] = 0ull;
+  if (threadIdx.x == 0) bad_count = 0;
+  __syncthreads();
+  const uint32_t err = build_masks(mask, &bad_count, ids, threadIdx.x, T, k, E);
+  __syncthreads();
+  // Thread i owns experts 4i .. 4i+3 for the scan.
+  int c[4], local = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * threadIdx.x + q;
+    c[q] = (e < E) ? mask_count(mask, e) : 0;
+    local += c[q];
+  }
+  int total_valid;
+  int run = block_exclusive_scan256(local, tmp, &total_valid);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * threadIdx.x + q;
+    if (e < E) {
+      start[e] = run;
+      offsets[e] = run;
+    }
+    run += c[q];
+  }
+  if (threadIdx.x == 0) offsets[E] = total_valid;
+  __syncthreads();
+  scatter_chunk(mask, ids, 0, T, k, E, start, total_valid, bad_count, sorted_src, dest_row);
+  report(dev_status, err);
+}
+
+// counts: [n_chunks][E+1]; entry E is the chunk's number of invalid slots.
+__global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                            int32_t* __restrict__ counts,
+                                                            int32_t* __restrict__ dev_status) {
+  __shared__ unsigned long long mask[kMaxExperts * 4];
+  __shared__ int bad_count;
+  for (int i = threadIdx.x; i < E * 4; i += 256) mask[i] = 0ull;
+  if (threadIdx.x == 0) bad_count = 0;
+  __syncthreads();
+  const int64_t chunk0 = (int64_t)blockIdx.x * kChunk;
+  const uint32_t err = build_masks(mask, &bad_count, ids, chunk0 + threadIdx.x, T, k, E);
+  __syncthreads();
+  int32_t* row = counts + (int64_t)blockIdx.x * (E + 1);
+  for (int e = threadIdx.x; e < E; e += 256) row[e] = mask_count(mask, e);
+  if (threadIdx.x == 0) row[E] = bad_count;
+  report(dev_status, err);
+}
+
+// One workgroup of 1024 threads; thread e scans expert e over the chunks.
+__global__ __launch_bounds__(1024) void permute_scan_kernel(const int32_t* __restrict__ counts, int n_chunks, int E,
+                                                            int32_t* __restrict__ base,
+                                                            int32_t* __restrict__ offsets) {
+  __shared__ int tmp[1024];
+  const int e = threadIdx.x;
+  int tot = 0;
+  if (e < E)
+    for (int c = 0; c < n_chunks; ++c) tot += counts[(int64_t)c * (E + 1) + e];
+  tmp[e] = tot;
+  __syncthreads();
+  for (int d = 1; d < 1024; d <<= 1) {
+    const int add = (e >= d) ? tmp[e - d] : 0;
+    __syncthreads();
+    tmp[e] += add;
+    __syncthreads();
+  }
+  const int total_valid = tmp[1023];
+  if (e < E) {
+    int run = tmp[e] - tot;
+    offsets[e] = run;
+    for (int c = 0; c < n_chunks; ++c) {
+      const int64_t i = (int64_t)c * (E + 1) + e;
+      base[i] = run;
+      run += counts[i];
+    }
+  }
+  if (e == 0) {
+    offsets[E] = total_valid;
+    int run = total_valid;
+    for (int c = 0; c < n_chunks; ++c) {
+      const int64_t i = (int64_t)c * (E + 1) + E;
+      base[i] = run;
+      run += counts[i];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void permute_scatter_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                              const int32_t* __restrict__ counts,
+                                                              const int32_t* __restrict__ base,
+                                                              int32_t* __restrict__ sorted_src,
+                                                              int32_t* __restrict__ dest_row) {
+  __shared__ unsigned long long mask[kMaxExperts * 4];
+  __shared__ int bad_count;
+  for (int i = threadIdx.x; i < E * 4; i += 256) mask[i] = 0ull;
+  if (threadIdx.x == 0) bad_count = 0;
+  __syncthreads();
+  const int64_t chunk0 = (int64_t)blockIdx.x * kChunk;
+  build_masks(mask, &bad_count, ids, chunk0 + threadIdx.x, T, k, E);
+  __syncthreads();
+  const int32_t* brow = base + (int64_t)blockIdx.x * (E + 1);
+  const int nbad = counts[(int64_t)blockIdx.x * (E + 1) + E];
+  scatter_chunk(mask, ids, chunk0, T, k, E, brow, brow[E], nbad, sorted_src, dest_row);
+}
+
+int64_t n_chunks_of(int32_t T) { return ((int64_t)T + kChunk - 1) / kChunk; }
+
+}  // namespace
+
+}  // namespace moe
+
+using namespace moe;
+
+extern "C" size_t moe_permute_workspace(int32_t T, int32_t k, int32_t E) {
+  (void)k;
+  if (T < 0 || E <= 0) return 0;
+  const int64_t nc = n_chunks_of(T);
+  if (nc <= 1) return 256;
+  return (size_t)(2 * nc * (E + 1) * sizeof(int32_t) + 256);
+}
+
+extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                                    int32_t* expert_offsets, int32_t* sorted_src, int32_t* dest_row,
+                                    int32_t* dev_status, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (T < 0 || E < 1 || E > kMaxExperts || k < 1 || k > kMaxTopk || k > E)
+    return fail(MOE_ERR_INVALID_ARG, "moe_permute: T=%d k=%d E=%d (need T>=0, 1<=k<=min(E,32), 1<=E<=1024)", T, k,
+                E);
+  if ((int64_t)T * k > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_permute: T*k overflows int32");
+  if (!expert_offsets || (T > 0 && (!topk_ids || !sorted_src || !dest_row)))
+    return fail(MOE_ERR_INVALID_ARG, "moe_permute: null pointer");
+  const int64_t nc = n_chunks_of(T);
+  if (nc <= 1) {
+    hipLaunchKernelGGL(permute_small_kernel, dim3(1), dim3(256), 0, stream, topk_ids, T, k, E, expert_offsets,
+                       sorted_src, dest_row, dev_status);
+    return check_launch("moe_permute");
+  }
+  const size_t need = moe_permute_workspace(T, k, E);
+  if (!ws || ws_bytes < need)
+    return fail(MOE_ERR_WORKSPACE, "moe_permute: workspace %zu bytes < %zu", ws_bytes, need);
+  if (!aligned(ws, 4)) return fail(MOE_ERR_INVALID_ARG, "moe_permute: misaligned workspace");
+  int32_t* counts = static_cast<int32_t*>(ws);
+  int32_t* base = counts + nc * (E + 1);
+  hipLaunchKernelGGL(permute_count_kernel, dim3((unsigned)nc), dim3(256), 0, stream, topk_ids, T, k, E, counts,
+                     dev_status);
+  hipLaunchKernelGGL(permute_scan_kernel, dim3(1), dim3(1024), 0, stream, counts, (int)nc, E, base,
+                     expert_offsets);
+  hipLaunchKernelGGL(permute_scatter_kernel, dim3((unsigned)nc), dim3(256), 0, stream, topk_ids, T, k, E, counts,
+                     base, sorted_src, dest_row);
+  return check_launch("moe_permute");
+}

@@ -1,0 +1,105 @@
+"""Helpers of the GPU parity tests: seeded inputs on both sides, oracle runs.
+
+Weights are drawn in fp32 by ``synth``; the GPU quantizes them with
+moe_quant_weight and the oracle with its own quantize_weight.  The oracle
+never receives a value produced by the HIP library.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+import synth
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def require_gpu():
+    if not torch.cuda.is_available():
+        raise RuntimeError("GPU tests need an MI355X; run them with -m gpu on a GPU machine")
+    import paper_2606_10493_amd as moe  # noqa: F401  (fails loudly if libmoe.so is missing)
+    return moe
+
+
+def to_dev(a: np.ndarray, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.view(dtype)
+    return t.cuda()
+
+
+def bf16_dev(bits: np.ndarray):
+    return to_dev(bits.view(np.int16))
+
+
+def quantize_weights_gpu(moe, wg, wu, wd):
+    """fp32 host stacks -> device (q, s) triples quantized by the library."""
+    out = []
+    for w in (wg, wu, wd):
+        e, n, k = w.shape
+        dw = to_dev(w)
+        q = torch.empty((e, n, k), dtype=torch.uint8, device="cuda")
+        s = torch.empty((e, n // 128, k // 128), dtype=torch.float32, device="cuda")
+        moe.moe_quant_weight(dw, q, s)
+        out += [q, s]
+        del dw
+    torch.cuda.synchronize()
+    return tuple(out)
+
+
+def generated_layer_gpu(moe, w: synth.Workload, layer: int = 0):
+    """Full layer: fp32 experts drawn on the GPU one by one, quantized in place."""
+    e, i, h = w.n_experts, w.inter, w.hidden
+    qg = torch.empty((e, i, h), dtype=torch.uint8, device="cuda")
+    qu = torch.empty((e, i, h), dtype=torch.uint8, device="cuda")
+    qd = torch.empty((e, h, i), dtype=torch.uint8, device="cuda")
+    sg = torch.empty((e, i // 128, h // 128), dtype=torch.float32, device="cuda")
+    su = torch.empty((e, i // 128, h // 128), dtype=torch.float32, device="cuda")
+    sd = torch.empty((e, h // 128, i // 128), dtype=torch.float32, device="cuda")
+    for x in range(e):
+        for which, (q, s) in enumerate(((qg, sg), (qu, su), (qd, sd))):
+            f = synth.expert_weight_device(w, layer, x, which)
+            moe.moe_quant_weight(f, q[x], s[x])
+    torch.cuda.synchronize()
+    return qg, sg, qu, su, qd, sd
+
+
+def oracle_expert_weights(w: synth.Workload, experts, layer: int = 0):
+    """Oracle-side weights of some experts: re-drawn in fp32, quantized by the oracle."""
+    res = {}
+    for x in experts:
+        mats = []
+        for which in range(3):
+            f = synth.expert_weight_device(w, layer, int(x), which).cpu().numpy()
+            mats += list(oracle.quantize_weight(f))
+        res[int(x)] = tuple(mats)
+    return res
+
+
+def oracle_tokens(x_bits, ids, wts, tokens, ow):
+    """Oracle output rows (bf16 bits) of some tokens, from per-expert weights ow."""
+    qx, sx = oracle.quant_act(x_bits[tokens])
+    k = ids.shape[1]
+    outs = []
+    for r, t in enumerate(tokens):
+        ys = []
+        for j in range(k):
+            qg, sg, qu, su, qd, sd = ow[int(ids[t, j])]
+            ys.append(oracle.expert_rows(qx[r:r + 1], sx[r:r + 1], qg, sg, qu, su, qd, sd)[0])
+        outs.append(oracle.combine(np.stack(ys), np.arange(k, dtype=np.int32), wts[t:t + 1])[0])
+    return np.stack(outs)
+
+
+def rel_err(got_f32: np.ndarray, ref_f32: np.ndarray) -> float:
+    den = float(np.max(np.abs(ref_f32)))
+    return float(np.max(np.abs(got_f32.astype(np.float64) - ref_f32))) / (den if den > 0 else 1.0)
+
+
+def bits_to_f32(t: torch.Tensor) -> np.ndarray:
+    return oracle.bf16_to_f32(t.cpu().numpy().view(np.uint16))
