@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Benchmark of one routed-expert FP8 MoE layer (DeepSeek-V3 shape) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload decode1]
+
+A step is one pass of the whole path over one batch already resident in
+HBM: moe_quant_act -> moe_permute -> moe_expert_ffn -> moe_combine.  The
+default workload is DeepSeek-V3-shaped decode with one token (hidden 7168,
+expert intermediate 2048, 256 experts, top-8, FP8 e4m3 weights with
+128x128 fp32 block scales, synthetic data).  Decode steps rotate over
+several independently drawn weight layers so that repeated steps cannot be
+served from the 256 MB Infinity Cache.
+
+Prints one JSON line: whole-job tokens/s, the roofline of the dominant
+kernel (timed live with HIP events on the stream it runs on) and the CPU
+oracle's throughput on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+FP8_PEAK_TFLOPS = 5000.0     # MI355X dense FP8 MFMA
+METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="decode1")
+    ap.add_argument("--layers", type=int, default=0, help="weight layers to rotate over (0: auto)")
+    ap.add_argument("--also", default="decode4", help="comma list of extra workloads (summary only)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def make_layer(moe, torch, synth, w, layer):
+    e, i, h = w.n_experts, w.inter, w.hidden
+    mats = []
+    for which, (n, k) in enumerate(((i, h), (i, h), (h, i))):
+        q = torch.empty((e, n, k), dtype=torch.uint8, device="cuda")
+        s = torch.empty((e, n // 128, k // 128), dtype=torch.float32, device="cuda")
+        for x in range(e):
+            moe.moe_quant_weight(synth.expert_weight_device(w, layer, x, which), q[x], s[x])
+        mats += [q, s]
+    torch.cuda.synchronize()
+    return tuple(mats)
+
+
+def algorithmic(w, ids):
+    """Per-call algorithmic work of the layer and of its kernels (see the design notes)."""
+    import numpy as np
+    t, k, h, i = w.tokens, w.topk, w.hidden, w.inter
+    r = t * k
+    n_act = int(np.unique(ids).size)
+    sc_gu = 2 * (i // 128) * (h // 128) * 4
+    sc_d = (h // 128) * (i // 128) * 4
+    return {
+        "active_experts": n_act,
+        "rows": r,
+        # decode gate/up kernel: touched W_gate + W_up + scales, gathered qx rows + sx, h written (fp32)
+        "gateup_bytes": n_act * (2 * i * h + sc_gu) + r * (h + (h // 128) * 4) + r * i * 4,
+        # decode down kernel: touched W_down + scales, qh rows + sh, y rows written (fp32)
+        "down_bytes": n_act * (h * i + sc_d) + r * (i + (i // 128) * 4) + r * h * 4,
+        "layer_weight_bytes": n_act * (3 * h * i + sc_gu + sc_d),
+        "gateup_flops": 2 * 2 * r * h * i,
+        "down_flops": 2 * r * h * i,
+    }
+
+
+def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache):
+    import numpy as np
+    w = synth.WORKLOADS[name]
+    if w.chunk_tokens:
+        raise SystemExit(f"{name}: the streamed workload is not benchmarked by this script yet")
+    x = synth.activations(w)
+    ids, wts = synth.routing(w)
+    dx = torch.from_numpy(x.view(np.int16)).cuda()
+    dids = torch.from_numpy(ids).cuda()
+    dw = torch.from_numpy(wts).cuda()
+    while len(layers_cache) < layers_n:
+        log(f"drawing and quantizing weight layer {len(layers_cache)} on the GPU")
+        layers_cache.append(make_layer(moe, torch, synth, w, len(layers_cache)))
+    layers = layers_cache[:layers_n]
+    buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, with_status=False)
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        moe.run_layer(buf, dx, dids, dw, layers[i % len(layers)], stream)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for i in range(steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+
+    # Per-kernel durations: the same steps again with the library's launch events.
+    moe.moe_profile_begin(16 * steps)
+    for i in range(steps):
+        step(i)
+    prof = moe.moe_profile_end()
+    torch.cuda.synchronize()
+    kern = {}
+    for kname, kms in prof:
+        kern.setdefault(kname, []).append(kms)
+    kern_us = {kname: 1000.0 * sum(v) / len(v) for kname, v in kern.items()}
+    out = buf.out.cpu().numpy()
+    if not np.all(np.isfinite((out.view(np.uint16).astype(np.uint32) << 16).view(np.float32))):
+        raise RuntimeError("non-finite output")
+    return w, ids, wts, x, ms, kern_us
+
+
+def cpu_baseline(torch, synth, w, x, ids, wts, budget_s):
+    """The oracle as it stands, on a bounded sample of the workload."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = os.cpu_count() or 1
+    k = w.topk
+    if w.tokens <= 64:
+        tokens = list(range(w.tokens))
+    else:
+        tokens = list(range(16))
+    experts = sorted(set(ids[tokens].reshape(-1).tolist()))
+    ow = {}
+    for e in experts:   # weight preparation (not timed): re-drawn fp32, quantized by the oracle
+        mats = []
+        for which in range(3):
+            f = synth.expert_weight_device(w, 0, e, which).cpu().numpy()
+            mats += list(oracle.quantize_weight(f))
+        ow[e] = tuple(mats)
+    done = 0
+    t0 = time.perf_counter()
+    while True:
+        qx, sx = oracle.quant_act(x[tokens])
+        sub_ids = ids[tokens]
+        offsets, src, dest = oracle.permute(sub_ids, w.n_experts)
+        y = np.zeros((len(tokens) * k, w.hidden), np.float32)
+        for e in experts:
+            p0, p1 = int(offsets[e]), int(offsets[e + 1])
+            if p1 > p0:
+                rows = src[p0:p1] // k
+                y[p0:p1] = oracle.expert_rows(qx[rows], sx[rows], *ow[e])
+        oracle.combine(y, dest, wts[tokens])
+        done += len(tokens)
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return {"value": done / el, "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
+            "sample": f"{len(tokens)} token(s) of the workload ({len(experts)} experts), full layer path "
+                      f"(quantize, permute, expert FFN, combine) repeated {done // len(tokens)} times "
+                      f"in {el:.1f} s; weight quantization excluded"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "the multi-GPU expert-parallel path is not built", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2606_10493_amd as moe
+    import synth
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+    w0 = synth.WORKLOADS[args.workload]
+    decode = w0.tokens <= moe.MOE_DECODE_MAX_TOKENS
+    layers_n = args.layers or (4 if decode else 1)
+    cache = []
+    w, ids, wts, x, ms, kern_us = time_workload(moe, torch, synth, args.workload, args.steps, args.warmup,
+                                                layers_n, cache)
+    alg = algorithmic(w, ids)
+    tok_s = w.tokens / (ms / 1000.0)
+    if decode:
+        dom = "ffn_decode_gateup"
+        us = kern_us[dom]
+        achieved = alg["gateup_bytes"] / (us * 1e-6) / 1e9
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "per_launch": {"algorithmic_bytes": alg["gateup_bytes"], "avg_us": round(us, 2)}}
+    else:
+        dom = "ffn_prefill_gateup"
+        us = kern_us[dom]
+        achieved = alg["gateup_flops"] / (us * 1e-6) / 1e12
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": FP8_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4), "traffic": None,
+                "per_launch": {"algorithmic_flops": alg["gateup_flops"], "avg_us": round(us, 2)}}
+    layer_gbs = alg["layer_weight_bytes"] / (ms * 1e-3) / 1e9
+    layer_tflops = (alg["gateup_flops"] + alg["down_flops"]) / (ms * 1e-3) / 1e12
+    also = {}
+    for extra in [a for a in args.also.split(",") if a and a != args.workload]:
+        try:
+            we, ide, _, _, mse, kue = time_workload(moe, torch, synth, extra, args.steps, args.warmup,
+                                                    layers_n, cache)
+        except SystemExit as exc:
+            also[extra] = {"skipped": str(exc)}
+            continue
+        ae = algorithmic(we, ide)
+        also[extra] = {"tokens_per_s": round(we.tokens / (mse / 1000.0), 1), "ms_per_step": round(mse, 4),
+                       "layer_weight_GBps": round(ae["layer_weight_bytes"] / (mse * 1e-3) / 1e9, 1),
+                       "active_experts": ae["active_experts"],
+                       "kernel_us": {kk: round(v, 2) for kk, v in kue.items()}}
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(torch, synth, w, x, ids, wts, args.cpu_seconds)
+    res = {
+        "metric": METRIC, "value": round(tok_s, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
+        "config": {"workload": args.workload, "hidden": w.hidden, "inter": w.inter, "n_experts": w.n_experts,
+                   "topk": w.topk, "tokens": w.tokens, "routing": w.routing,
+                   "weight_layers_rotated": layers_n, "active_experts": alg["active_experts"]},
+        "layer": {"weight_GBps": round(layer_gbs, 1), "frac_hbm": round(layer_gbs / HBM_PEAK_GBS, 4),
+                  "TFLOPs": round(layer_tflops, 2)},
+        "roofline": roof,
+        "kernel_us": {kk: round(v, 2) for kk, v in kern_us.items()},
+        "cpu_baseline": cpu,
+        "also": also,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -183,6 +183,19 @@ moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const flo
                          int32_t T, int32_t k, int32_t H, uint16_t* out_bf16,
                          hipStream_t stream);
 
+/*
+ * Diagnostics: per-launch kernel timing.  After moe_profile_begin(n), every
+ * kernel launch of the library (at most n) is bracketed by two HIP events
+ * recorded on its stream.  moe_profile_end() stops recording, waits for the
+ * recorded events and returns the number of launches; moe_profile_get(i)
+ * gives launch i's kernel name (static storage) and duration in ms.  The
+ * events are created by the library on the first begin and kept; use from
+ * one host thread at a time.
+ */
+moe_status_t moe_profile_begin(int32_t max_launches);
+int32_t moe_profile_end(void);
+moe_status_t moe_profile_get(int32_t i, float* ms, const char** name);
+
 #ifdef __cplusplus
 }
 #endif

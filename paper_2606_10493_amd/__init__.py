@@ -4,7 +4,7 @@ Thin Python binding of libmoe.so (the C ABI in include/moe.h).  Functions
 carry the C names and only marshal arguments: every step of the layer runs
 in the library's HIP kernels.  torch tensors supply device memory and
 streams; nothing here computes.  If libmoe.so is missing the import fails:
-build it with ``python -m paper_2606_10493_amd.build``.
+build it with ``python paper_2606_10493_amd/build.py``.
 """
 from __future__ import annotations
 
@@ -108,6 +108,22 @@ def moe_combine(y_rows, dest_row, topk_w, out_bf16, stream=None):
     H = out_bf16.shape[1]
     _check(lib.moe_combine(_ptr(y_rows), _ptr(dest_row), _ptr(topk_w), T, k, H, _ptr(out_bf16),
                            _stream(stream)))
+
+
+def moe_profile_begin(max_launches: int) -> None:
+    _check(lib.moe_profile_begin(max_launches))
+
+
+def moe_profile_end():
+    """Stop recording; returns [(kernel name, ms), ...] in launch order."""
+    n = lib.moe_profile_end()
+    out = []
+    for i in range(n):
+        ms = ctypes.c_float()
+        name = ctypes.c_char_p()
+        _check(lib.moe_profile_get(i, ctypes.byref(ms), ctypes.byref(name)))
+        out.append((name.value.decode(), float(ms.value)))
+    return out
 
 
 from .layer import MoELayerBuffers, run_layer  # noqa: E402,F401

@@ -33,7 +33,7 @@ class MoEError(RuntimeError):
 
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_10493_amd.build`")
+    raise ImportError(f"{LIB_PATH} is not built; run `python paper_2606_10493_amd/build.py`")
 
 lib = ctypes.CDLL(LIB_PATH)
 
@@ -53,6 +53,9 @@ _SIGS = {
     "moe_expert_ffn_workspace": (_S, [MoeDims, _I, _ST]),
     "moe_expert_ffn": (_ST, [MoeDims, _I, _ST, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "moe_combine": (_ST, [_P, _P, _P, _I, _I, _I, _P, _P]),
+    "moe_profile_begin": (_ST, [_I]),
+    "moe_profile_end": (_I, []),
+    "moe_profile_get": (_ST, [_I, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_char_p)]),
 }
 
 EXPORTED_SYMBOLS = tuple(_SIGS)

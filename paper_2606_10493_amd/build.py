@@ -1,6 +1,8 @@
 """Build libmoe.so (the HIP kernels and the C ABI) in-tree for gfx950.
 
-    python -m paper_2606_10493_amd.build
+    python paper_2606_10493_amd/build.py
+
+(run it by path: importing the package loads the library it builds).
 
 Every .hip file under csrc/ is compiled with hipcc in parallel and linked
 into paper_2606_10493_amd/libmoe.so.  It compiles on a machine without a

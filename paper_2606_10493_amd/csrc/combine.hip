@@ -57,7 +57,7 @@ extern "C" moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row
   const int bpt = (H + 1023) / 1024;
   const int64_t blocks = (int64_t)T * bpt;
   if (blocks > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_combine: too many tokens");
-  hipLaunchKernelGGL(combine_kernel, dim3((unsigned)blocks), dim3(128), 0, stream, y_rows, dest_row, topk_w, k, H,
+  MOE_LAUNCH("combine", combine_kernel, dim3((unsigned)blocks), dim3(128), 0, stream, y_rows, dest_row, topk_w, k, H,
                      bpt, out_bf16);
   return check_launch("moe_combine");
 }

@@ -85,6 +85,17 @@ __device__ __forceinline__ float silu_mul(float g, float u) {
 }
 
 // ----------------------------------------------------------------- host side
+void prof_before(hipStream_t s, const char* name);
+void prof_after(hipStream_t s);
+
+// Kernel launch bracketed by the optional per-launch timing events.
+#define MOE_LAUNCH(NAME, KERNEL, GRID, BLOCK, LDS, STREAM, ...)          \
+  do {                                                                  \
+    ::moe::prof_before((STREAM), (NAME));                               \
+    hipLaunchKernelGGL(KERNEL, GRID, BLOCK, LDS, STREAM, __VA_ARGS__);  \
+    ::moe::prof_after((STREAM));                                        \
+  } while (0)
+
 void set_error(const char* fmt, ...);
 moe_status_t fail(moe_status_t st, const char* fmt, ...);
 moe_status_t check_launch(const char* what);

@@ -13,14 +13,20 @@
 // Work item = (active expert, tile of 16*NT weight rows).  A 256-thread
 // workgroup (4 waves) splits K: wave w takes blocks b = w, w+4, ...; the
 // partial accumulators are summed through LDS in wave order (deterministic).
-// Every weight byte is read once, with each lane loading 32 contiguous bytes
-// of one row (16 rows x 128 bytes = 16 full cache lines per wave-load).
-// Token rows (at most 16*MT per pass) are gathered from the quantized
-// activations; rows beyond the expert's count are zero.
+// Every weight byte is read once, each lane loading 32 contiguous bytes of a
+// row (16 rows x 128 bytes = 16 full cache lines per wave-load).
+//
+// Latency is what limits a small GEMV, so the prologue before the first
+// weight load is short: every wave finds its expert with ballots over the
+// expert offsets (no LDS, no barrier), loads its token indices and then
+// issues a window of D K-blocks of weight fragments, gathered activation
+// fragments, weight scales and activation scales, all vector loads in one
+// in-order stream, so waiting for block j never waits for a later load.
 //
 // GATEUP: the tile holds the same 16*NT rows of W_gate and W_up, and the
-// epilogue writes h = SiLU(G) * U in fp32 (quantized per 128 by the next
-// launch).  Down: the epilogue writes the fp32 expert rows.
+// epilogue writes h = SiLU(G) * U in fp32.  Down: h is quantized per row per
+// 128 (QH: in this kernel's prologue, for at most kQhRows rows per expert;
+// else by a separate launch) and the epilogue writes the fp32 expert rows.
 #include "common.h"
 
 namespace moe {
@@ -39,60 +45,83 @@ struct DecodeArgs {
   const float* s1;
   int N, K;
   float* out;                 // fp32 [rows, N]
+  const float* hf;            // QH: fp32 h rows [rows, K] quantized in the prologue
 };
 
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int kMaxExperts = 1024;
+constexpr int kQhRows = 4;    // QH: rows of h quantized in the down kernel's prologue
+constexpr int kQhMaxK = 2048; // QH: 16 lane groups x 128 columns
 
-// Active experts (non-empty rows) in ascending id order, compacted in LDS.
-__device__ int list_active_experts(const int32_t* __restrict__ offsets, int E, int* active, int* wave_tot) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int base = 0;
-  for (int e0 = 0; e0 < E; e0 += 256) {
-    const int e = e0 + threadIdx.x;
-    const bool on = (e < E) && (offsets[e + 1] > offsets[e]);
-    const unsigned long long bal = __ballot(on);
-    const int before = __popcll(bal & ((1ull << lane) - 1ull));
-    if (lane == 0) wave_tot[wave] = __popcll(bal);
-    __syncthreads();
-    int off = base;
-    for (int w = 0; w < wave; ++w) off += wave_tot[w];
-    if (on) active[off + before] = e;
-    base += wave_tot[0] + wave_tot[1] + wave_tot[2] + wave_tot[3];
-    __syncthreads();
+// The a-th non-empty expert (or -1), the number of non-empty experts and the
+// expert's row range, found by one wave with ballots.  The offsets of 256
+// experts are loaded in one round trip (4 per lane + the end value), so the
+// lookup costs one L2 latency before the weight stream can start.
+struct ExpertRef {
+  int e, n_active, p0, m;
+};
+
+__device__ __forceinline__ ExpertRef find_expert(const int32_t* __restrict__ offsets, int E, int64_t a) {
+  const int lane = threadIdx.x & 63;
+  ExpertRef ref{-1, 0, 0, 0};
+  for (int c0 = 0; c0 < E; c0 += 256) {
+    int o[5];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int x = c0 + 64 * c + lane;
+      o[c] = x <= E ? offsets[x] : 0;
+    }
+    o[4] = offsets[min(c0 + 256, E)];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int x = c0 + 64 * c + lane;
+      const int nxt_first = c < 3 ? __shfl(o[c + 1], 0) : o[4];
+      const int up = __shfl_down(o[c], 1);
+      const int nxt = lane < 63 ? up : nxt_first;
+      const bool on = x < E && nxt > o[c];
+      const unsigned long long bal = __ballot(on);
+      const int cnt = __popcll(bal);
+      if (ref.e < 0 && a < ref.n_active + cnt) {
+        unsigned long long msk = bal;
+        for (int i = 0; i < (int)(a - ref.n_active); ++i) msk &= msk - 1ull;
+        const int bit = __ffsll((long long)msk) - 1;
+        ref.e = c0 + 64 * c + bit;
+        ref.p0 = __shfl(o[c], bit);
+        ref.m = __shfl(nxt, bit) - ref.p0;
+      }
+      ref.n_active += cnt;
+    }
   }
-  return base;
+  return ref;
 }
 
-template <int MT, int NT, bool GATEUP>
+template <int MT, int NT, bool GATEUP, bool QH, int U>
 __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
+  static_assert(!QH || (!GATEUP && MT == 1), "QH is the down projection with at most 16 rows");
   constexpr int G = GATEUP ? 2 : 1;
-  constexpr int kRows = 16 * MT;
-  extern __shared__ float smem[];
-  __shared__ int active[kMaxExperts];
-  __shared__ int wave_tot[kWaves];
-  __shared__ int tok[kRows];
+  constexpr int kPer = G * MT * NT * 4;
+  __shared__ float red[(kWaves - 1) * kPer * 64];
+  __shared__ __attribute__((aligned(16))) uint8_t qh_lds[QH ? kQhRows * kQhMaxK : 16];
+  __shared__ float sh_lds[QH ? kQhRows * (kQhMaxK / kBlock) : 1];
 
   const int nb = p.K / kBlock;
-  float* sa_lds = smem;                        // [kRows][nb]
-  float* red = smem + kRows * nb;              // [kWaves-1][G][MT][NT][4][64]
-
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15;   // row of the A / B fragment this lane loads
   const int kq = lane >> 4;  // 32-byte K slice of the block this lane loads
-
-  const int n_active = list_active_experts(p.offsets, p.E, active, wave_tot);
   const int tiles = p.N / (16 * NT);
-  const int64_t items = (int64_t)n_active * tiles;
+  const int nkw = (nb - wave + kWaves - 1) / kWaves;  // K blocks of this wave: wave, wave+4, ...
+
+  ExpertRef ref = find_expert(p.offsets, p.E, blockIdx.x / tiles);
+  const int64_t items = (int64_t)ref.n_active * tiles;
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
-    const int e = active[item / tiles];
+    if (item != blockIdx.x) ref = find_expert(p.offsets, p.E, item / tiles);
+    const int e = ref.e;
     const int n0 = (int)(item % tiles) * 16 * NT;
-    const int p0 = p.offsets[e];
-    const int M = p.offsets[e + 1] - p0;
+    const int p0 = ref.p0;
+    const int M = ref.m;
     const uint8_t* wrow0[NT];
     const uint8_t* wrow1[NT];
 #pragma unroll
@@ -102,31 +131,88 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       wrow1[nt] = GATEUP ? p.w1 + row * p.K + kq * 32 : nullptr;
     }
     const int64_t srow = ((int64_t)e * (p.N / kBlock) + n0 / kBlock) * nb;
-    const float* sw0 = p.s0 + srow;
-    const float* sw1 = GATEUP ? p.s1 + srow : nullptr;
 
-    for (int mb = 0; mb < M; mb += kRows) {
-      const int mc = min(M - mb, kRows);
-      for (int i = threadIdx.x; i < kRows; i += 256) {
-        int arow = -1;
-        if (i < mc) {
-          const int src = p.sorted_src ? p.sorted_src[p0 + mb + i] / p.topk : p0 + mb + i;
-          arow = (src >= 0 && src < p.a_rows) ? src : -1;
-        }
-        tok[i] = arow;
-      }
-      __syncthreads();
-      for (int i = threadIdx.x; i < kRows * nb; i += 256) {
-        const int m = i / nb, b = i - m * nb;
-        sa_lds[i] = tok[m] >= 0 ? p.sa[(int64_t)tok[m] * nb + b] : 0.0f;
-      }
-      const uint8_t* arow_ptr[MT];
+    for (int mb = 0; mb < M; mb += 16 * MT) {
+      const int mc = min(M - mb, 16 * MT);
+      // Activation rows this lane loads (row r of each sub-tile) and the rows
+      // whose outputs it holds (4*kq + i), or -1 beyond the expert's rows.
+      // All index loads are issued before any of them is used (clamped
+      // indices, no branches), so they cost one round trip together.
+      int ta[MT], ts[MT][4];
+      if (!QH) {
+        int raw[MT][5];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int t = tok[mt * 16 + r];
-        arow_ptr[mt] = t >= 0 ? p.a + (int64_t)t * p.K + kq * 32 : nullptr;
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int q = 0; q < 5; ++q) {
+            const int m = mt * 16 + (q == 0 ? r : 4 * kq + q - 1);
+            const int mm = m < mc ? m : mc - 1;
+            raw[mt][q] = p.sorted_src ? p.sorted_src[p0 + mb + mm] : p0 + mb + mm;
+          }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int q = 0; q < 5; ++q) {
+            const int m = mt * 16 + (q == 0 ? r : 4 * kq + q - 1);
+            const int src = p.sorted_src ? raw[mt][q] / p.topk : raw[mt][q];
+            const int v = (m < mc && src >= 0 && src < p.a_rows) ? src : -1;
+            if (q == 0) ta[mt] = v; else ts[mt][q - 1] = v;
+          }
       }
-      __syncthreads();
+
+      // QH: h values of this lane group (column block qgrp), loaded first.
+      const int qsub = threadIdx.x & 15, qgrp = threadIdx.x >> 4;
+      const int qcol = qgrp * kBlock + qsub * 8;
+      float hv[QH ? kQhRows : 1][8];
+      if (QH) {
+#pragma unroll
+        for (int q = 0; q < kQhRows; ++q) {
+          if (q < mc && qcol < p.K) {
+            const float* src = p.hf + (int64_t)(p0 + mb + q) * p.K + qcol;
+            const float4 x0 = *reinterpret_cast<const float4*>(src);
+            const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
+            hv[q][0] = x0.x; hv[q][1] = x0.y; hv[q][2] = x0.z; hv[q][3] = x0.w;
+            hv[q][4] = x1.x; hv[q][5] = x1.y; hv[q][6] = x1.z; hv[q][7] = x1.w;
+          } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) hv[q][i] = 0.0f;
+          }
+        }
+      }
+
+      auto load_w = [&](int bk, v8i (&w)[G][NT], float (&ws)[G]) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          w[0][nt] = load_v8i(wrow0[nt] + bk * kBlock);
+          if (GATEUP) w[G - 1][nt] = load_v8i(wrow1[nt] + bk * kBlock);
+        }
+        // Weight scales travel in the same in-order load stream as the weights.
+        ws[0] = p.s0[srow + bk];
+        if (GATEUP) ws[G - 1] = p.s1[srow + bk];
+      };
+
+      if (QH) {
+        // h rows of this expert -> e4m3 per 128 in LDS (same rule as moe_quant_rows_f32).
+#pragma unroll
+        for (int q = 0; q < kQhRows; ++q) {
+          if (q < mc && qcol < p.K) {
+            float amax = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(hv[q][i]));
+#pragma unroll
+            for (int sh = 8; sh >= 1; sh >>= 1) amax = fmaxf(amax, __shfl_xor(amax, sh, 16));
+            const float sc = amax / kE4M3Max;
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) lo |= quantize_e4m3(hv[q][i], sc) << (8 * i);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) hi |= quantize_e4m3(hv[q][4 + i], sc) << (8 * i);
+            *reinterpret_cast<uint2*>(qh_lds + q * kQhMaxK + qcol) = make_uint2(lo, hi);
+            if (qsub == 0) sh_lds[q * (kQhMaxK / kBlock) + qgrp] = sc;
+          }
+        }
+        __syncthreads();
+      }
 
       v4f acc[G][MT][NT];
 #pragma unroll
@@ -136,60 +222,47 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) acc[g][mt][nt] = v4f{0.f, 0.f, 0.f, 0.f};
 
-      v8i bcur[G][NT], bnext[G][NT];
-      int b = wave;
-      if (b < nb) {
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          bcur[0][nt] = load_v8i(wrow0[nt] + b * kBlock);
-          if (GATEUP) bcur[G - 1][nt] = load_v8i(wrow1[nt] + b * kBlock);
-        }
-      }
-      for (; b < nb; b += kWaves) {
-        const int bn = b + kWaves;
-        if (bn < nb) {
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
-            bnext[0][nt] = load_v8i(wrow0[nt] + bn * kBlock);
-            if (GATEUP) bnext[G - 1][nt] = load_v8i(wrow1[nt] + bn * kBlock);
-          }
-        }
-        v8i afrag[MT];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          if (arow_ptr[mt]) {
-            afrag[mt] = load_v8i(arow_ptr[mt] + b * kBlock);
-          } else {
-            afrag[mt] = v8i{0, 0, 0, 0, 0, 0, 0, 0};
-          }
-        }
+      // K loop: each block's loads are issued at the top of its iteration;
+      // the unrolled copies let the compiler hoist the next blocks' loads.
+#pragma unroll U
+      for (int j = 0; j < nkw; ++j) {
+        const int bk = wave + kWaves * j;
+        v8i w[G][NT];
         float ws[G];
-        ws[0] = sw0[b];
-        if (GATEUP) ws[G - 1] = sw1[b];
+        load_w(bk, w, ws);
+        v8i afrag[MT];
+        float sa[MT][4];
+        if (QH) {
+          // Rows beyond kQhRows read a valid LDS row; their outputs are never stored.
+          const int qr = r < kQhRows ? r : kQhRows - 1;
+          afrag[0] = *reinterpret_cast<const v8i*>(qh_lds + qr * kQhMaxK + bk * kBlock + kq * 32);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          float sa[4];
+          for (int i = 0; i < 4; ++i) {
+            const int row = 4 * kq + i;
+            sa[0][i] = row < kQhRows ? sh_lds[row * (kQhMaxK / kBlock) + bk] : 0.0f;
+          }
+        } else {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) sa[i] = sa_lds[(mt * 16 + 4 * kq + i) * nb + b];
+          for (int mt = 0; mt < MT; ++mt) {
+            afrag[mt] = ta[mt] >= 0 ? load_v8i(p.a + (int64_t)ta[mt] * p.K + bk * kBlock + kq * 32)
+                                    : v8i{0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) sa[mt][i] = ts[mt][i] >= 0 ? p.sa[(int64_t)ts[mt][i] * nb + bk] : 0.0f;
+          }
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
           for (int g = 0; g < G; ++g)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
-              const v4f part = mfma_f8_16x16x128(afrag[mt], bcur[g][nt]);
+              const v4f part = mfma_f8_16x16x128(afrag[mt], w[g][nt]);
 #pragma unroll
-              for (int i = 0; i < 4; ++i) acc[g][mt][nt][i] += part[i] * (sa[i] * ws[g]);
+              for (int i = 0; i < 4; ++i) acc[g][mt][nt][i] += part[i] * (sa[mt][i] * ws[g]);
             }
-        }
-        if (bn < nb) {
-#pragma unroll
-          for (int g = 0; g < G; ++g)
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) bcur[g][nt] = bnext[g][nt];
-        }
       }
 
       // Cross-wave reduction in wave order 0, 1, 2, 3.
-      constexpr int kPer = G * MT * NT * 4;
       if (wave > 0) {
         float* dst = red + (wave - 1) * kPer * 64;
         int q = 0;
@@ -236,14 +309,12 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   }
 }
 
-template <int MT, int NT, bool GATEUP>
+template <int MT, int NT, bool GATEUP, bool QH, int U>
 moe_status_t launch_decode(const DecodeArgs& a, int64_t max_items, hipStream_t stream) {
-  constexpr int G = GATEUP ? 2 : 1;
-  const int nb = a.K / kBlock;
-  const size_t lds = sizeof(float) * ((size_t)16 * MT * nb + (size_t)(kWaves - 1) * G * MT * NT * 4 * 64);
   const int64_t grid = max_items < 2048 ? max_items : 2048;
   if (grid <= 0) return MOE_OK;
-  hipLaunchKernelGGL((ffn_decode_kernel<MT, NT, GATEUP>), dim3((unsigned)grid), dim3(256), lds, stream, a);
+  MOE_LAUNCH(GATEUP ? "ffn_decode_gateup" : "ffn_decode_down", (ffn_decode_kernel<MT, NT, GATEUP, QH, U>),
+             dim3((unsigned)grid), dim3(256), 0, stream, a);
   return check_launch(GATEUP ? "ffn_decode_gateup" : "ffn_decode_down");
 }
 
@@ -264,23 +335,25 @@ moe_status_t run_ffn_decode(const moe_dims_t& d, int32_t T, const uint8_t* qx, c
   g.N = d.inter; g.K = d.hidden; g.out = h;
   moe_status_t st;
   const int64_t gu_items = max_active * (d.inter / 16);
-  if (T <= 16) st = launch_decode<1, 1, true>(g, gu_items, stream);
-  else if (T <= 32) st = launch_decode<2, 1, true>(g, gu_items, stream);
-  else st = launch_decode<4, 1, true>(g, gu_items, stream);
-  if (st != MOE_OK) return st;
-
-  st = moe_quant_rows_f32(h, (int32_t)R, d.inter, qh, sh, stream);
+  if (T <= 16) st = launch_decode<1, 1, true, false, 3>(g, gu_items, stream);
+  else if (T <= 32) st = launch_decode<2, 1, true, false, 2>(g, gu_items, stream);
+  else st = launch_decode<4, 1, true, false, 2>(g, gu_items, stream);
   if (st != MOE_OK) return st;
 
   DecodeArgs dn{};
   dn.a = qh; dn.sa = sh; dn.sorted_src = nullptr; dn.topk = d.topk; dn.a_rows = (int)R;
   dn.offsets = offsets; dn.E = d.n_experts;
   dn.w0 = w_down; dn.s0 = s_down; dn.w1 = nullptr; dn.s1 = nullptr;
-  dn.N = d.hidden; dn.K = d.inter; dn.out = y_rows;
+  dn.N = d.hidden; dn.K = d.inter; dn.out = y_rows; dn.hf = h;
   const int64_t dn_items = max_active * (d.hidden / 32);
-  if (T <= 16) return launch_decode<1, 2, false>(dn, dn_items, stream);
-  if (T <= 32) return launch_decode<2, 2, false>(dn, dn_items, stream);
-  return launch_decode<4, 2, false>(dn, dn_items, stream);
+  // Up to kQhRows tokens (so at most kQhRows rows per expert) the down kernel
+  // quantizes h itself; above that a separate launch writes qh, sh first.
+  if (T <= kQhRows && d.inter <= kQhMaxK) return launch_decode<1, 2, false, true, 4>(dn, dn_items, stream);
+  st = moe_quant_rows_f32(h, (int32_t)R, d.inter, qh, sh, stream);
+  if (st != MOE_OK) return st;
+  if (T <= 16) return launch_decode<1, 2, false, false, 4>(dn, dn_items, stream);
+  if (T <= 32) return launch_decode<2, 2, false, false, 2>(dn, dn_items, stream);
+  return launch_decode<4, 2, false, false, 2>(dn, dn_items, stream);
 }
 
 }  // namespace moe

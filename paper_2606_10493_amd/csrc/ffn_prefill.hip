@@ -296,7 +296,7 @@ moe_status_t launch_prefill(const PrefillArgs& a, int64_t max_mtiles, hipStream_
   const hipError_t ae = hipFuncSetAttribute(reinterpret_cast<const void*>(&ffn_prefill_kernel<GATEUP>),
                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (ae != hipSuccess) return fail(MOE_ERR_HIP, "ffn_prefill: LDS attribute: %s", hipGetErrorString(ae));
-  hipLaunchKernelGGL((ffn_prefill_kernel<GATEUP>), dim3((unsigned)grid), dim3(kThreads), lds, stream, a);
+  MOE_LAUNCH(GATEUP ? "ffn_prefill_gateup" : "ffn_prefill_down", (ffn_prefill_kernel<GATEUP>), dim3((unsigned)grid), dim3(kThreads), lds, stream, a);
   return check_launch(GATEUP ? "ffn_prefill_gateup" : "ffn_prefill_down");
 }
 
@@ -315,7 +315,7 @@ moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, 
   if (d.hidden % kBN) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "prefill regime needs H %% 256 == 0 (H=%d)", d.hidden);
   const int64_t R = (int64_t)T * d.topk;
   const int64_t max_mtiles = (R + kBM - 1) / kBM + (R < d.n_experts ? R : d.n_experts);
-  hipLaunchKernelGGL(prefill_tiles_kernel, dim3(1), dim3(1024), 0, stream, offsets, d.n_experts, tiles);
+  MOE_LAUNCH("prefill_tiles", prefill_tiles_kernel, dim3(1), dim3(1024), 0, stream, offsets, d.n_experts, tiles);
   moe_status_t st = check_launch("prefill_tiles");
   if (st != MOE_OK) return st;
 

@@ -270,7 +270,7 @@ extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t 
     return fail(MOE_ERR_INVALID_ARG, "moe_permute: null pointer");
   const int64_t nc = n_chunks_of(T);
   if (nc <= 1) {
-    hipLaunchKernelGGL(permute_small_kernel, dim3(1), dim3(256), 0, stream, topk_ids, T, k, E, expert_offsets,
+    MOE_LAUNCH("permute_small", permute_small_kernel, dim3(1), dim3(256), 0, stream, topk_ids, T, k, E, expert_offsets,
                        sorted_src, dest_row, dev_status);
     return check_launch("moe_permute");
   }
@@ -280,11 +280,11 @@ extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t 
   if (!aligned(ws, 4)) return fail(MOE_ERR_INVALID_ARG, "moe_permute: misaligned workspace");
   int32_t* counts = static_cast<int32_t*>(ws);
   int32_t* base = counts + nc * (E + 1);
-  hipLaunchKernelGGL(permute_count_kernel, dim3((unsigned)nc), dim3(256), 0, stream, topk_ids, T, k, E, counts,
+  MOE_LAUNCH("permute_count", permute_count_kernel, dim3((unsigned)nc), dim3(256), 0, stream, topk_ids, T, k, E, counts,
                      dev_status);
-  hipLaunchKernelGGL(permute_scan_kernel, dim3(1), dim3(1024), 0, stream, counts, (int)nc, E, base,
+  MOE_LAUNCH("permute_scan", permute_scan_kernel, dim3(1), dim3(1024), 0, stream, counts, (int)nc, E, base,
                      expert_offsets);
-  hipLaunchKernelGGL(permute_scatter_kernel, dim3((unsigned)nc), dim3(256), 0, stream, topk_ids, T, k, E, counts,
+  MOE_LAUNCH("permute_scatter", permute_scatter_kernel, dim3((unsigned)nc), dim3(256), 0, stream, topk_ids, T, k, E, counts,
                      base, sorted_src, dest_row);
   return check_launch("moe_permute");
 }

@@ -120,7 +120,7 @@ moe_status_t quant_rows(const InT* x, int32_t rows, int32_t cols, uint8_t* q, fl
   const int gpr = cols / kBlock;
   const int64_t n_groups = (int64_t)rows * gpr;
   const int64_t blocks = (n_groups + 15) / 16;
-  hipLaunchKernelGGL(quant_rows_kernel<InT>, dim3((unsigned)blocks), dim3(256), 0, stream, x, n_groups, gpr, q, s);
+  MOE_LAUNCH(name, quant_rows_kernel<InT>, dim3((unsigned)blocks), dim3(256), 0, stream, x, n_groups, gpr, q, s);
   return check_launch(name);
 }
 
@@ -152,6 +152,6 @@ extern "C" moe_status_t moe_quant_weight(const float* w, int32_t n_mats, int32_t
     return fail(MOE_ERR_INVALID_ARG, "moe_quant_weight: misaligned pointer");
   const int64_t blocks = (int64_t)n_mats * (rows / kBlock) * (cols / kBlock);
   if (blocks > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_quant_weight: too many blocks");
-  hipLaunchKernelGGL(quant_weight_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, w, rows, cols, q, s);
+  MOE_LAUNCH("quant_weight", quant_weight_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, w, rows, cols, q, s);
   return check_launch("moe_quant_weight");
 }
