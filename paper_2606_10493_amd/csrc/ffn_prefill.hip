@@ -76,6 +76,10 @@ __global__ __launch_bounds__(1024) void prefill_tiles_kernel(const int32_t* __re
   if (e == 0) mtile_start[E] = tmp[1023];
 }
 
+__device__ __forceinline__ uint4 and4(uint4 v, uint32_t m) {
+  return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+}
+
 template <bool GATEUP>
 __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -123,14 +127,18 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 
   // Global -> LDS copy assignment: A = 1024 16-byte chunks (2 per thread),
   // B = 2048 chunks (4 per thread); chunk c covers row c/8, bytes 16*(c%8).
+  // Rows beyond the expert (or with a bad index) load a valid row and are
+  // zeroed after the load, which keeps every load a plain global load.
   const uint8_t* a_src[2];
+  uint32_t a_mask[2];
   int a_dst[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int c = tid + i * kThreads;
     const int row = c >> 3, col = (c & 7) * 16;
     const int ar = arow[row];
-    a_src[i] = ar >= 0 ? p.a + (int64_t)ar * p.K + col : nullptr;
+    a_mask[i] = ar >= 0 ? 0xffffffffu : 0u;
+    a_src[i] = p.a + (int64_t)(ar >= 0 ? ar : 0) * p.K + col;
     a_dst[i] = row * kLdsRow + col;
   }
   const uint8_t* b_src[4];
@@ -172,29 +180,43 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  uint4 ra[2], rb[4];
-  auto gload = [&](int b) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      ra[i] = a_src[i] ? *reinterpret_cast<const uint4*>(a_src[i] + b * kBlock) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) rb[i] = *reinterpret_cast<const uint4*>(b_src[i] + b * kBlock);
-  };
-  auto lstore = [&](int stage) {
-    uint8_t* s = smem + stage * kStage;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) *reinterpret_cast<uint4*>(s + a_dst[i]) = ra[i];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) *reinterpret_cast<uint4*>(s + b_dst[i]) = rb[i];
-  };
+  // Staging registers of one K block (global -> registers -> LDS).  Plain
+  // scalars, fully unrolled, so they stay in VGPRs.
+  uint4 ra0, ra1, rb0, rb1, rb2, rb3;
+#define MOE_PF_GLOAD(BLK)                                                                            \
+  do {                                                                                               \
+    const int off_ = (BLK) * kBlock;                                                                 \
+    ra0 = *reinterpret_cast<const uint4*>(a_src[0] + off_);                                          \
+    ra1 = *reinterpret_cast<const uint4*>(a_src[1] + off_);                                          \
+    rb0 = *reinterpret_cast<const uint4*>(b_src[0] + off_);                                          \
+    rb1 = *reinterpret_cast<const uint4*>(b_src[1] + off_);                                          \
+    rb2 = *reinterpret_cast<const uint4*>(b_src[2] + off_);                                          \
+    rb3 = *reinterpret_cast<const uint4*>(b_src[3] + off_);                                          \
+  } while (0)
+#define MOE_PF_LSTORE(STAGE)                                                                         \
+  do {                                                                                               \
+    uint8_t* st_ = smem + (STAGE) * kStage;                                                          \
+    *reinterpret_cast<uint4*>(st_ + a_dst[0]) = and4(ra0, a_mask[0]);                                \
+    *reinterpret_cast<uint4*>(st_ + a_dst[1]) = and4(ra1, a_mask[1]);                                \
+    *reinterpret_cast<uint4*>(st_ + b_dst[0]) = rb0;                                                 \
+    *reinterpret_cast<uint4*>(st_ + b_dst[1]) = rb1;                                                 \
+    *reinterpret_cast<uint4*>(st_ + b_dst[2]) = rb2;                                                 \
+    *reinterpret_cast<uint4*>(st_ + b_dst[3]) = rb3;                                                 \
+  } while (0)
 
-  gload(0);
-  lstore(0);
+  MOE_PF_GLOAD(0);
+  MOE_PF_LSTORE(0);
   __syncthreads();
 
   for (int b = 0; b < nb; ++b) {
     const int stage = b & 1;
-    if (b + 1 < nb) gload(b + 1);
+    // The next block's global loads go out first; scheduling barriers keep
+    // them above the math and keep the LDS store of the next stage below it,
+    // so their latency overlaps this block's MFMAs.  The body is one basic
+    // block: the last step re-loads its own block and stores it into the
+    // stage nobody reads any more.
+    MOE_PF_GLOAD(b + 1 < nb ? b + 1 : b);
+    __builtin_amdgcn_sched_barrier(0);
     const uint8_t* sA = smem + stage * kStage;
     const uint8_t* sB = sA + kStageA;
     v8i af[4], bf[4];
@@ -217,9 +239,12 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
         for (int q = 0; q < 4; ++q) acc[i][j][q] += part[q] * (sa[q] * sw[j]);
       }
     }
-    if (b + 1 < nb) lstore(stage ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    MOE_PF_LSTORE(stage ^ 1);
     __syncthreads();
   }
+#undef MOE_PF_GLOAD
+#undef MOE_PF_LSTORE
 
   if (!GATEUP) {
     // y[m0 + row, nt*256 + col]; lane holds rows 4*kq+q of each 16x16 sub-tile, column r.
