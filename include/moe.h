@@ -184,6 +184,50 @@ moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const flo
                          hipStream_t stream);
 
 /*
+ * Stream-loaded layer (System Design, Stream-loading Prefill: a loader
+ * stages each expert's weights from host memory into a device experts ring
+ * buffer and sets an ON event, the model waits for ON, runs the expert and
+ * sets an OFF event, and the slot is reused without copying back).
+ *
+ * The whole layer (quantize, permute, expert FFN, combine) with the expert
+ * weights in pinned host memory.  Expert e is copied on `copy` into ring
+ * slot e % ring_slots (waiting for that slot's previous expert to finish),
+ * then run on `compute` over every chunk's rows of e as soon as its copy
+ * lands.  Tokens are permuted and combined per chunk of chunk_tokens.  Each
+ * output row equals moe_expert_ffn with MOE_REGIME_PREFILL on resident
+ * weights bit for bit (same kernels, same per-row arithmetic).
+ *
+ * host_w_*: pinned host e4m3 weights, layouts as moe_expert_ffn ([E,I,H]
+ * for gate/up, [E,H,I] for down); host_s_*: pinned host fp32 scales.
+ * dev_ring: device, moe_ring_bytes(dims, slots) bytes, three sub-rings
+ * [slots][I*H] of W_gate, W_up and [slots][H*I] of W_down (slot s holds one
+ * expert in each).  dev_ring_scales: device, moe_ring_scale_bytes(dims,
+ * slots) bytes, the same three sub-rings of scales.  Experts are copied and
+ * run in groups of consecutive experts (a divisor of the slot count) so
+ * that each launch fills the GPU.  ctx: from moe_stream_ctx_create
+ * with the same slot count (its events order the slots; one call at a time
+ * per ctx).  x_bf16, topk_ids, topk_w, out_bf16 as in the other calls (device).
+ * ws: device, moe_ffn_streamed_workspace(dims, T, chunk_tokens) bytes, 256-byte
+ * aligned (it holds the fp32 expert rows of all T*k slots).  compute and copy
+ * should be distinct streams for the copies to overlap the kernels.
+ * Requires H % 256 == 0.
+ */
+typedef struct moe_stream_ctx* moe_stream_ctx_t;
+moe_status_t moe_stream_ctx_create(int32_t ring_slots, moe_stream_ctx_t* out);
+void moe_stream_ctx_destroy(moe_stream_ctx_t ctx);
+size_t moe_ring_bytes(moe_dims_t dims, int32_t ring_slots);
+size_t moe_ring_scale_bytes(moe_dims_t dims, int32_t ring_slots);
+size_t moe_ffn_streamed_workspace(moe_dims_t dims, int32_t T, int32_t chunk_tokens);
+moe_status_t moe_ffn_streamed(moe_dims_t dims, int32_t T, int32_t chunk_tokens, const uint16_t* x_bf16,
+                              const int32_t* topk_ids, const float* topk_w,
+                              const uint8_t* host_w_gate, const float* host_s_gate,
+                              const uint8_t* host_w_up, const float* host_s_up,
+                              const uint8_t* host_w_down, const float* host_s_down,
+                              uint8_t* dev_ring, float* dev_ring_scales, moe_stream_ctx_t ctx,
+                              uint16_t* out_bf16, int32_t* dev_status, void* ws, size_t ws_bytes,
+                              hipStream_t compute, hipStream_t copy);
+
+/*
  * Diagnostics: per-launch kernel timing.  After moe_profile_begin(n), every
  * kernel launch of the library (at most n) is bracketed by two HIP events
  * recorded on its stream.  moe_profile_end() stops recording, waits for the

@@ -110,6 +110,67 @@ def moe_combine(y_rows, dest_row, topk_w, out_bf16, stream=None):
                            _stream(stream)))
 
 
+class StreamContext:
+    """Owns the per-slot ON/OFF events of moe_ffn_streamed (created once, at setup)."""
+
+    def __init__(self, ring_slots: int):
+        h = ctypes.c_void_p()
+        _check(lib.moe_stream_ctx_create(ring_slots, ctypes.byref(h)))
+        self.handle = h
+        self.slots = ring_slots
+
+    def close(self):
+        if self.handle:
+            lib.moe_stream_ctx_destroy(self.handle)
+            self.handle = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:  # interpreter shutdown
+            pass
+
+
+def moe_ring_bytes(dims: MoeDims, ring_slots: int) -> int:
+    return int(lib.moe_ring_bytes(dims, ring_slots))
+
+
+def moe_ring_scale_bytes(dims: MoeDims, ring_slots: int) -> int:
+    return int(lib.moe_ring_scale_bytes(dims, ring_slots))
+
+
+def moe_ffn_streamed_workspace(dims: MoeDims, T: int, chunk_tokens: int) -> int:
+    return int(lib.moe_ffn_streamed_workspace(dims, T, chunk_tokens))
+
+
+def _need_pinned(t, dtype_bytes, name):
+    if t.is_cuda or not t.is_pinned():
+        raise ValueError(f"{name} must be a pinned host tensor")
+    if not t.is_contiguous() or t.element_size() != dtype_bytes:
+        raise ValueError(f"{name} must be contiguous with element size {dtype_bytes}")
+
+
+def moe_ffn_streamed(dims: MoeDims, chunk_tokens: int, x_bf16, topk_ids, topk_w, host_weights, dev_ring,
+                     dev_ring_scales, ctx: "StreamContext", out_bf16, dev_status, ws, compute_stream=None,
+                     copy_stream=None):
+    """host_weights = (w_gate, s_gate, w_up, s_up, w_down, s_down) pinned host tensors."""
+    T = x_bf16.shape[0]
+    _need(x_bf16, 2, "x_bf16"); _need(topk_ids, 4, "topk_ids"); _need(topk_w, 4, "topk_w")
+    _need(dev_ring, 1, "dev_ring"); _need(dev_ring_scales, 4, "dev_ring_scales")
+    _need(out_bf16, 2, "out_bf16"); _need(dev_status, 4, "dev_status"); _need(ws, 1, "ws")
+    for t, nb, n in zip(host_weights, (1, 4, 1, 4, 1, 4),
+                        ("host_w_gate", "host_s_gate", "host_w_up", "host_s_up", "host_w_down", "host_s_down")):
+        _need_pinned(t, nb, n)
+    if dev_ring.numel() < moe_ring_bytes(dims, ctx.slots):
+        raise ValueError("dev_ring is smaller than moe_ring_bytes(dims, ctx.slots)")
+    if dev_ring_scales.numel() * 4 < moe_ring_scale_bytes(dims, ctx.slots):
+        raise ValueError("dev_ring_scales is smaller than moe_ring_scale_bytes(dims, ctx.slots)")
+    hw = [_ptr(t) for t in host_weights]
+    _check(lib.moe_ffn_streamed(dims, T, chunk_tokens, _ptr(x_bf16), _ptr(topk_ids), _ptr(topk_w), *hw,
+                                _ptr(dev_ring), _ptr(dev_ring_scales), ctx.handle, _ptr(out_bf16), _ptr(dev_status),
+                                _ptr(ws), _nbytes(ws), _stream(compute_stream), _stream(copy_stream)))
+
+
 def moe_profile_begin(max_launches: int) -> None:
     _check(lib.moe_profile_begin(max_launches))
 

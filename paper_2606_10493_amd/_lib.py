@@ -53,6 +53,13 @@ _SIGS = {
     "moe_expert_ffn_workspace": (_S, [MoeDims, _I, _ST]),
     "moe_expert_ffn": (_ST, [MoeDims, _I, _ST, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "moe_combine": (_ST, [_P, _P, _P, _I, _I, _I, _P, _P]),
+    "moe_stream_ctx_create": (_ST, [_I, ctypes.POINTER(ctypes.c_void_p)]),
+    "moe_stream_ctx_destroy": (None, [_P]),
+    "moe_ring_bytes": (_S, [MoeDims, _I]),
+    "moe_ring_scale_bytes": (_S, [MoeDims, _I]),
+    "moe_ffn_streamed_workspace": (_S, [MoeDims, _I, _I]),
+    "moe_ffn_streamed": (_ST, [MoeDims, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S,
+                                _P, _P]),
     "moe_profile_begin": (_ST, [_I]),
     "moe_profile_end": (_I, []),
     "moe_profile_get": (_ST, [_I, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_char_p)]),

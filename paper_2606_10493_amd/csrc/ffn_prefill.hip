@@ -21,9 +21,11 @@
 // Work items are (expert m-tile, n-tile) pairs; m-tiles of all experts are
 // numbered by an exclusive scan of ceil(M_e / 128) (prefill_tiles_kernel).
 // Work items are assigned XCD-major: the hardware deals workgroups to the 8
-// XCDs round-robin, so item = (block % 8) * (grid / 8) + block / 8 keeps the
-// n-tiles of one m-tile (which share the gathered activation rows) and the
-// m-tiles of one expert (which share weights) on one XCD's L2.
+// XCDs round-robin, so with n real items (read from the tile scan; the grid
+// is only an upper bound) item = (block % 8) * ceil(n / 8) + block / 8
+// keeps the n-tiles of one m-tile (which share the gathered activation
+// rows) and the m-tiles of one expert (which share weights) on one XCD's L2
+// while every XCD gets an equal share.
 #include "common.h"
 
 namespace moe {
@@ -91,13 +93,16 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   const int wm = wave >> 2, wn = wave & 3;
   const int r = lane & 15, kq = lane >> 4;
 
-  // XCD-major work item.
-  const int64_t grid = gridDim.x;
-  const int64_t item = (grid % kXcd == 0) ? (int64_t)(blockIdx.x % kXcd) * (grid / kXcd) + blockIdx.x / kXcd
-                                          : (int64_t)blockIdx.x;
+  // XCD-major work item over the real items (the grid is an upper bound):
+  // XCD x takes items [x*per, (x+1)*per) in order.
+  const int64_t real = (int64_t)p.mtile_start[p.E] * p.n_tiles;
+  const int64_t per = (real + kXcd - 1) / kXcd;
+  const int64_t slot = blockIdx.x / kXcd;
+  if (slot >= per) return;
+  const int64_t item = (int64_t)(blockIdx.x % kXcd) * per + slot;
+  if (item >= real) return;
   const int64_t mt_global = item / p.n_tiles;
   const int nt = (int)(item % p.n_tiles);
-  if (mt_global >= p.mtile_start[p.E]) return;
   // Expert owning this m-tile: last e with mtile_start[e] <= mt_global.
   int lo = 0, hi = p.E - 1;
   while (lo < hi) {
@@ -332,20 +337,21 @@ size_t prefill_tile_workspace(const moe_dims_t& d, int32_t T) {
   return sizeof(int32_t) * (size_t)(d.n_experts + 1);
 }
 
-moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, const float* sx,
-                             const int32_t* offsets, const int32_t* sorted_src, const uint8_t* w_gate,
-                             const float* s_gate, const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
-                             const float* s_down, float* y_rows, uint8_t* qh, float* sh, int32_t* tiles,
-                             hipStream_t stream) {
+// Gate/up then down over the expert-sorted rows described by offsets[0..E].
+// max_mtiles bounds the number of 128-row tiles over all experts (it sizes
+// the grid); a_rows is the number of activation rows (tokens).
+moe_status_t run_ffn_prefill_view(const moe_dims_t& d, int64_t max_mtiles, int32_t a_rows, const uint8_t* qx,
+                                  const float* sx, const int32_t* offsets, const int32_t* sorted_src,
+                                  const uint8_t* w_gate, const float* s_gate, const uint8_t* w_up, const float* s_up,
+                                  const uint8_t* w_down, const float* s_down, float* y_rows, uint8_t* qh, float* sh,
+                                  int32_t* tiles, hipStream_t stream) {
   if (d.hidden % kBN) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "prefill regime needs H %% 256 == 0 (H=%d)", d.hidden);
-  const int64_t R = (int64_t)T * d.topk;
-  const int64_t max_mtiles = (R + kBM - 1) / kBM + (R < d.n_experts ? R : d.n_experts);
   MOE_LAUNCH("prefill_tiles", prefill_tiles_kernel, dim3(1), dim3(1024), 0, stream, offsets, d.n_experts, tiles);
   moe_status_t st = check_launch("prefill_tiles");
   if (st != MOE_OK) return st;
 
   PrefillArgs g{};
-  g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = T;
+  g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = a_rows;
   g.offsets = offsets; g.mtile_start = tiles; g.E = d.n_experts;
   g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
   g.N = d.inter; g.K = d.hidden; g.n_tiles = d.inter / kBlock;
@@ -354,12 +360,23 @@ moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, 
   if (st != MOE_OK) return st;
 
   PrefillArgs dn{};
-  dn.a = qh; dn.sa = sh; dn.sorted_src = nullptr; dn.topk = d.topk; dn.a_rows = (int)R;
+  dn.a = qh; dn.sa = sh; dn.sorted_src = nullptr; dn.topk = d.topk; dn.a_rows = (int)((int64_t)a_rows * d.topk);
   dn.offsets = offsets; dn.mtile_start = tiles; dn.E = d.n_experts;
   dn.w0 = w_down; dn.s0 = s_down; dn.w1 = nullptr; dn.s1 = nullptr;
   dn.N = d.hidden; dn.K = d.inter; dn.n_tiles = d.hidden / kBN;
   dn.y = y_rows; dn.qh = nullptr; dn.sh = nullptr;
   return launch_prefill<false>(dn, max_mtiles, stream);
+}
+
+moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, const float* sx,
+                             const int32_t* offsets, const int32_t* sorted_src, const uint8_t* w_gate,
+                             const float* s_gate, const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
+                             const float* s_down, float* y_rows, uint8_t* qh, float* sh, int32_t* tiles,
+                             hipStream_t stream) {
+  const int64_t R = (int64_t)T * d.topk;
+  const int64_t max_mtiles = (R + kBM - 1) / kBM + (R < d.n_experts ? R : d.n_experts);
+  return run_ffn_prefill_view(d, max_mtiles, T, qx, sx, offsets, sorted_src, w_gate, s_gate, w_up, s_up, w_down,
+                              s_down, y_rows, qh, sh, tiles, stream);
 }
 
 }  // namespace moe

@@ -1,0 +1,247 @@
+// Stream-loading of one routed-expert layer whose FP8 weights stay in pinned
+// host memory (the paper's stream-loading prefill, System Design: a loader
+// stages each expert's weights into an experts ring buffer on the device and
+// signals an ON event; the model runs the expert after waiting for it and
+// signals an OFF event; the slot is then reused without copying anything
+// back, the host copy being authoritative).
+//
+// MI355X form: one host thread enqueues everything.  The loader is a copy
+// stream issuing hipMemcpyAsync from pinned host memory into the ring; the
+// model is the caller's compute stream; ON/OFF are HIP events per group of
+// slots (stream-ordered, so the paper's host-side threading events are not
+// needed).  Experts go in groups of G consecutive experts held in G
+// consecutive slots (the ring is three sub-rings, gate | up | down, each
+// [R][matrix], so a group looks like a small weight tensor to the kernels).
+// G is the largest divisor of R that gives about 2048 rows per launch, so a
+// launch fills the GPU.  Enqueue order per group g (slot group v = g mod R/G):
+//   copy:    [wait OFF[v] if g >= R/G]  6 copies (W, S of gate/up/down)  record ON[v]
+//   compute: wait ON[v]  FFN(group) over every chunk's rows           record OFF[v]
+// Because copy(g) is enqueued after compute(g - R/G) and compute(g) after
+// copy(g), every wait refers to the intended record.
+//
+// Tokens: all T are quantized at once; the permutation, the expert FFN and
+// the combine work per chunk of chunk_tokens tokens.  The FFN of a group on
+// chunk c reads a G-expert view of chunk c's offsets (offsets pointer + e0),
+// so the kernels and every row's arithmetic are those of the resident path:
+// each output row is bit-identical to moe_expert_ffn with the prefill regime.
+#include <vector>
+
+#include "common.h"
+
+struct moe_stream_ctx {
+  int32_t slots;
+  std::vector<hipEvent_t> on, off;
+};
+
+namespace moe {
+
+moe_status_t run_ffn_prefill_view(const moe_dims_t& d, int64_t max_mtiles, int32_t a_rows, const uint8_t* qx,
+                                  const float* sx, const int32_t* offsets, const int32_t* sorted_src,
+                                  const uint8_t* w_gate, const float* s_gate, const uint8_t* w_up, const float* s_up,
+                                  const uint8_t* w_down, const float* s_down, float* y_rows, uint8_t* qh, float* sh,
+                                  int32_t* tiles, hipStream_t stream);
+
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct StreamLayout {
+  size_t qx, sx, offsets, sorted_src, dest_row, perm_ws, qh, sh, tiles, y, total;
+  int64_t n_chunks, chunk;
+};
+
+StreamLayout layout(const moe_dims_t& d, int32_t T, int32_t chunk_tokens) {
+  StreamLayout L{};
+  const int64_t H = d.hidden, I = d.inter, E = d.n_experts, k = d.topk;
+  L.chunk = chunk_tokens;
+  L.n_chunks = (T + chunk_tokens - 1) / chunk_tokens;
+  const int64_t ck = (int64_t)chunk_tokens * k;  // rows of one chunk
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align256(bytes);
+    return at;
+  };
+  L.qx = take((size_t)T * H);
+  L.sx = take((size_t)T * (H / kBlock) * sizeof(float));
+  L.offsets = take((size_t)L.n_chunks * (E + 1) * sizeof(int32_t));
+  L.sorted_src = take((size_t)L.n_chunks * ck * sizeof(int32_t));
+  L.dest_row = take((size_t)L.n_chunks * ck * sizeof(int32_t));
+  L.perm_ws = take(moe_permute_workspace(chunk_tokens, d.topk, d.n_experts));
+  L.qh = take((size_t)ck * I);
+  L.sh = take((size_t)ck * (I / kBlock) * sizeof(float));
+  L.tiles = take((size_t)(E + 1) * sizeof(int32_t));
+  L.y = take((size_t)T * k * H * sizeof(float));
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+}  // namespace moe
+
+using namespace moe;
+
+extern "C" size_t moe_ring_bytes(moe_dims_t d, int32_t slots) {
+  if (slots < 1 || d.hidden <= 0 || d.inter <= 0) return 0;
+  return (size_t)slots * 3 * (size_t)d.hidden * d.inter;
+}
+
+extern "C" size_t moe_ring_scale_bytes(moe_dims_t d, int32_t slots) {
+  if (slots < 1 || d.hidden <= 0 || d.inter <= 0) return 0;
+  return (size_t)slots * 3 * (size_t)(d.hidden / kBlock) * (d.inter / kBlock) * sizeof(float);
+}
+
+extern "C" moe_status_t moe_stream_ctx_create(int32_t ring_slots, moe_stream_ctx_t* out) {
+  if (!out || ring_slots < 1 || ring_slots > 4096)
+    return fail(MOE_ERR_INVALID_ARG, "moe_stream_ctx_create: ring_slots=%d", ring_slots);
+  *out = nullptr;
+  moe_stream_ctx* c = new moe_stream_ctx;
+  c->slots = ring_slots;
+  c->on.resize(ring_slots);
+  c->off.resize(ring_slots);
+  for (int i = 0; i < ring_slots; ++i) {
+    if (hipEventCreateWithFlags(&c->on[i], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&c->off[i], hipEventDisableTiming) != hipSuccess) {
+      for (int j = 0; j <= i; ++j) {
+        if (c->on[j]) (void)hipEventDestroy(c->on[j]);
+        if (c->off[j]) (void)hipEventDestroy(c->off[j]);
+      }
+      delete c;
+      return fail(MOE_ERR_HIP, "moe_stream_ctx_create: hipEventCreate failed");
+    }
+  }
+  *out = c;
+  return MOE_OK;
+}
+
+extern "C" void moe_stream_ctx_destroy(moe_stream_ctx_t ctx) {
+  if (!ctx) return;
+  for (auto e : ctx->on) (void)hipEventDestroy(e);
+  for (auto e : ctx->off) (void)hipEventDestroy(e);
+  delete ctx;
+}
+
+extern "C" size_t moe_ffn_streamed_workspace(moe_dims_t d, int32_t T, int32_t chunk_tokens) {
+  if (T < 0 || chunk_tokens < 1 || d.hidden <= 0 || d.inter <= 0 || d.n_experts <= 0 || d.topk <= 0) return 0;
+  return layout(d, T, chunk_tokens).total;
+}
+
+extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_tokens, const uint16_t* x_bf16,
+                                         const int32_t* topk_ids, const float* topk_w, const uint8_t* host_w_gate,
+                                         const float* host_s_gate, const uint8_t* host_w_up, const float* host_s_up,
+                                         const uint8_t* host_w_down, const float* host_s_down, uint8_t* dev_ring,
+                                         float* dev_ring_scales, moe_stream_ctx_t ctx, uint16_t* out_bf16,
+                                         int32_t* dev_status, void* ws, size_t ws_bytes, hipStream_t compute,
+                                         hipStream_t copy) {
+  if (d.hidden <= 0 || d.inter <= 0 || d.n_experts < 1 || d.n_experts > 1024 || d.topk < 1 || d.topk > 32 ||
+      d.topk > d.n_experts || T < 0 || chunk_tokens < 1)
+    return fail(MOE_ERR_INVALID_ARG, "moe_ffn_streamed: H=%d I=%d E=%d k=%d T=%d chunk=%d", d.hidden, d.inter,
+                d.n_experts, d.topk, T, chunk_tokens);
+  if (d.hidden % 256 || d.inter % kBlock)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_ffn_streamed: H must be a multiple of 256 and I of 128");
+  if (!ctx) return fail(MOE_ERR_INVALID_ARG, "moe_ffn_streamed: null stream context");
+  if (T == 0) return MOE_OK;
+  if ((int64_t)T * d.topk > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_ffn_streamed: T*k overflows");
+  if (!x_bf16 || !topk_ids || !topk_w || !host_w_gate || !host_s_gate || !host_w_up || !host_s_up || !host_w_down ||
+      !host_s_down || !dev_ring || !dev_ring_scales || !out_bf16)
+    return fail(MOE_ERR_INVALID_ARG, "moe_ffn_streamed: null pointer");
+  if (!aligned(dev_ring, 16) || !aligned(x_bf16, 16) || !aligned(out_bf16, 16) || !aligned(ws, 256))
+    return fail(MOE_ERR_INVALID_ARG, "moe_ffn_streamed: misaligned pointer");
+  const StreamLayout L = layout(d, T, chunk_tokens);
+  if (!ws || ws_bytes < L.total)
+    return fail(MOE_ERR_WORKSPACE, "moe_ffn_streamed: workspace %zu bytes < %zu", ws_bytes, L.total);
+
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  uint8_t* qx = base + L.qx;
+  float* sx = reinterpret_cast<float*>(base + L.sx);
+  int32_t* offsets = reinterpret_cast<int32_t*>(base + L.offsets);
+  int32_t* sorted_src = reinterpret_cast<int32_t*>(base + L.sorted_src);
+  int32_t* dest_row = reinterpret_cast<int32_t*>(base + L.dest_row);
+  void* perm_ws = base + L.perm_ws;
+  uint8_t* qh = base + L.qh;
+  float* sh = reinterpret_cast<float*>(base + L.sh);
+  int32_t* tiles = reinterpret_cast<int32_t*>(base + L.tiles);
+  float* y = reinterpret_cast<float*>(base + L.y);
+
+  const int64_t H = d.hidden, I = d.inter, E = d.n_experts, k = d.topk;
+  const size_t wmat = (size_t)I * H;                                   // bytes of one expert matrix
+  const size_t smat = (size_t)(I / kBlock) * (H / kBlock);             // scales of one expert matrix
+  const int R = ctx->slots;
+
+  // Quantize every token, then permute each chunk (compute stream).
+  moe_status_t st = moe_quant_act(x_bf16, T, d.hidden, qx, sx, compute);
+  if (st != MOE_OK) return st;
+  const size_t perm_ws_bytes = moe_permute_workspace(chunk_tokens, d.topk, d.n_experts);
+  for (int64_t c = 0; c < L.n_chunks; ++c) {
+    const int32_t t0 = (int32_t)(c * L.chunk);
+    const int32_t tc = (int32_t)((T - t0) < L.chunk ? (T - t0) : L.chunk);
+    st = moe_permute(topk_ids + (int64_t)t0 * k, tc, d.topk, d.n_experts, offsets + c * (E + 1),
+                     sorted_src + c * L.chunk * k, dest_row + c * L.chunk * k, dev_status, perm_ws, perm_ws_bytes,
+                     compute);
+    if (st != MOE_OK) return st;
+  }
+
+  // Experts are streamed and run in groups of G consecutive experts, held in
+  // G consecutive ring slots, so that one launch covers enough rows to fill
+  // the GPU (about 2048 rows per chunk).  G divides R.
+  int G = 1;
+  {
+    const int64_t rows_per_expert = ((int64_t)L.chunk * k + E - 1) / E;
+    int64_t want = (2048 + rows_per_expert - 1) / rows_per_expert;
+    if (want > R) want = R;
+    for (int g = (int)want; g >= 1; --g)
+      if (R % g == 0) { G = g; break; }
+  }
+  const int groups_in_ring = R / G;
+  const moe_dims_t view{d.hidden, d.inter, G, d.topk};
+  const int64_t max_mtiles = ((int64_t)L.chunk * k + 127) / 128 + G;  // G experts, at most chunk rows each
+  uint8_t* ring_gate = dev_ring;
+  uint8_t* ring_up = dev_ring + (size_t)R * wmat;
+  uint8_t* ring_down = dev_ring + 2 * (size_t)R * wmat;
+  float* ring_sgate = dev_ring_scales;
+  float* ring_sup = dev_ring_scales + (size_t)R * smat;
+  float* ring_sdown = dev_ring_scales + 2 * (size_t)R * smat;
+  for (int64_t e0 = 0; e0 < E; e0 += G) {
+    const int g_here = (int)((E - e0) < G ? (E - e0) : G);
+    const int64_t grp = e0 / G;
+    const int ev = (int)(grp % groups_in_ring);
+    const int slot0 = (int)(e0 % R);
+    // Loader: the group's slots are free once the group that used them last ran.
+    if (grp >= groups_in_ring && hipStreamWaitEvent(copy, ctx->off[ev], 0) != hipSuccess)
+      return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait OFF");
+    const size_t nb_w = (size_t)g_here * wmat, nb_s = (size_t)g_here * smat * sizeof(float);
+    if (hipMemcpyAsync(ring_gate + slot0 * wmat, host_w_gate + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
+        hipMemcpyAsync(ring_up + slot0 * wmat, host_w_up + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
+        hipMemcpyAsync(ring_down + slot0 * wmat, host_w_down + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
+        hipMemcpyAsync(ring_sgate + slot0 * smat, host_s_gate + e0 * smat, nb_s, hipMemcpyHostToDevice, copy) ||
+        hipMemcpyAsync(ring_sup + slot0 * smat, host_s_up + e0 * smat, nb_s, hipMemcpyHostToDevice, copy) ||
+        hipMemcpyAsync(ring_sdown + slot0 * smat, host_s_down + e0 * smat, nb_s, hipMemcpyHostToDevice, copy))
+      return fail(MOE_ERR_HIP, "moe_ffn_streamed: copy of experts %lld..", (long long)e0);
+    if (hipEventRecord(ctx->on[ev], copy) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record ON");
+    // Model: the group's rows of every chunk, one launch set per chunk.
+    if (hipStreamWaitEvent(compute, ctx->on[ev], 0) != hipSuccess)
+      return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait ON");
+    const moe_dims_t vd{view.hidden, view.inter, g_here, view.topk};
+    for (int64_t c = 0; c < L.n_chunks; ++c) {
+      const int32_t t0 = (int32_t)(c * L.chunk);
+      const int32_t tc = (int32_t)((T - t0) < L.chunk ? (T - t0) : L.chunk);
+      st = run_ffn_prefill_view(vd, max_mtiles, tc, qx + (int64_t)t0 * H, sx + (int64_t)t0 * (H / kBlock),
+                                offsets + c * (E + 1) + e0, sorted_src + c * L.chunk * k, ring_gate + slot0 * wmat,
+                                ring_sgate + slot0 * smat, ring_up + slot0 * wmat, ring_sup + slot0 * smat,
+                                ring_down + slot0 * wmat, ring_sdown + slot0 * smat, y + c * L.chunk * k * H, qh,
+                                sh, tiles, compute);
+      if (st != MOE_OK) return st;
+    }
+    if (hipEventRecord(ctx->off[ev], compute) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record OFF");
+  }
+
+  // Combine each chunk.
+  for (int64_t c = 0; c < L.n_chunks; ++c) {
+    const int32_t t0 = (int32_t)(c * L.chunk);
+    const int32_t tc = (int32_t)((T - t0) < L.chunk ? (T - t0) : L.chunk);
+    st = moe_combine(y + c * L.chunk * k * H, dest_row + c * L.chunk * k, topk_w + (int64_t)t0 * k, tc, d.topk,
+                     d.hidden, out_bf16 + (int64_t)t0 * H, compute);
+    if (st != MOE_OK) return st;
+  }
+  return MOE_OK;
+}
