@@ -35,6 +35,12 @@ class MoEError(RuntimeError):
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run `python paper_2606_10493_amd/build.py`")
 
+# torch brings its own HIP runtime (soname libamdhip64.so.7).  Loading it
+# first makes libmoe.so bind to that same runtime, so the streams and device
+# memory torch hands over belong to the runtime that launches the kernels.
+# Loading libmoe.so first would pull a second HIP runtime into the process.
+import torch  # noqa: E402,F401
+
 lib = ctypes.CDLL(LIB_PATH)
 
 _P = ctypes.c_void_p

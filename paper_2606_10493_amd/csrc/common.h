@@ -84,6 +84,31 @@ __device__ __forceinline__ float silu_mul(float g, float u) {
   return (g * (1.0f / (1.0f + expf(-g)))) * u;
 }
 
+// Exclusive prefix sum of v over the whole workgroup (blockDim.x a multiple
+// of 64, at most 1024): shuffle scan inside each wave, wave totals through
+// LDS (wave_tot holds blockDim.x/64 ints).  Returns the exclusive prefix and
+// the workgroup total.  Every thread of the workgroup must call it.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* wave_tot, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) wave_tot[wave] = x;
+  __syncthreads();
+  int pre = 0, tot = 0;
+  for (int w = 0; w < nw; ++w) {
+    const int t = wave_tot[w];
+    pre += (w < wave) ? t : 0;
+    tot += t;
+  }
+  __syncthreads();  // wave_tot may be reused right after
+  *total = tot;
+  return pre + x - v;
+}
+
 // ----------------------------------------------------------------- host side
 void prof_before(hipStream_t s, const char* name);
 void prof_after(hipStream_t s);

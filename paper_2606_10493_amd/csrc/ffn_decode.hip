@@ -138,9 +138,19 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       // whose outputs it holds (4*kq + i), or -1 beyond the expert's rows.
       // All index loads are issued before any of them is used (clamped
       // indices, no branches), so they cost one round trip together.
+      auto load_w = [&](int bk, v8i (&w)[G][NT], float (&ws)[G]) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          w[0][nt] = load_v8i(wrow0[nt] + bk * kBlock);
+          if (GATEUP) w[G - 1][nt] = load_v8i(wrow1[nt] + bk * kBlock);
+        }
+        // Weight scales travel in the same in-order load stream as the weights.
+        ws[0] = p.s0[srow + bk];
+        if (GATEUP) ws[G - 1] = p.s1[srow + bk];
+      };
       int ta[MT], ts[MT][4];
+      int raw[MT][5];
       if (!QH) {
-        int raw[MT][5];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -149,18 +159,8 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
             const int mm = m < mc ? m : mc - 1;
             raw[mt][q] = p.sorted_src ? p.sorted_src[p0 + mb + mm] : p0 + mb + mm;
           }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int q = 0; q < 5; ++q) {
-            const int m = mt * 16 + (q == 0 ? r : 4 * kq + q - 1);
-            const int src = p.sorted_src ? raw[mt][q] / p.topk : raw[mt][q];
-            const int v = (m < mc && src >= 0 && src < p.a_rows) ? src : -1;
-            if (q == 0) ta[mt] = v; else ts[mt][q - 1] = v;
-          }
       }
-
-      // QH: h values of this lane group (column block qgrp), loaded first.
+      // QH: h values of this lane group (column block qgrp), loaded before the weights.
       const int qsub = threadIdx.x & 15, qgrp = threadIdx.x >> 4;
       const int qcol = qgrp * kBlock + qsub * 8;
       float hv[QH ? kQhRows : 1][8];
@@ -179,17 +179,25 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
           }
         }
       }
-
-      auto load_w = [&](int bk, v8i (&w)[G][NT], float (&ws)[G]) {
+      // The wave's first weight block goes out now, so the weight stream
+      // starts while the index (or h) loads are still in flight.  A wave
+      // without K blocks (nb < 4) loads nothing: its block index would lie
+      // past the end of the rows.
+      v8i wfirst[G][NT];
+      float wsfirst[G];
+      if (nkw > 0) load_w(wave, wfirst, wsfirst);
+      __builtin_amdgcn_sched_barrier(0);
+      if (!QH) {
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          w[0][nt] = load_v8i(wrow0[nt] + bk * kBlock);
-          if (GATEUP) w[G - 1][nt] = load_v8i(wrow1[nt] + bk * kBlock);
-        }
-        // Weight scales travel in the same in-order load stream as the weights.
-        ws[0] = p.s0[srow + bk];
-        if (GATEUP) ws[G - 1] = p.s1[srow + bk];
-      };
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int q = 0; q < 5; ++q) {
+            const int m = mt * 16 + (q == 0 ? r : 4 * kq + q - 1);
+            const int src = p.sorted_src ? raw[mt][q] / p.topk : raw[mt][q];
+            const int v = (m < mc && src >= 0 && src < p.a_rows) ? src : -1;
+            if (q == 0) ta[mt] = v; else ts[mt][q - 1] = v;
+          }
+      }
 
       if (QH) {
         // h rows of this expert -> e4m3 per 128 in LDS (same rule as moe_quant_rows_f32).
@@ -222,14 +230,8 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) acc[g][mt][nt] = v4f{0.f, 0.f, 0.f, 0.f};
 
-      // K loop: each block's loads are issued at the top of its iteration;
-      // the unrolled copies let the compiler hoist the next blocks' loads.
-#pragma unroll U
-      for (int j = 0; j < nkw; ++j) {
-        const int bk = wave + kWaves * j;
-        v8i w[G][NT];
-        float ws[G];
-        load_w(bk, w, ws);
+      // Multiply K block bk (weights in w, ws) into the accumulators.
+      auto compute_block = [&](int bk, const v8i (&w)[G][NT], const float (&ws)[G]) {
         v8i afrag[MT];
         float sa[MT][4];
         if (QH) {
@@ -260,6 +262,19 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
 #pragma unroll
               for (int i = 0; i < 4; ++i) acc[g][mt][nt][i] += part[i] * (sa[mt][i] * ws[g]);
             }
+      };
+
+      // K loop: block 0 was loaded above; each later block's loads are
+      // issued at the top of its iteration and the unrolled copies let the
+      // compiler hoist the next blocks' loads.
+      if (nkw > 0) compute_block(wave, wfirst, wsfirst);
+#pragma unroll U
+      for (int j = 1; j < nkw; ++j) {
+        const int bk = wave + kWaves * j;
+        v8i w[G][NT];
+        float ws[G];
+        load_w(bk, w, ws);
+        compute_block(bk, w, ws);
       }
 
       // Cross-wave reduction in wave order 0, 1, 2, 3.

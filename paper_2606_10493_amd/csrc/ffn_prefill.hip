@@ -63,19 +63,13 @@ struct PrefillArgs {
 
 __global__ __launch_bounds__(1024) void prefill_tiles_kernel(const int32_t* __restrict__ offsets, int E,
                                                              int32_t* __restrict__ mtile_start) {
-  __shared__ int tmp[1024];
+  __shared__ int wave_tot[16];
   const int e = threadIdx.x;
   const int c = (e < E) ? (offsets[e + 1] - offsets[e] + kBM - 1) / kBM : 0;
-  tmp[e] = c;
-  __syncthreads();
-  for (int d = 1; d < 1024; d <<= 1) {
-    const int add = (e >= d) ? tmp[e - d] : 0;
-    __syncthreads();
-    tmp[e] += add;
-    __syncthreads();
-  }
-  if (e < E) mtile_start[e] = tmp[e] - c;
-  if (e == 0) mtile_start[E] = tmp[1023];
+  int total;
+  const int excl = block_exclusive_scan(c, wave_tot, &total);
+  if (e < E) mtile_start[e] = excl;
+  if (e == 0) mtile_start[E] = total;
 }
 
 __device__ __forceinline__ uint4 and4(uint4 v, uint32_t m) {

@@ -113,23 +113,6 @@ __device__ __forceinline__ void scatter_chunk(const unsigned long long* mask, co
   }
 }
 
-// Exclusive scan of v over a 256-thread block (LDS, Hillis-Steele).
-__device__ __forceinline__ int block_exclusive_scan256(int v, int* tmp, int* total) {
-  const int t = threadIdx.x;
-  tmp[t] = v;
-  __syncthreads();
-  for (int d = 1; d < 256; d <<= 1) {
-    const int add = (t >= d) ? tmp[t - d] : 0;
-    __syncthreads();
-    tmp[t] += add;
-    __syncthreads();
-  }
-  const int incl = tmp[t];
-  *total = tmp[255];
-  __syncthreads();
-  return incl - v;
-}
-
 __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
                                                             int32_t* __restrict__ offsets,
                                                             int32_t* __restrict__ sorted_src,
@@ -137,7 +120,7 @@ __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __res
                                                             int32_t* __restrict__ dev_status) {
   __shared__ unsigned long long mask[kMaxExperts * 4];
   __shared__ int start[kMaxExperts];
-  __shared__ int tmp[256];
+  __shared__ int tmp[4];
   __shared__ int bad_count;
   for (int i = threadIdx.x; i < E * 4; i += 256) mask[i] = 0ull;
   if (threadIdx.x == 0) bad_count = 0;
@@ -153,7 +136,7 @@ __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __res
     local += c[q];
   }
   int total_valid;
-  int run = block_exclusive_scan256(local, tmp, &total_valid);
+  int run = block_exclusive_scan(local, tmp, &total_valid);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = 4 * threadIdx.x + q;
@@ -191,22 +174,15 @@ __global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __res
 __global__ __launch_bounds__(1024) void permute_scan_kernel(const int32_t* __restrict__ counts, int n_chunks, int E,
                                                             int32_t* __restrict__ base,
                                                             int32_t* __restrict__ offsets) {
-  __shared__ int tmp[1024];
+  __shared__ int wave_tot[16];
   const int e = threadIdx.x;
   int tot = 0;
   if (e < E)
     for (int c = 0; c < n_chunks; ++c) tot += counts[(int64_t)c * (E + 1) + e];
-  tmp[e] = tot;
-  __syncthreads();
-  for (int d = 1; d < 1024; d <<= 1) {
-    const int add = (e >= d) ? tmp[e - d] : 0;
-    __syncthreads();
-    tmp[e] += add;
-    __syncthreads();
-  }
-  const int total_valid = tmp[1023];
+  int total_valid;
+  const int excl = block_exclusive_scan(tot, wave_tot, &total_valid);
   if (e < E) {
-    int run = tmp[e] - tot;
+    int run = excl;
     offsets[e] = run;
     for (int c = 0; c < n_chunks; ++c) {
       const int64_t i = (int64_t)c * (E + 1) + e;
