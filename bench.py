@@ -74,11 +74,14 @@ def log(msg):
 def make_layer(moe, torch, synth, w, layer):
     e, i, h = w.n_experts, w.inter, w.hidden
     mats = []
+    tmp = torch.empty((i * h,), dtype=torch.uint8, device="cuda")
     for which, (n, k) in enumerate(((i, h), (i, h), (h, i))):
         q = torch.empty((e, n, k), dtype=torch.uint8, device="cuda")
         s = torch.empty((e, n // 128, k // 128), dtype=torch.float32, device="cuda")
+        rowmajor = tmp.view(n, k)
         for x in range(e):
-            moe.moe_quant_weight(synth.expert_weight_device(w, layer, x, which), q[x], s[x])
+            moe.moe_quant_weight(synth.expert_weight_device(w, layer, x, which), rowmajor, s[x])
+            moe.moe_pack_weight(rowmajor, q[x])
         mats += [q, s]
     torch.cuda.synchronize()
     return tuple(mats)

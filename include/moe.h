@@ -116,6 +116,29 @@ moe_status_t moe_quant_weight(const float* w, int32_t n_mats, int32_t rows, int3
                               uint8_t* q, float* s, hipStream_t stream);
 
 /*
+ * Weight packing into the operand-tile layout that moe_expert_ffn and
+ * moe_ffn_streamed read (a storage order of the FP8 Block Scaling Format's
+ * codes; the values and the 128x128 scales are unchanged).
+ *
+ * Each [rows, cols] matrix is cut into 16-row x 128-column tiles of 2048
+ * bytes, stored row-group major: tile (g, b) starts at byte
+ * (g * cols/128 + b) * 2048 of the matrix.  Inside a tile, byte
+ * h*1024 + 16*l + j (h in {0,1}, l in [0,64), j in [0,16)) holds
+ *   q[16g + (l % 16), 128b + 64h + 16(l / 16) + j],
+ * the order in which the 64 lanes of a wave feed one 16x16x128 FP8 MFMA
+ * operand, so the kernels read each tile with two fully contiguous 1 KB
+ * wave loads.  A matrix keeps its size (rows*cols bytes) and an expert's
+ * matrix stays contiguous.
+ *
+ * q: device e4m3 [n_mats, rows, cols] row-major (from moe_quant_weight).
+ * packed: device, n_mats*rows*cols bytes, not overlapping q.  rows a
+ * multiple of 16, cols a multiple of 128; both pointers 16-byte aligned.
+ * Offline weight preparation, like moe_quant_weight.
+ */
+moe_status_t moe_pack_weight(const uint8_t* q, int32_t n_mats, int32_t rows, int32_t cols,
+                             uint8_t* packed, hipStream_t stream);
+
+/*
  * Token -> expert permutation (tokens are gated and sorted by expert into
  * per-expert token lists: Multi-GPU Parallelism and the standard EP
  * workflow of Distributed Stream-loading Prefill).
@@ -156,6 +179,8 @@ moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t 
  * qx: device e4m3 [T, H]; sx: device fp32 [T, H/128] (from moe_quant_act).
  * w_gate, w_up: device e4m3 [E, I, H]; s_gate, s_up: fp32 [E, I/128, H/128].
  * w_down: device e4m3 [E, H, I]; s_down: fp32 [E, H/128, I/128].
+ * The three weight stacks are in the packed layout of moe_pack_weight
+ * (the scales stay row-major).
  * y_rows: device fp32 [T*k, H] in expert-sorted order.
  * ws: device workspace of moe_expert_ffn_workspace(dims, T, regime) bytes.
  * regime: see moe_regime_t; DECODE requires T <= MOE_DECODE_MAX_TOKENS.
@@ -197,8 +222,9 @@ moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const flo
  * output row equals moe_expert_ffn with MOE_REGIME_PREFILL on resident
  * weights bit for bit (same kernels, same per-row arithmetic).
  *
- * host_w_*: pinned host e4m3 weights, layouts as moe_expert_ffn ([E,I,H]
- * for gate/up, [E,H,I] for down); host_s_*: pinned host fp32 scales.
+ * host_w_*: pinned host e4m3 weights, packed as for moe_expert_ffn ([E,I,H]
+ * for gate/up, [E,H,I] for down, each expert's matrix in the layout of
+ * moe_pack_weight); host_s_*: pinned host fp32 scales.
  * dev_ring: device, moe_ring_bytes(dims, slots) bytes, three sub-rings
  * [slots][I*H] of W_gate, W_up and [slots][H*I] of W_down (slot s holds one
  * expert in each).  dev_ring_scales: device, moe_ring_scale_bytes(dims,

@@ -71,6 +71,15 @@ def moe_quant_weight(w, q, s, stream=None):
     _check(lib.moe_quant_weight(_ptr(w), shape[0], shape[1], shape[2], _ptr(q), _ptr(s), _stream(stream)))
 
 
+def moe_pack_weight(q, packed, stream=None):
+    """q uint8 [n_mats, rows, cols] (or [rows, cols]) row-major -> packed operand tiles (same size)."""
+    _need(q, 1, "q"); _need(packed, 1, "packed")
+    shape = q.shape if q.dim() == 3 else (1, *q.shape)
+    if packed.numel() != q.numel():
+        raise MoEError(MOE_ERR_INVALID_ARG, "moe_pack_weight: packed must have as many bytes as q")
+    _check(lib.moe_pack_weight(_ptr(q), shape[0], shape[1], shape[2], _ptr(packed), _stream(stream)))
+
+
 def moe_permute_workspace(T: int, k: int, E: int) -> int:
     return int(lib.moe_permute_workspace(T, k, E))
 

@@ -54,6 +54,7 @@ _SIGS = {
     "moe_quant_act": (_ST, [_P, _I, _I, _P, _P, _P]),
     "moe_quant_rows_f32": (_ST, [_P, _I, _I, _P, _P, _P]),
     "moe_quant_weight": (_ST, [_P, _I, _I, _I, _P, _P, _P]),
+    "moe_pack_weight": (_ST, [_P, _I, _I, _I, _P, _P]),
     "moe_permute_workspace": (_S, [_I, _I, _I]),
     "moe_permute": (_ST, [_P, _I, _I, _I, _P, _P, _P, _P, _P, _S, _P]),
     "moe_expert_ffn_workspace": (_S, [MoeDims, _I, _ST]),

@@ -61,9 +61,11 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
 }
 
 // FP8 x FP8 MFMA over one 128-element K block: D[16x16] = A[16x128] * B[128x16].
-// Lane l supplies row (l & 15) of A and column (l & 15) of B, 32 bytes each,
-// taken from the same 32-byte K range for A and B; the instruction's internal
-// order of K does not change the dot products because A and B share it.
+// Lane l supplies row (l & 15) of A and column (l & 15) of B, 32 bytes each.
+// Every operand of the library uses one K assignment: lane group kq = l / 16
+// supplies K bytes [16 kq, 16 kq + 16) and [64 + 16 kq, 80 + 16 kq) of the
+// block.  A and B share it, so each dot product runs over the whole block;
+// the instruction's internal order of K does not matter.
 // The E8M0 block scales of the instruction are left at 127 (= 1.0); the fp32
 // scales are applied to the result.
 __device__ __forceinline__ v4f mfma_f8_16x16x128(const v8i& a, const v8i& b) {
@@ -71,13 +73,30 @@ __device__ __forceinline__ v4f mfma_f8_16x16x128(const v8i& a, const v8i& b) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, zero, 0, 0, 0, 127, 0, 127);
 }
 
-__device__ __forceinline__ v8i load_v8i(const uint8_t* p) {
-  const uint4 lo = *reinterpret_cast<const uint4*>(p);
-  const uint4 hi = *reinterpret_cast<const uint4*>(p + 16);
+// Packed weight layout (moe_pack_weight): a [rows, K] e4m3 matrix is stored
+// as 16-row x 128-K operand tiles of 2048 bytes, tile (g, b) at
+// (g * K/128 + b) * 2048.  Inside a tile, byte h*1024 + 16*l + j holds
+// row 16g + (l & 15), K index 128b + 64h + 16(l >> 4) + j: lane l of a wave
+// finds its whole operand at 16*l and 1024 + 16*l, so one 16-byte load per
+// lane reads 1 KB of contiguous memory.
+constexpr int kTileBytes = 16 * MOE_BLOCK;
+
+__device__ __forceinline__ v8i join_v8i(const uint4& lo, const uint4& hi) {
   v8i r;
   r[0] = lo.x; r[1] = lo.y; r[2] = lo.z; r[3] = lo.w;
   r[4] = hi.x; r[5] = hi.y; r[6] = hi.z; r[7] = hi.w;
   return r;
+}
+
+// Operand of lane group kq from a row-major K block: p points at byte 16 kq
+// of the lane's row within the block.
+__device__ __forceinline__ v8i load_v8i_ksplit(const uint8_t* p) {
+  return join_v8i(*reinterpret_cast<const uint4*>(p), *reinterpret_cast<const uint4*>(p + 64));
+}
+
+// Operand from a packed weight tile: p points at byte 16*l of the tile.
+__device__ __forceinline__ v8i load_v8i_packed(const uint8_t* p) {
+  return join_v8i(*reinterpret_cast<const uint4*>(p), *reinterpret_cast<const uint4*>(p + 1024));
 }
 
 __device__ __forceinline__ float silu_mul(float g, float u) {

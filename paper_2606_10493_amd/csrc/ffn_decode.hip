@@ -13,8 +13,9 @@
 // Work item = (active expert, tile of 16*NT weight rows).  A 256-thread
 // workgroup (4 waves) splits K: wave w takes blocks b = w, w+4, ...; the
 // partial accumulators are summed through LDS in wave order (deterministic).
-// Every weight byte is read once, each lane loading 32 contiguous bytes of a
-// row (16 rows x 128 bytes = 16 full cache lines per wave-load).
+// Every weight byte is read once; the weights are packed in operand tiles
+// (moe_pack_weight), so a wave reads one 16-row x 128-K operand as two
+// contiguous 1 KB loads.
 //
 // Latency is what limits a small GEMV, so the prologue before the first
 // weight load is short: every wave finds its expert with ballots over the
@@ -39,7 +40,7 @@ struct DecodeArgs {
   int a_rows;
   const int32_t* offsets;     // [E+1]
   int E;
-  const uint8_t* w0;          // e4m3 [E, N, K]
+  const uint8_t* w0;          // e4m3 [E, N, K], packed tiles
   const float* s0;            // fp32 [E, N/128, K/128]
   const uint8_t* w1;          // second matrix (up) when GATEUP
   const float* s1;
@@ -109,7 +110,7 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15;   // row of the A / B fragment this lane loads
-  const int kq = lane >> 4;  // 32-byte K slice of the block this lane loads
+  const int kq = lane >> 4;  // K lane group: bytes [16 kq, +16) and [64 + 16 kq, +16) of a block
   const int tiles = p.N / (16 * NT);
   const int nkw = (nb - wave + kWaves - 1) / kWaves;  // K blocks of this wave: wave, wave+4, ...
 
@@ -122,13 +123,15 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
     const int n0 = (int)(item % tiles) * 16 * NT;
     const int p0 = ref.p0;
     const int M = ref.m;
+    // Lane's byte of the first packed tile of each 16-row operand; the
+    // tiles of one 16-row group follow each other along K.
     const uint8_t* wrow0[NT];
     const uint8_t* wrow1[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const int64_t row = (int64_t)e * p.N + n0 + nt * 16 + r;
-      wrow0[nt] = p.w0 + row * p.K + kq * 32;
-      wrow1[nt] = GATEUP ? p.w1 + row * p.K + kq * 32 : nullptr;
+      const int64_t grp = ((int64_t)e * p.N + n0 + nt * 16) / 16;
+      wrow0[nt] = p.w0 + grp * nb * kTileBytes + lane * 16;
+      wrow1[nt] = GATEUP ? p.w1 + grp * nb * kTileBytes + lane * 16 : nullptr;
     }
     const int64_t srow = ((int64_t)e * (p.N / kBlock) + n0 / kBlock) * nb;
 
@@ -141,8 +144,8 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       auto load_w = [&](int bk, v8i (&w)[G][NT], float (&ws)[G]) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-          w[0][nt] = load_v8i(wrow0[nt] + bk * kBlock);
-          if (GATEUP) w[G - 1][nt] = load_v8i(wrow1[nt] + bk * kBlock);
+          w[0][nt] = load_v8i_packed(wrow0[nt] + bk * kTileBytes);
+          if (GATEUP) w[G - 1][nt] = load_v8i_packed(wrow1[nt] + bk * kTileBytes);
         }
         // Weight scales travel in the same in-order load stream as the weights.
         ws[0] = p.s0[srow + bk];
@@ -237,7 +240,7 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
         if (QH) {
           // Rows beyond kQhRows read a valid LDS row; their outputs are never stored.
           const int qr = r < kQhRows ? r : kQhRows - 1;
-          afrag[0] = *reinterpret_cast<const v8i*>(qh_lds + qr * kQhMaxK + bk * kBlock + kq * 32);
+          afrag[0] = load_v8i_ksplit(qh_lds + qr * kQhMaxK + bk * kBlock + kq * 16);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int row = 4 * kq + i;
@@ -246,7 +249,7 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
         } else {
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
-            afrag[mt] = ta[mt] >= 0 ? load_v8i(p.a + (int64_t)ta[mt] * p.K + bk * kBlock + kq * 32)
+            afrag[mt] = ta[mt] >= 0 ? load_v8i_ksplit(p.a + (int64_t)ta[mt] * p.K + bk * kBlock + kq * 16)
                                     : v8i{0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
             for (int i = 0; i < 4; ++i) sa[mt][i] = ts[mt][i] >= 0 ? p.sa[(int64_t)ts[mt][i] * nb + bk] : 0.0f;

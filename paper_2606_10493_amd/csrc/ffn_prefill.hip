@@ -4,19 +4,31 @@
 // to FP8, FP8 x FP8 products with FP32 accumulation; gate and up fused with
 // SiLU(gate)*up as in the paper's stage one, down after it).
 //
-// Tile: 128 expert rows x 256 output columns x one 128-K scale block per
-// step, 512 threads (8 waves as 2 x 4).  Both operands are staged through LDS
-// (double buffered, one barrier per K step).  Each wave owns 64 rows x 4
-// column sub-tiles of 16; every K step issues 16 MFMA 16x16x128 (one scale
-// block each) and promotes each result into the fp32 accumulators with the
-// block's scale product sa[row,b] * sw[nblock,b] (one FMA per output).
+// The products are formed transposed, D = W x X^T: the MFMA's A operand is
+// 16 weight rows (output channels), its B operand 16 expert rows (tokens).
+// A lane's four results then share one token and lie inside one 128-channel
+// weight-scale block, so the per-block scale of a result is (the lane's
+// token scale) x (a wave-uniform weight scale).
 //
-// GATEUP: the 256 columns are 128 gate rows and the same 128 up rows of the
-// weights, so a workgroup holds one full 128-wide block of h: its epilogue
+// Tile: 256 weight rows x 128 expert rows x one 128-K scale block per step,
+// 512 threads (8 waves).  Wave w owns 32 weight rows (two 16-row MFMA
+// operands) against all 128 expert rows (eight 16-row operands): 16 MFMA
+// 16x16x128 per K step, each promoted into fp32 accumulators with one FMA
+// per result.  The weights are packed in operand tiles (moe_pack_weight),
+// so they go from global memory straight into the MFMA operand registers
+// with two contiguous 1 KB wave loads per operand (no wave shares them),
+// through a ring of kRing K blocks loaded kRing - 1 steps ahead.  Only the
+// expert rows, which all waves read, are staged through LDS (double
+// buffered, one barrier per K step; loaded as whole 128-byte row pieces),
+// and their scales sit in LDS transposed, [K block][row].
+//
+// GATEUP: wave w's rows are gate rows nt*128 + 16w + [0, 16) and the same up
+// rows, so a workgroup holds one full 128-wide block of h: its epilogue
 // computes h = SiLU(G) * U, the per-row amax of the block (lanes, then the
-// four column waves through LDS), the scale sh = amax / 448 and the e4m3
-// codes qh, staged through LDS and written as 16-byte rows.
-// DOWN: the 256 columns are 256 rows of W_down; the epilogue writes fp32.
+// eight waves through LDS), the scale sh = amax / 448 and the e4m3 codes qh,
+// staged through LDS and written as 16-byte rows.
+// DOWN: wave w's rows are W_down rows nt*256 + 32w + [0, 32); the epilogue
+// writes fp32 in 16-byte pieces.
 //
 // Work items are (expert m-tile, n-tile) pairs; m-tiles of all experts are
 // numbered by an exclusive scan of ceil(M_e / 128) (prefill_tiles_kernel).
@@ -32,14 +44,17 @@ namespace moe {
 
 namespace {
 
-constexpr int kBM = 128;
-constexpr int kBN = 256;
-constexpr int kThreads = 512;
-constexpr int kLdsRow = kBlock + 16;  // padded LDS row (bytes) to spread banks
-constexpr int kStageA = kBM * kLdsRow;
-constexpr int kStageB = kBN * kLdsRow;
-constexpr int kStage = kStageA + kStageB;
+constexpr int kBM = 128;                // expert rows (tokens) per tile
+constexpr int kBN = 256;                // weight rows per tile
+constexpr int kThreads = 512;           // 8 waves x 32 weight rows
+constexpr int kLdsRow = kBlock + 16;    // padded LDS row (bytes) to spread banks
+constexpr int kStage = kBM * kLdsRow;   // one K block of the expert rows
+constexpr int kSaStride = kBM + 1;      // floats per K block of the row-scale table
+constexpr int kRing = 4;                // weight K blocks in registers
 constexpr int kXcd = 8;
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 struct PrefillArgs {
   const uint8_t* a;           // e4m3 activations [a_rows, K]
@@ -50,9 +65,9 @@ struct PrefillArgs {
   const int32_t* offsets;     // [E+1]
   const int32_t* mtile_start; // [E+1] exclusive scan of ceil(M_e/128)
   int E;
-  const uint8_t* w0;          // GATEUP: W_gate [E, N, K]; DOWN: W_down [E, N, K]
+  const uint8_t* w0;          // GATEUP: W_gate [E, N, K]; DOWN: W_down [E, N, K]; packed tiles
   const float* s0;
-  const uint8_t* w1;          // GATEUP: W_up
+  const uint8_t* w1;          // GATEUP: W_up, packed tiles
   const float* s1;
   int N, K;                   // N: output columns of the expert (I for gate/up, H for down)
   int n_tiles;                // GATEUP: N/128; DOWN: N/256
@@ -72,19 +87,31 @@ __global__ __launch_bounds__(1024) void prefill_tiles_kernel(const int32_t* __re
   if (e == 0) mtile_start[E] = total;
 }
 
-__device__ __forceinline__ uint4 and4(uint4 v, uint32_t m) {
-  return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+// Raw buffer view of [base, base + bytes): loads outside it return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_view(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kRsrcWord3);
+}
+
+// One MFMA operand of K block b from a packed weight tile: voff addresses
+// byte 16*lane of the operand's first tile, the tiles of one 16-row group
+// follow each other along K.
+__device__ __forceinline__ v8i load_operand(__amdgpu_buffer_rsrc_t r, uint32_t voff, int b) {
+  const u32x4 lo = __builtin_amdgcn_raw_buffer_load_b128(r, voff, b * kTileBytes, 0);
+  const u32x4 hi = __builtin_amdgcn_raw_buffer_load_b128(r, voff + 1024, b * kTileBytes, 0);
+  v8i o;
+  o[0] = lo[0]; o[1] = lo[1]; o[2] = lo[2]; o[3] = lo[3];
+  o[4] = hi[0]; o[5] = hi[1]; o[6] = hi[2]; o[7] = hi[3];
+  return o;
 }
 
 template <bool GATEUP>
 __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ int arow[kBM];
-  __shared__ float rowmax[4][kBM];
+  __shared__ float rowmax[8][kBM];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
   const int r = lane & 15, kq = lane >> 4;
 
   // XCD-major work item over the real items (the grid is an upper bound):
@@ -108,7 +135,8 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   const int mc = min(kBM, p.offsets[e + 1] - m0);                            // rows in the tile
   const int nb = p.K / kBlock;
 
-  float* sa_lds = reinterpret_cast<float*>(smem + 2 * kStage);  // [kBM][nb]
+  float* sa_lds = reinterpret_cast<float*>(smem + 2 * kStage);  // [nb][kSaStride]
+  float* sw_lds = sa_lds + nb * kSaStride;                       // [2][nb]
 
   for (int i = tid; i < kBM; i += kThreads) {
     int row = -1;
@@ -118,186 +146,181 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     }
     arow[i] = row;
   }
+  // Weight scales of the tile's two 128-row blocks: GATEUP gate and up block
+  // nt; DOWN blocks 2nt and 2nt + 1 (waves 0-3 and 4-7).
+  for (int i = tid; i < 2 * nb; i += kThreads) {
+    const int h = i / nb, b = i - h * nb;
+    const int64_t wrow = (int64_t)e * (p.N / kBlock) + (GATEUP ? nt : 2 * nt + h);
+    sw_lds[i] = ((GATEUP && h) ? p.s1 : p.s0)[wrow * nb + b];
+  }
   __syncthreads();
   for (int i = tid; i < kBM * nb; i += kThreads) {
     const int m = i / nb, b = i - m * nb;
-    sa_lds[i] = arow[m] >= 0 ? p.sa[(int64_t)arow[m] * nb + b] : 0.0f;
+    sa_lds[b * kSaStride + m] = arow[m] >= 0 ? p.sa[(int64_t)arow[m] * nb + b] : 0.0f;
   }
 
-  // Global -> LDS copy assignment: A = 1024 16-byte chunks (2 per thread),
-  // B = 2048 chunks (4 per thread); chunk c covers row c/8, bytes 16*(c%8).
-  // Rows beyond the expert (or with a bad index) load a valid row and are
-  // zeroed after the load, which keeps every load a plain global load.
+  // Expert rows: 1024 16-byte chunks per K block, 2 per thread; chunk c
+  // covers row c/8, bytes 16*(c%8).  Rows beyond the expert (or with a bad
+  // index) load row 0 instead: their codes are finite and their scale in
+  // sa_lds is 0, so their products promote to exactly 0, and only rows
+  // below mc are written.
   const uint8_t* a_src[2];
-  uint32_t a_mask[2];
   int a_dst[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int c = tid + i * kThreads;
     const int row = c >> 3, col = (c & 7) * 16;
     const int ar = arow[row];
-    a_mask[i] = ar >= 0 ? 0xffffffffu : 0u;
     a_src[i] = p.a + (int64_t)(ar >= 0 ? ar : 0) * p.K + col;
     a_dst[i] = row * kLdsRow + col;
   }
-  const uint8_t* b_src[4];
-  int b_dst[4];
+
+  // This wave's two 16-row weight operands (f = 0, 1), as buffer views of
+  // one expert's packed matrix, and the LDS row of their weight scales.
+  const uint32_t wbytes = (uint32_t)p.N * (uint32_t)p.K;
+  __amdgpu_buffer_rsrc_t wv[2];
+  uint32_t w_off[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + i * kThreads;
-    const int row = c >> 3, col = (c & 7) * 16;
-    const uint8_t* base;
-    if (GATEUP) {
-      const int n = nt * 128 + (row & 127);
-      base = (row < 128 ? p.w0 : p.w1) + ((int64_t)e * p.N + n) * p.K;
-    } else {
-      base = p.w0 + ((int64_t)e * p.N + nt * kBN + row) * p.K;
-    }
-    b_src[i] = base + col;
-    b_dst[i] = kStageA + row * kLdsRow + col;
+  for (int f = 0; f < 2; ++f) {
+    // 16-row group of the operand: GATEUP rows nt*128 + 16w, DOWN rows nt*256 + 32w + 16f.
+    const int g = GATEUP ? nt * (kBlock / 16) + wave : nt * (kBN / 16) + wave * 2 + f;
+    wv[f] = buffer_view((GATEUP && f ? p.w1 : p.w0) + (int64_t)e * wbytes, wbytes);
+    w_off[f] = (uint32_t)g * (uint32_t)nb * kTileBytes + lane * 16;
   }
+  const float* swf0 = sw_lds + (GATEUP ? 0 : (wave >> 2)) * nb;
+  const float* swf1 = sw_lds + (GATEUP ? 1 : (wave >> 2)) * nb;
 
-  // Column sub-tiles of this wave: LDS B rows and their weight-scale source.
-  int bsub_row[4];
-  const float* wscale[4];
+  v4f acc[2][8];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (GATEUP) {
-      bsub_row[j] = (j < 2 ? 0 : 128) + wn * 32 + (j & 1) * 16;
-      const int64_t srow = ((int64_t)e * (p.N / kBlock) + nt) * nb;
-      wscale[j] = (j < 2 ? p.s0 : p.s1) + srow;
-    } else {
-      bsub_row[j] = wn * 64 + j * 16;
-      const int ncol = nt * kBN + wn * 64;
-      wscale[j] = p.s0 + ((int64_t)e * (p.N / kBlock) + ncol / kBlock) * nb;
-    }
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[f][i] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  v8i wr[kRing][2];
+  u32x4 ra[kRing][2];  // ext vectors: an array of HIP's uint4 structs would not stay in registers
+#define MOE_PF_WLOAD(SLOT, BLK)                        \
+  do {                                                 \
+    wr[SLOT][0] = load_operand(wv[0], w_off[0], BLK);  \
+    wr[SLOT][1] = load_operand(wv[1], w_off[1], BLK);  \
+  } while (0)
+#define MOE_PF_ALOAD(SLOT, BLK)                                                         \
+  do {                                                                                  \
+    ra[SLOT][0] = *reinterpret_cast<const u32x4*>(a_src[0] + (int64_t)(BLK) * kBlock);  \
+    ra[SLOT][1] = *reinterpret_cast<const u32x4*>(a_src[1] + (int64_t)(BLK) * kBlock);  \
+  } while (0)
+#define MOE_PF_ASTORE(SLOT, STAGE)                                                         \
+  do {                                                                                     \
+    uint8_t* st_ = smem + (STAGE) * kStage;                                                \
+    *reinterpret_cast<u32x4*>(st_ + a_dst[0]) = ra[SLOT][0];                               \
+    *reinterpret_cast<u32x4*>(st_ + a_dst[1]) = ra[SLOT][1];                               \
+  } while (0)
+  // One K step b using register slot U (= b % kRing).  The loads of block
+  // b + kRing - 1 (expert rows and weights; clamped to the last block, a
+  // harmless reload) go out first; scheduling barriers keep them above the
+  // math and the LDS store of block b + 1 (loaded kRing - 2 steps ago) below
+  // it.
+#define MOE_PF_STEP(U, B)                                                                  \
+  do {                                                                                     \
+    const int b_ = (B);                                                                    \
+    const int bl_ = b_ + kRing - 1 < nb ? b_ + kRing - 1 : nb - 1;                         \
+    MOE_PF_ALOAD(((U) + kRing - 1) % kRing, bl_);                                          \
+    MOE_PF_WLOAD(((U) + kRing - 1) % kRing, bl_);                                          \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+    const uint8_t* sB = smem + (b_ & 1) * kStage + r * kLdsRow + kq * 16;                  \
+    const float* sa_b = sa_lds + b_ * kSaStride + r;                                       \
+    const float sw0 = swf0[b_], sw1 = swf1[b_];                                            \
+    /* products of operand i are promoted while those of i + 1 run */                      \
+    v8i bx = load_v8i_ksplit(sB);                                                          \
+    v4f p0 = mfma_f8_16x16x128(wr[U][0], bx);                                              \
+    v4f p1 = mfma_f8_16x16x128(wr[U][1], bx);                                              \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                        \
+      v4f n0, n1;                                                                          \
+      if (i < 7) {                                                                         \
+        bx = load_v8i_ksplit(sB + (i + 1) * 16 * kLdsRow);                                 \
+        n0 = mfma_f8_16x16x128(wr[U][0], bx);                                              \
+        n1 = mfma_f8_16x16x128(wr[U][1], bx);                                              \
+      }                                                                                    \
+      const float sa = sa_b[i * 16];                                                       \
+      const float s0 = sa * sw0, s1 = sa * sw1;                                            \
+      _Pragma("unroll") for (int q = 0; q < 4; ++q) {                                      \
+        acc[0][i][q] += p0[q] * s0;                                                        \
+        acc[1][i][q] += p1[q] * s1;                                                        \
+      }                                                                                    \
+      if (i < 7) { p0 = n0; p1 = n1; }                                                     \
+    }                                                                                      \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+    MOE_PF_ASTORE(((U) + 1) % kRing, (b_ + 1) & 1);                                        \
+    __syncthreads();                                                                       \
+  } while (0)
+
+#pragma unroll
+  for (int s = 0; s < kRing - 1; ++s) {
+    MOE_PF_ALOAD(s, s < nb ? s : nb - 1);
+    MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
   }
-
-  v4f acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-
-  // Staging registers of one K block (global -> registers -> LDS).  Plain
-  // scalars, fully unrolled, so they stay in VGPRs.
-  uint4 ra0, ra1, rb0, rb1, rb2, rb3;
-#define MOE_PF_GLOAD(BLK)                                                                            \
-  do {                                                                                               \
-    const int off_ = (BLK) * kBlock;                                                                 \
-    ra0 = *reinterpret_cast<const uint4*>(a_src[0] + off_);                                          \
-    ra1 = *reinterpret_cast<const uint4*>(a_src[1] + off_);                                          \
-    rb0 = *reinterpret_cast<const uint4*>(b_src[0] + off_);                                          \
-    rb1 = *reinterpret_cast<const uint4*>(b_src[1] + off_);                                          \
-    rb2 = *reinterpret_cast<const uint4*>(b_src[2] + off_);                                          \
-    rb3 = *reinterpret_cast<const uint4*>(b_src[3] + off_);                                          \
-  } while (0)
-#define MOE_PF_LSTORE(STAGE)                                                                         \
-  do {                                                                                               \
-    uint8_t* st_ = smem + (STAGE) * kStage;                                                          \
-    *reinterpret_cast<uint4*>(st_ + a_dst[0]) = and4(ra0, a_mask[0]);                                \
-    *reinterpret_cast<uint4*>(st_ + a_dst[1]) = and4(ra1, a_mask[1]);                                \
-    *reinterpret_cast<uint4*>(st_ + b_dst[0]) = rb0;                                                 \
-    *reinterpret_cast<uint4*>(st_ + b_dst[1]) = rb1;                                                 \
-    *reinterpret_cast<uint4*>(st_ + b_dst[2]) = rb2;                                                 \
-    *reinterpret_cast<uint4*>(st_ + b_dst[3]) = rb3;                                                 \
-  } while (0)
-
-  MOE_PF_GLOAD(0);
-  MOE_PF_LSTORE(0);
+  MOE_PF_ASTORE(0, 0);
   __syncthreads();
 
-  for (int b = 0; b < nb; ++b) {
-    const int stage = b & 1;
-    // The next block's global loads go out first; scheduling barriers keep
-    // them above the math and keep the LDS store of the next stage below it,
-    // so their latency overlaps this block's MFMAs.  The body is one basic
-    // block: the last step re-loads its own block and stores it into the
-    // stage nobody reads any more.
-    MOE_PF_GLOAD(b + 1 < nb ? b + 1 : b);
-    __builtin_amdgcn_sched_barrier(0);
-    const uint8_t* sA = smem + stage * kStage;
-    const uint8_t* sB = sA + kStageA;
-    v8i af[4], bf[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = load_v8i(sA + (wm * 64 + i * 16 + r) * kLdsRow + kq * 32);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) bf[j] = load_v8i(sB + (bsub_row[j] + r) * kLdsRow + kq * 32);
-    float sw[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) sw[j] = wscale[j][b];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float sa[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) sa[q] = sa_lds[(wm * 64 + i * 16 + 4 * kq + q) * nb + b];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const v4f part = mfma_f8_16x16x128(af[i], bf[j]);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) acc[i][j][q] += part[q] * (sa[q] * sw[j]);
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    MOE_PF_LSTORE(stage ^ 1);
-    __syncthreads();
+  int b0 = 0;
+  for (; b0 + kRing <= nb; b0 += kRing) {
+    MOE_PF_STEP(0, b0);
+    MOE_PF_STEP(1, b0 + 1);
+    MOE_PF_STEP(2, b0 + 2);
+    MOE_PF_STEP(3, b0 + 3);
   }
-#undef MOE_PF_GLOAD
-#undef MOE_PF_LSTORE
+  if (b0 < nb) MOE_PF_STEP(0, b0);
+  if (b0 + 1 < nb) MOE_PF_STEP(1, b0 + 1);
+  if (b0 + 2 < nb) MOE_PF_STEP(2, b0 + 2);
+#undef MOE_PF_WLOAD
+#undef MOE_PF_ALOAD
+#undef MOE_PF_ASTORE
+#undef MOE_PF_STEP
 
   if (!GATEUP) {
-    // y[m0 + row, nt*256 + col]; lane holds rows 4*kq+q of each 16x16 sub-tile, column r.
+    // y[m0 + t][nt*256 + 32w + 16f + 4kq + q] for expert row t = 16i + r.
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i) {
+      const int t = i * 16 + r;
+      if (t < mc) {
+        float* dst = p.y + (int64_t)(m0 + t) * p.N + nt * kBN + wave * 32 + kq * 4;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int row = wm * 64 + i * 16 + 4 * kq + q;
-        if (row < mc) {
-          float* dst = p.y + (int64_t)(m0 + row) * p.N + nt * kBN + wn * 64 + r;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) dst[j * 16] = acc[i][j][q];
-        }
+        for (int f = 0; f < 2; ++f) *reinterpret_cast<v4f*>(dst + f * 16) = acc[f][i];
       }
+    }
     return;
   }
 
-  // GATEUP epilogue: h = SiLU(G) * U; sub-tiles j = 0,1 are gate, 2,3 up.
-  float h[4][2][4];
-  float pmax[4][4];
+  // GATEUP epilogue: h = SiLU(G) * U for channels 16w + 4kq + q of rows
+  // t = 16i + r; per-row amax over the lane's 4 channels, the 4 lanes of
+  // the row (kq) and the 8 waves.
+  float h[8][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i) {
+    float mx = 0.0f;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      float mx = 0.0f;
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        h[i][j][q] = silu_mul(acc[i][j][q], acc[i][j + 2][q]);
-        mx = fmaxf(mx, fabsf(h[i][j][q]));
-      }
-      // max over the 16 lanes that share these rows (same kq)
-#pragma unroll
-      for (int m = 8; m >= 1; m >>= 1) mx = fmaxf(mx, __shfl_xor(mx, m, 16));
-      pmax[i][q] = mx;
+      h[i][q] = silu_mul(acc[0][i][q], acc[1][i][q]);
+      mx = fmaxf(mx, fabsf(h[i][q]));
     }
-  if (r == 0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) rowmax[wn][wm * 64 + i * 16 + 4 * kq + q] = pmax[i][q];
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    if (kq == 0) rowmax[wave][i * 16 + r] = mx;
   }
   __syncthreads();
   uint8_t* qtile = smem;  // [kBM][kLdsRow], the K-loop buffers are free now
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i) {
+    const int t = i * 16 + r;
+    float amax = rowmax[0][t];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int row = wm * 64 + i * 16 + 4 * kq + q;
-      const float amax = fmaxf(fmaxf(rowmax[0][row], rowmax[1][row]), fmaxf(rowmax[2][row], rowmax[3][row]));
-      const float s = amax / kE4M3Max;
+    for (int w = 1; w < 8; ++w) amax = fmaxf(amax, rowmax[w][t]);
+    const float s = amax / kE4M3Max;
+    uint32_t packed = 0;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) qtile[row * kLdsRow + wn * 32 + j * 16 + r] = (uint8_t)quantize_e4m3(h[i][j][q], s);
-      if (wn == 0 && r == 0 && row < mc) p.sh[(int64_t)(m0 + row) * (p.N / kBlock) + nt] = s;
-    }
+    for (int q = 0; q < 4; ++q) packed |= quantize_e4m3(h[i][q], s) << (8 * q);
+    *reinterpret_cast<uint32_t*>(qtile + t * kLdsRow + wave * 16 + kq * 4) = packed;
+    if (wave == 0 && kq == 0 && t < mc) p.sh[(int64_t)(m0 + t) * (p.N / kBlock) + nt] = s;
+  }
   __syncthreads();
   // 128 rows x 128 bytes = 1024 16-byte chunks, 2 per thread.
 #pragma unroll
@@ -315,7 +338,9 @@ moe_status_t launch_prefill(const PrefillArgs& a, int64_t max_mtiles, hipStream_
   int64_t grid = max_mtiles * a.n_tiles;
   grid = (grid + kXcd - 1) / kXcd * kXcd;
   if (grid > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: grid too large");
-  const size_t lds = 2 * (size_t)kStage + sizeof(float) * (size_t)kBM * (a.K / kBlock);
+  if ((int64_t)a.N * a.K > 0x7fffffff)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: one expert matrix (%d x %d) exceeds 2 GiB", a.N, a.K);
+  const size_t lds = 2 * (size_t)kStage + sizeof(float) * ((size_t)kSaStride + 2) * (a.K / kBlock);
   if (lds > 150 * 1024) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: K=%d needs %zu bytes of LDS", a.K, lds);
   const hipError_t ae = hipFuncSetAttribute(reinterpret_cast<const void*>(&ffn_prefill_kernel<GATEUP>),
                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -124,6 +124,23 @@ moe_status_t quant_rows(const InT* x, int32_t rows, int32_t cols, uint8_t* q, fl
   return check_launch(name);
 }
 
+// Row-major e4m3 [total_rows, cols] -> packed operand tiles (the layout is
+// described with kTileBytes).  One thread moves one 16-byte chunk: output
+// chunk c is lane l = c % 64 of half h = (c / 64) % 2 of tile c / 128.
+__global__ __launch_bounds__(256) void pack_weight_kernel(const uint8_t* __restrict__ q, int64_t chunks, int cols,
+                                                          uint8_t* __restrict__ out) {
+  const int nkb = cols / kBlock;
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < chunks; c += (int64_t)gridDim.x * blockDim.x) {
+    const int l = (int)(c & 63), h = (int)((c >> 6) & 1);
+    const int64_t tile = c >> 7;
+    const int64_t g = tile / nkb;
+    const int b = (int)(tile - g * nkb);
+    const int64_t row = g * 16 + (l & 15);
+    const int64_t col = (int64_t)b * kBlock + h * 64 + (l >> 4) * 16;
+    *reinterpret_cast<uint4*>(out + c * 16) = *reinterpret_cast<const uint4*>(q + row * cols + col);
+  }
+}
+
 }  // namespace
 
 }  // namespace moe
@@ -154,4 +171,21 @@ extern "C" moe_status_t moe_quant_weight(const float* w, int32_t n_mats, int32_t
   if (blocks > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_quant_weight: too many blocks");
   MOE_LAUNCH("quant_weight", quant_weight_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, w, rows, cols, q, s);
   return check_launch("moe_quant_weight");
+}
+
+extern "C" moe_status_t moe_pack_weight(const uint8_t* q, int32_t n_mats, int32_t rows, int32_t cols,
+                                        uint8_t* packed, hipStream_t stream) {
+  if (n_mats < 0 || rows <= 0 || cols <= 0)
+    return fail(MOE_ERR_INVALID_ARG, "moe_pack_weight: n_mats=%d rows=%d cols=%d", n_mats, rows, cols);
+  if (rows % 16 || cols % kBlock)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_pack_weight: %dx%d needs rows %% 16 == 0 and cols %% 128 == 0", rows, cols);
+  if (n_mats == 0) return MOE_OK;
+  if (!q || !packed) return fail(MOE_ERR_INVALID_ARG, "moe_pack_weight: null pointer");
+  if (q == packed) return fail(MOE_ERR_INVALID_ARG, "moe_pack_weight: packing in place is not supported");
+  if (!aligned(q, 16) || !aligned(packed, 16)) return fail(MOE_ERR_INVALID_ARG, "moe_pack_weight: misaligned pointer");
+  const int64_t chunks = (int64_t)n_mats * rows * (cols / 16);
+  int64_t grid = (chunks + 255) / 256;
+  if (grid > 65536) grid = 65536;
+  MOE_LAUNCH("pack_weight", pack_weight_kernel, dim3((unsigned)grid), dim3(256), 0, stream, q, chunks, cols, packed);
+  return check_launch("moe_pack_weight");
 }

@@ -1,8 +1,10 @@
 """Helpers of the GPU parity tests: seeded inputs on both sides, oracle runs.
 
 Weights are drawn in fp32 by ``synth``; the GPU quantizes them with
-moe_quant_weight and the oracle with its own quantize_weight.  The oracle
-never receives a value produced by the HIP library.
+moe_quant_weight (then packs them into operand tiles with moe_pack_weight,
+the layout the FFN kernels read) and the oracle with its own
+quantize_weight.  The oracle never receives a value produced by the HIP
+library.
 """
 from __future__ import annotations
 
@@ -38,8 +40,16 @@ def bf16_dev(bits: np.ndarray):
     return to_dev(bits.view(np.int16))
 
 
+def pack_reference(q: np.ndarray) -> np.ndarray:
+    """The operand-tile layout of moe_pack_weight, by its definition: byte
+    h*1024 + 16*l + j of tile (g, b) holds q[16g + l%16, 128b + 64h + 16(l//16) + j]."""
+    n, rows, cols = q.shape
+    t = q.reshape(n, rows // 16, 16, cols // 128, 2, 4, 16)   # n, g, r, b, h, kq, j
+    return np.ascontiguousarray(t.transpose(0, 1, 3, 4, 5, 2, 6)).reshape(n, rows, cols)
+
+
 def quantize_weights_gpu(moe, wg, wu, wd):
-    """fp32 host stacks -> device (q, s) triples quantized by the library."""
+    """fp32 host stacks -> device (packed q, s) triples quantized and packed by the library."""
     out = []
     for w in (wg, wu, wd):
         e, n, k = w.shape
@@ -47,14 +57,16 @@ def quantize_weights_gpu(moe, wg, wu, wd):
         q = torch.empty((e, n, k), dtype=torch.uint8, device="cuda")
         s = torch.empty((e, n // 128, k // 128), dtype=torch.float32, device="cuda")
         moe.moe_quant_weight(dw, q, s)
-        out += [q, s]
-        del dw
+        packed = torch.empty_like(q)
+        moe.moe_pack_weight(q, packed)
+        out += [packed, s]
+        del dw, q
     torch.cuda.synchronize()
     return tuple(out)
 
 
 def generated_layer_gpu(moe, w: synth.Workload, layer: int = 0):
-    """Full layer: fp32 experts drawn on the GPU one by one, quantized in place."""
+    """Full layer: fp32 experts drawn on the GPU one by one, quantized and packed in place."""
     e, i, h = w.n_experts, w.inter, w.hidden
     qg = torch.empty((e, i, h), dtype=torch.uint8, device="cuda")
     qu = torch.empty((e, i, h), dtype=torch.uint8, device="cuda")
@@ -62,10 +74,13 @@ def generated_layer_gpu(moe, w: synth.Workload, layer: int = 0):
     sg = torch.empty((e, i // 128, h // 128), dtype=torch.float32, device="cuda")
     su = torch.empty((e, i // 128, h // 128), dtype=torch.float32, device="cuda")
     sd = torch.empty((e, h // 128, i // 128), dtype=torch.float32, device="cuda")
+    tmp = torch.empty((max(i, h) * max(i, h),), dtype=torch.uint8, device="cuda")
     for x in range(e):
         for which, (q, s) in enumerate(((qg, sg), (qu, su), (qd, sd))):
             f = synth.expert_weight_device(w, layer, x, which)
-            moe.moe_quant_weight(f, q[x], s[x])
+            rowmajor = tmp[:f.numel()].view(f.shape)
+            moe.moe_quant_weight(f, rowmajor, s[x])
+            moe.moe_pack_weight(rowmajor, q[x])
     torch.cuda.synchronize()
     return qg, sg, qu, su, qd, sd
 

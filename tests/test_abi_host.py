@@ -24,7 +24,7 @@ def _declared_functions():
 
 def test_header_declares_the_documented_entry_points():
     names = _declared_functions()
-    for n in ("moe_quant_act", "moe_permute", "moe_expert_ffn", "moe_combine", "moe_ffn_streamed",
+    for n in ("moe_quant_act", "moe_pack_weight", "moe_permute", "moe_expert_ffn", "moe_combine", "moe_ffn_streamed",
               "moe_status_string", "moe_permute_workspace", "moe_expert_ffn_workspace"):
         assert n in names
 
@@ -51,6 +51,11 @@ def test_argument_errors_return_before_any_launch():
     assert lib.moe_quant_act(None, 4, 128, fake, fake, None) == moe.MOE_ERR_INVALID_ARG
     assert lib.moe_quant_act(None, 0, 128, None, None, None) == moe.MOE_OK      # empty: no-op
     assert lib.moe_quant_weight(fake, 1, 100, 128, fake, fake, None) == moe.MOE_ERR_UNSUPPORTED_SHAPE
+    assert lib.moe_pack_weight(fake, 1, 24, 128, P(0x2000), None) == moe.MOE_ERR_UNSUPPORTED_SHAPE
+    assert lib.moe_pack_weight(fake, 1, 16, 100, P(0x2000), None) == moe.MOE_ERR_UNSUPPORTED_SHAPE
+    assert lib.moe_pack_weight(fake, 1, 16, 128, fake, None) == moe.MOE_ERR_INVALID_ARG      # in place
+    assert lib.moe_pack_weight(None, 1, 16, 128, fake, None) == moe.MOE_ERR_INVALID_ARG
+    assert lib.moe_pack_weight(None, 0, 16, 128, None, None) == moe.MOE_OK                   # empty: no-op
     assert lib.moe_permute(fake, 4, 9, 8, fake, fake, fake, None, None, 0, None) == moe.MOE_ERR_INVALID_ARG
     assert lib.moe_permute(fake, 4, 2, 2000, fake, fake, fake, None, None, 0, None) == moe.MOE_ERR_INVALID_ARG
     # more than one chunk of tokens needs the workspace

@@ -13,7 +13,7 @@ import torch
 import oracle
 import synth
 from gpu_cases import (bf16_dev, bits_to_f32, generated_layer_gpu, log, oracle_expert_weights,
-                       oracle_tokens, quantize_weights_gpu, rel_err, require_gpu, to_dev)
+                       oracle_tokens, pack_reference, quantize_weights_gpu, rel_err, require_gpu, to_dev)
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2
@@ -120,6 +120,18 @@ def test_quant_weight_deepseek_matrix_bit_exact(moe):
     q_ref, s_ref = oracle.quantize_weight(f.cpu().numpy())
     assert np.array_equal(s.cpu().numpy(), s_ref)
     assert np.array_equal(q.cpu().numpy(), q_ref)
+
+
+@pytest.mark.parametrize("n,rows,cols", [(1, 16, 128), (3, 32, 384), (2, 256, 256), (1, 2048, 7168)])
+def test_pack_weight_matches_layout_definition(moe, n, rows, cols):
+    """moe_pack_weight is a pure byte permutation; every byte lands where the layout definition puts it."""
+    rng = np.random.default_rng(rows + cols)
+    q = rng.integers(0, 256, size=(n, rows, cols), dtype=np.uint8)
+    dq = to_dev(q)
+    packed = torch.full_like(dq, 0xA5)
+    moe.moe_pack_weight(dq, packed)
+    torch.cuda.synchronize()
+    assert np.array_equal(packed.cpu().numpy(), pack_reference(q))
 
 
 # --------------------------------------------------------------- permute
@@ -229,8 +241,9 @@ def test_layer_parity_small(moe, case, regime):
     log(f"layer {case} {regime}")
     ow = oracle.prepare_weights(wg, wu, wd)
     dweights = quantize_weights_gpu(moe, wg, wu, wd)
-    for dq, rq in zip(dweights, ow):
-        assert np.array_equal(dq.cpu().numpy(), rq)
+    for j, (dq, rq) in enumerate(zip(dweights, ow)):
+        # codes are packed into operand tiles on the device, scales stay row-major
+        assert np.array_equal(dq.cpu().numpy(), pack_reference(rq) if j % 2 == 0 else rq)
     ref, inter = oracle.moe_layer(x, ids, wts, ow, want_intermediates=True)
     buf = _gpu_layer(moe, w, x, ids, wts, dweights, rg)
     assert int(buf.dev_status.item()) == 0
