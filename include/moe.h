@@ -122,13 +122,12 @@ moe_status_t moe_quant_weight(const float* w, int32_t n_mats, int32_t rows, int3
  *
  * Each [rows, cols] matrix is cut into 16-row x 128-column tiles of 2048
  * bytes, stored row-group major: tile (g, b) starts at byte
- * (g * cols/128 + b) * 2048 of the matrix.  Inside a tile, byte
- * h*1024 + 16*l + j (h in {0,1}, l in [0,64), j in [0,16)) holds
- *   q[16g + (l % 16), 128b + 64h + 16(l / 16) + j],
- * the order in which the 64 lanes of a wave feed one 16x16x128 FP8 MFMA
- * operand, so the kernels read each tile with two fully contiguous 1 KB
- * wave loads.  A matrix keeps its size (rows*cols bytes) and an expert's
- * matrix stays contiguous.
+ * (g * cols/128 + b) * 2048 of the matrix.  Inside a tile, the 16 bytes at
+ *   1024*h + 512*(kq % 2) + 256*(kq / 2) + 16*r      (h in {0,1}, kq in [0,4), r in [0,16))
+ * hold q[16g + r, 128b + 64h + 16kq + j] for j = 0..15: the orders in which
+ * the 64 lanes of a wave feed a 16x16x128 and a 32x32x64 FP8 MFMA operand
+ * both map to two fully contiguous 1 KB wave loads per operand.  A matrix
+ * keeps its size (rows*cols bytes) and an expert's matrix stays contiguous.
  *
  * q: device e4m3 [n_mats, rows, cols] row-major (from moe_quant_weight).
  * packed: device, n_mats*rows*cols bytes, not overlapping q.  rows a

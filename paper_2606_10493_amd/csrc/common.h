@@ -23,21 +23,18 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 //   * otherwise re-bias the exponent (127 -> 7) and round the 23-bit
 //     mantissa to 3 bits by adding 0x7FFFF plus the kept LSB before dropping
 //     20 bits; a mantissa carry moves into the exponent field by itself.
+// Both candidates are computed and the right one selected (no branches:
+// this runs per element in the GEMM epilogues); the subnormal candidate is
+// formed from min(|v|, 1) so that its conversion stays in range.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t encode_e4m3(float v) {
   const uint32_t u = __float_as_uint(v);
   const uint32_t sign = (u >> 24) & 0x80u;
   const uint32_t a = u & 0x7fffffffu;
   const float fa = __uint_as_float(a);
-  uint32_t code;
-  if (!(fa < kE4M3Max)) {
-    code = 0x7eu;
-  } else if (a < 0x3c800000u) {  // 2^-6
-    code = (uint32_t)__builtin_rintf(fa * 512.0f);
-  } else {
-    const uint32_t r = a + 0x7ffffu + ((a >> 20) & 1u);
-    code = (r >> 20) - (120u << 3);
-  }
+  const uint32_t sub = (uint32_t)__builtin_rintf(fminf(fa, 1.0f) * 512.0f);
+  const uint32_t nrm = ((a + 0x7ffffu + ((a >> 20) & 1u)) >> 20) - (120u << 3);
+  const uint32_t code = (fa < kE4M3Max) ? (a < 0x3c800000u ? sub : nrm) : 0x7eu;  // 2^-6; NaN saturates
   return code | sign;
 }
 
@@ -45,8 +42,8 @@ __device__ __forceinline__ uint32_t encode_e4m3(float v) {
 // the sign only).  x / s is the correctly rounded fp32 quotient (the library
 // is built with correctly rounded fp32 division).
 __device__ __forceinline__ uint32_t quantize_e4m3(float x, float s) {
-  if (s > 0.0f) return encode_e4m3(x / s);
-  return (__float_as_uint(x) >> 24) & 0x80u;
+  const uint32_t code = encode_e4m3(x / s);
+  return s > 0.0f ? code : ((__float_as_uint(x) >> 24) & 0x80u);
 }
 
 // fp32 -> bf16 bits, round to nearest even (finite inputs).
@@ -74,11 +71,18 @@ __device__ __forceinline__ v4f mfma_f8_16x16x128(const v8i& a, const v8i& b) {
 }
 
 // Packed weight layout (moe_pack_weight): a [rows, K] e4m3 matrix is stored
-// as 16-row x 128-K operand tiles of 2048 bytes, tile (g, b) at
-// (g * K/128 + b) * 2048.  Inside a tile, byte h*1024 + 16*l + j holds
-// row 16g + (l & 15), K index 128b + 64h + 16(l >> 4) + j: lane l of a wave
-// finds its whole operand at 16*l and 1024 + 16*l, so one 16-byte load per
-// lane reads 1 KB of contiguous memory.
+// as 16-row x 128-K tiles of 2048 bytes, tile (g, b) at (g * K/128 + b) *
+// 2048.  Inside a tile, the 16 bytes at
+//   packed_lane_offset(h, kq, r) = 1024 h + 512 (kq & 1) + 256 (kq >> 1) + 16 r
+// hold row 16g + r, K indices 128b + 64h + 16kq + [0, 16) (h in {0,1},
+// kq in [0,4), r in [0,16)).  A wave reads one operand as two loads that
+// each cover 1 KB of contiguous memory, for both MFMA shapes the library
+// uses: 16x16x128 (lane l: r = l % 16, kq = l / 16, h = the two halves of
+// its 32 bytes) and 32x32x64 (lane l: row l % 32 of two consecutive 16-row
+// groups, K bytes 64h + 32 (l / 32) + [0, 32), i.e. kq = 2 (l / 32) + part).
+__device__ __forceinline__ int packed_lane_offset(int h, int kq, int r) {
+  return 1024 * h + 512 * (kq & 1) + 256 * (kq >> 1) + 16 * r;
+}
 constexpr int kTileBytes = 16 * MOE_BLOCK;
 
 __device__ __forceinline__ v8i join_v8i(const uint4& lo, const uint4& hi) {
@@ -94,7 +98,8 @@ __device__ __forceinline__ v8i load_v8i_ksplit(const uint8_t* p) {
   return join_v8i(*reinterpret_cast<const uint4*>(p), *reinterpret_cast<const uint4*>(p + 64));
 }
 
-// Operand from a packed weight tile: p points at byte 16*l of the tile.
+// 16x16x128 operand from a packed weight tile: p points at
+// packed_lane_offset(0, kq, r) of the tile (the second half is 1024 further).
 __device__ __forceinline__ v8i load_v8i_packed(const uint8_t* p) {
   return join_v8i(*reinterpret_cast<const uint4*>(p), *reinterpret_cast<const uint4*>(p + 1024));
 }

@@ -130,8 +130,8 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int64_t grp = ((int64_t)e * p.N + n0 + nt * 16) / 16;
-      wrow0[nt] = p.w0 + grp * nb * kTileBytes + lane * 16;
-      wrow1[nt] = GATEUP ? p.w1 + grp * nb * kTileBytes + lane * 16 : nullptr;
+      wrow0[nt] = p.w0 + grp * nb * kTileBytes + packed_lane_offset(0, kq, r);
+      wrow1[nt] = GATEUP ? p.w1 + grp * nb * kTileBytes + packed_lane_offset(0, kq, r) : nullptr;
     }
     const int64_t srow = ((int64_t)e * (p.N / kBlock) + n0 / kBlock) * nb;
 

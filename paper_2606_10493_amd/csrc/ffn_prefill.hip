@@ -4,29 +4,36 @@
 // to FP8, FP8 x FP8 products with FP32 accumulation; gate and up fused with
 // SiLU(gate)*up as in the paper's stage one, down after it).
 //
-// The products are formed transposed, D = W x X^T: the MFMA's A operand is
-// 16 weight rows (output channels), its B operand 16 expert rows (tokens).
-// A lane's four results then share one token and lie inside one 128-channel
-// weight-scale block, so the per-block scale of a result is (the lane's
-// token scale) x (a wave-uniform weight scale).
+// The products are formed transposed, D = W x X^T, with the MFMA 32x32x64:
+// its A operand is 32 weight rows (output channels), its B operand 32
+// expert rows (tokens), two instructions per 128-K scale block.  A lane's
+// 16 results then share one token and lie inside one 128-channel weight-
+// scale block (GATEUP: eight gate, eight up), so the per-block scale of a
+// result is (the lane's token scale) x (a wave-uniform weight scale), and
+// the promotion into the fp32 accumulators costs 16 FMAs per two MFMAs: few
+// enough VALU operations for the matrix core to stay busy (measured on
+// gfx950: up to about 9 independent VALU operations per 32x32x64 MFMA issue
+// alongside it at full rate, against 4 per 16x16x128).
 //
-// Tile: 256 weight rows x 128 expert rows x one 128-K scale block per step,
-// 512 threads (8 waves).  Wave w owns 32 weight rows (two 16-row MFMA
-// operands) against all 128 expert rows (eight 16-row operands): 16 MFMA
-// 16x16x128 per K step, each promoted into fp32 accumulators with one FMA
-// per result.  The weights are packed in operand tiles (moe_pack_weight),
-// so they go from global memory straight into the MFMA operand registers
-// with two contiguous 1 KB wave loads per operand (no wave shares them),
-// through a ring of kRing K blocks loaded kRing - 1 steps ahead.  Only the
-// expert rows, which all waves read, are staged through LDS (double
-// buffered, one barrier per K step; loaded as whole 128-byte row pieces),
-// and their scales sit in LDS transposed, [K block][row].
+// Tile: 256 weight rows x 128 expert rows x one 128-K block per step, 512
+// threads (8 waves).  Wave w owns 32 weight rows against all 128 expert rows
+// (four B operands): 8 MFMA per K step.  The weights are packed in operand
+// tiles (moe_pack_weight), so they go from global memory straight into the
+// MFMA operand registers with 1 KB-contiguous wave loads (no wave shares
+// them), through a ring of kRing K blocks loaded kRing - 1 steps ahead.
+// Only the expert rows, which all waves read, are staged through LDS
+// (three stages, 16-byte chunks XOR-swizzled by row) and their scales sit
+// in LDS transposed, [K block][row].  Waves 0-3 and 4-7 run the K loop half
+// a step apart (a memory phase and a compute phase per step, a barrier after
+// each), so that on every SIMD one wave feeds the matrix core while the
+// other loads: with all eight waves in step, both waves of a SIMD wait for
+// LDS together and then queue for the matrix core together.
 //
-// GATEUP: wave w's rows are gate rows nt*128 + 16w + [0, 16) and the same up
-// rows, so a workgroup holds one full 128-wide block of h: its epilogue
-// computes h = SiLU(G) * U, the per-row amax of the block (lanes, then the
-// eight waves through LDS), the scale sh = amax / 448 and the e4m3 codes qh,
-// staged through LDS and written as 16-byte rows.
+// GATEUP: wave w's rows are gate rows nt*128 + 16w + [0, 16) followed by the
+// same up rows, so a workgroup holds one full 128-wide block of h: its
+// epilogue computes h = SiLU(G) * U, the per-row amax of the block (lanes,
+// then the eight waves through LDS), the scale sh = amax / 448 and the e4m3
+// codes qh, staged through LDS and written as 16-byte rows.
 // DOWN: wave w's rows are W_down rows nt*256 + 32w + [0, 32); the epilogue
 // writes fp32 in 16-byte pieces.
 //
@@ -47,14 +54,15 @@ namespace {
 constexpr int kBM = 128;                // expert rows (tokens) per tile
 constexpr int kBN = 256;                // weight rows per tile
 constexpr int kThreads = 512;           // 8 waves x 32 weight rows
-constexpr int kLdsRow = kBlock + 16;    // padded LDS row (bytes) to spread banks
-constexpr int kStage = kBM * kLdsRow;   // one K block of the expert rows
+constexpr int kLdsRow = kBlock;         // LDS row (bytes); 16-byte chunks XOR-swizzled, see swz()
+constexpr int kHalf = kBM * kLdsRow;    // one K block of the expert rows (one LDS stage)
+constexpr int kStages = 3;              // LDS stages of the ping-pong pipeline
 constexpr int kSaStride = kBM + 1;      // floats per K block of the row-scale table
-constexpr int kRing = 4;                // weight K blocks in registers
+constexpr int kRing = 3;                // weight K blocks in registers
 constexpr int kXcd = 8;
-constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
 struct PrefillArgs {
   const uint8_t* a;           // e4m3 activations [a_rows, K]
@@ -87,21 +95,15 @@ __global__ __launch_bounds__(1024) void prefill_tiles_kernel(const int32_t* __re
   if (e == 0) mtile_start[E] = total;
 }
 
-// Raw buffer view of [base, base + bytes): loads outside it return zero.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_view(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kRsrcWord3);
-}
+// LDS byte offset of 16-byte chunk c (0..7) of row `row` in a 128-byte-row
+// tile: the chunk index is XOR-ed with row % 8, so the 16 rows that one
+// operand read touches spread over all LDS banks (measured on gfx950: a
+// swizzled b128 read costs what a contiguous one does, a 144-byte padded
+// row layout about 1.7 times as much).
+__device__ __forceinline__ int swz(int row, int c) { return row * kLdsRow + ((c ^ (row & 7)) << 4); }
 
-// One MFMA operand of K block b from a packed weight tile: voff addresses
-// byte 16*lane of the operand's first tile, the tiles of one 16-row group
-// follow each other along K.
-__device__ __forceinline__ v8i load_operand(__amdgpu_buffer_rsrc_t r, uint32_t voff, int b) {
-  const u32x4 lo = __builtin_amdgcn_raw_buffer_load_b128(r, voff, b * kTileBytes, 0);
-  const u32x4 hi = __builtin_amdgcn_raw_buffer_load_b128(r, voff + 1024, b * kTileBytes, 0);
-  v8i o;
-  o[0] = lo[0]; o[1] = lo[1]; o[2] = lo[2]; o[3] = lo[3];
-  o[4] = hi[0]; o[5] = hi[1]; o[6] = hi[2]; o[7] = hi[3];
-  return o;
+__device__ __forceinline__ v16f mfma_f8_32x32x64(const v8i& a, const v8i& b, const v16f& c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
 }
 
 template <bool GATEUP>
@@ -109,10 +111,12 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ int arow[kBM];
   __shared__ float rowmax[8][kBM];
+  __shared__ int tile_info[3];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int r = lane & 15, kq = lane >> 4;
+  const int r32 = lane & 31;  // operand row (A) / column (B) of this lane
+  const int g2 = lane >> 5;   // K half of a 64-K MFMA slice this lane supplies
 
   // XCD-major work item over the real items (the grid is an upper bound):
   // XCD x takes items [x*per, (x+1)*per) in order.
@@ -124,18 +128,29 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   if (item >= real) return;
   const int64_t mt_global = item / p.n_tiles;
   const int nt = (int)(item % p.n_tiles);
-  // Expert owning this m-tile: last e with mtile_start[e] <= mt_global.
-  int lo = 0, hi = p.E - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (p.mtile_start[mid] <= mt_global) lo = mid; else hi = mid - 1;
+  // Expert owning this m-tile: the e with mtile_start[e] <= mt_global <
+  // mtile_start[e+1] (empty experts own no m-tile), found by all threads in
+  // one round of loads; the owner also publishes the tile's row range.
+  if (tid == 0) tile_info[0] = -1;
+  __syncthreads();
+  for (int x = tid; x < p.E; x += kThreads) {
+    const int s0 = p.mtile_start[x], s1 = p.mtile_start[x + 1];
+    const int o0 = p.offsets[x], o1 = p.offsets[x + 1];
+    if (s0 <= mt_global && mt_global < s1) {
+      const int first = o0 + (int)(mt_global - s0) * kBM;
+      tile_info[0] = x;
+      tile_info[1] = first;
+      tile_info[2] = min(kBM, o1 - first);
+    }
   }
-  const int e = lo;
-  const int m0 = p.offsets[e] + (int)(mt_global - p.mtile_start[e]) * kBM;  // first sorted row of the tile
-  const int mc = min(kBM, p.offsets[e + 1] - m0);                            // rows in the tile
+  __syncthreads();
+  const int e = tile_info[0];
+  if (e < 0) return;            // no owner: inconsistent offsets, nothing to compute
+  const int m0 = tile_info[1];  // first sorted row of the tile
+  const int mc = tile_info[2];  // rows in the tile
   const int nb = p.K / kBlock;
 
-  float* sa_lds = reinterpret_cast<float*>(smem + 2 * kStage);  // [nb][kSaStride]
+  float* sa_lds = reinterpret_cast<float*>(smem + kStages * kHalf);  // [nb][kSaStride]
   float* sw_lds = sa_lds + nb * kSaStride;                       // [2][nb]
 
   for (int i = tid; i < kBM; i += kThreads) {
@@ -172,154 +187,215 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     const int row = c >> 3, col = (c & 7) * 16;
     const int ar = arow[row];
     a_src[i] = p.a + (int64_t)(ar >= 0 ? ar : 0) * p.K + col;
-    a_dst[i] = row * kLdsRow + col;
+    a_dst[i] = swz(row, c & 7);
   }
 
-  // This wave's two 16-row weight operands (f = 0, 1), as buffer views of
-  // one expert's packed matrix, and the LDS row of their weight scales.
-  const uint32_t wbytes = (uint32_t)p.N * (uint32_t)p.K;
-  __amdgpu_buffer_rsrc_t wv[2];
-  uint32_t w_off[2];
-#pragma unroll
-  for (int f = 0; f < 2; ++f) {
-    // 16-row group of the operand: GATEUP rows nt*128 + 16w, DOWN rows nt*256 + 32w + 16f.
-    const int g = GATEUP ? nt * (kBlock / 16) + wave : nt * (kBN / 16) + wave * 2 + f;
-    wv[f] = buffer_view((GATEUP && f ? p.w1 : p.w0) + (int64_t)e * wbytes, wbytes);
-    w_off[f] = (uint32_t)g * (uint32_t)nb * kTileBytes + lane * 16;
+  // This wave's 32-row weight operand: rows 0-15 and 16-31 are two packed
+  // 16-row groups (GATEUP: the gate and the up group nt*8 + w; DOWN: groups
+  // nt*16 + 2w and + 1).  Lane l reads row l % 32, K bytes 64h + 32 g2 +
+  // [0, 32) of each block, i.e. kq = 2 g2 and 2 g2 + 1 of the packed tile.
+  const uint8_t* wsrc;
+  {
+    const int64_t ebase = (int64_t)e * p.N * p.K;
+    const int64_t grp = GATEUP ? (int64_t)nt * (kBlock / 16) + wave : (int64_t)nt * (kBN / 16) + 2 * wave + (r32 >> 4);
+    const uint8_t* wm = (GATEUP && r32 >= 16) ? p.w1 : p.w0;
+    wsrc = wm + ebase + grp * nb * kTileBytes + packed_lane_offset(0, 2 * g2, r32 & 15);
   }
-  const float* swf0 = sw_lds + (GATEUP ? 0 : (wave >> 2)) * nb;
-  const float* swf1 = sw_lds + (GATEUP ? 1 : (wave >> 2)) * nb;
-
-  v4f acc[2][8];
+  const float* swf0 = sw_lds + (GATEUP ? 0 : (wave >> 2)) * nb;  // scale of result rows 0-15
+  const float* swf1 = sw_lds + (GATEUP ? 1 : (wave >> 2)) * nb;  // scale of result rows 16-31
+  // LDS offsets of this lane's B operand pieces in expert row r32: K chunks
+  // 4h + 2 g2 + part; rows 32j + r32 share row % 8, hence the swizzle.
+  int bo[2][2];
 #pragma unroll
-  for (int f = 0; f < 2; ++f)
+  for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[f][i] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int part = 0; part < 2; ++part) bo[h][part] = swz(r32, 4 * h + 2 * g2 + part);
 
-  v8i wr[kRing][2];
-  u32x4 ra[kRing][2];  // ext vectors: an array of HIP's uint4 structs would not stay in registers
-#define MOE_PF_WLOAD(SLOT, BLK)                        \
-  do {                                                 \
-    wr[SLOT][0] = load_operand(wv[0], w_off[0], BLK);  \
-    wr[SLOT][1] = load_operand(wv[1], w_off[1], BLK);  \
-  } while (0)
-#define MOE_PF_ALOAD(SLOT, BLK)                                                         \
-  do {                                                                                  \
-    ra[SLOT][0] = *reinterpret_cast<const u32x4*>(a_src[0] + (int64_t)(BLK) * kBlock);  \
-    ra[SLOT][1] = *reinterpret_cast<const u32x4*>(a_src[1] + (int64_t)(BLK) * kBlock);  \
-  } while (0)
-#define MOE_PF_ASTORE(SLOT, STAGE)                                                         \
+  // acc[j][i]: weight row 8*(i/4) + 4*g2 + i%4 of the operand, expert row 32j + r32.
+  v16f acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[j][i] = 0.0f;
+
+  v8i wr[kRing][2];  // [slot][K half]
+  u32x4 ra[2];       // this thread's two 16-byte chunks of one K block of expert rows (ext vectors stay in VGPRs)
+  v8i bx[4][2];      // B operands of the step: [expert-row operand][K half]
+  float sa[4], sw0 = 0.0f, sw1 = 0.0f;
+#define MOE_PF_WLOAD(SLOT, BLK)                                                            \
   do {                                                                                     \
-    uint8_t* st_ = smem + (STAGE) * kStage;                                                \
-    *reinterpret_cast<u32x4*>(st_ + a_dst[0]) = ra[SLOT][0];                               \
-    *reinterpret_cast<u32x4*>(st_ + a_dst[1]) = ra[SLOT][1];                               \
+    const uint8_t* w_ = wsrc + (int64_t)(BLK) * kTileBytes;                                \
+    wr[SLOT][0] = join_v8i(*reinterpret_cast<const uint4*>(w_),                            \
+                           *reinterpret_cast<const uint4*>(w_ + 512));                     \
+    wr[SLOT][1] = join_v8i(*reinterpret_cast<const uint4*>(w_ + 1024),                     \
+                           *reinterpret_cast<const uint4*>(w_ + 1536));                    \
   } while (0)
-  // One K step b using register slot U (= b % kRing).  The loads of block
-  // b + kRing - 1 (expert rows and weights; clamped to the last block, a
-  // harmless reload) go out first; scheduling barriers keep them above the
-  // math and the LDS store of block b + 1 (loaded kRing - 2 steps ago) below
-  // it.
-#define MOE_PF_STEP(U, B)                                                                  \
+  // Expert rows of K block BLK (clamped to the last block, a harmless
+  // reload) into registers, and from there into its LDS stage BLK % 3.
+#define MOE_PF_ALOAD(BLK)                                                                  \
   do {                                                                                     \
-    const int b_ = (B);                                                                    \
-    const int bl_ = b_ + kRing - 1 < nb ? b_ + kRing - 1 : nb - 1;                         \
-    MOE_PF_ALOAD(((U) + kRing - 1) % kRing, bl_);                                          \
-    MOE_PF_WLOAD(((U) + kRing - 1) % kRing, bl_);                                          \
+    const int blk_ = (BLK) < nb ? (BLK) : nb - 1;                                          \
+    ra[0] = *reinterpret_cast<const u32x4*>(a_src[0] + (int64_t)blk_ * kBlock);            \
+    ra[1] = *reinterpret_cast<const u32x4*>(a_src[1] + (int64_t)blk_ * kBlock);            \
+  } while (0)
+#define MOE_PF_ASTORE(BLK)                                                                 \
+  do {                                                                                     \
+    uint8_t* st_ = smem + ((BLK) % 3) * kHalf;                                             \
+    *reinterpret_cast<u32x4*>(st_ + a_dst[0]) = ra[0];                                     \
+    *reinterpret_cast<u32x4*>(st_ + a_dst[1]) = ra[1];                                     \
+  } while (0)
+#define MOE_PF_BREAD(J, SB)                                                                \
+  do {                                                                                     \
+    _Pragma("unroll") for (int h = 0; h < 2; ++h)                                          \
+      bx[J][h] = join_v8i(*reinterpret_cast<const uint4*>((SB) + bo[h][0] + (J) * 32 * kLdsRow), \
+                          *reinterpret_cast<const uint4*>((SB) + bo[h][1] + (J) * 32 * kLdsRow)); \
+  } while (0)
+#define MOE_PF_PROMOTE(J, D)                                                               \
+  do {                                                                                     \
+    const float s0_ = sa[J] * sw0, s1_ = sa[J] * sw1;                                      \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i) acc[J][i] += (D)[i] * s0_;               \
+    _Pragma("unroll") for (int i = 8; i < 16; ++i) acc[J][i] += (D)[i] * s1_;              \
+  } while (0)
+  // Each K step j is a memory phase and a compute phase, each ended by a
+  // workgroup barrier.  Waves 4-7 run one phase behind waves 0-3 (they pass
+  // one extra barrier first), so on every SIMD one wave issues MFMAs while
+  // the other issues loads and LDS traffic, instead of both doing the same
+  // thing at once.
+  // Memory phase of step j: store K block j + 1 (loaded one memory phase
+  // earlier) into its stage, load block j + 2 and weight block j + 2, read
+  // the step's scales and its first two B operands.  The compute phase reads
+  // the other two B operands while the first ones' MFMAs run.
+  // Stage safety (three stages, block t in stage t % 3): block j is complete
+  // once both halves of the workgroup finished memory phase j - 1, which the
+  // lagging half does one phase before the leading half starts memory phase
+  // j; its stage is rewritten (block j + 3) in memory phase j + 2, after the
+  // lagging half's compute phase j.
+#define MOE_PF_MEM(U, J)                                                                   \
+  do {                                                                                     \
+    const int j_ = (J);                                                                    \
+    MOE_PF_ASTORE(j_ + 1);                                                                 \
+    MOE_PF_ALOAD(j_ + 2);                                                                  \
+    MOE_PF_WLOAD(((U) + kRing - 1) % kRing, j_ + kRing - 1 < nb ? j_ + kRing - 1 : nb - 1); \
     __builtin_amdgcn_sched_barrier(0);                                                     \
-    const uint8_t* sB = smem + (b_ & 1) * kStage + r * kLdsRow + kq * 16;                  \
-    const float* sa_b = sa_lds + b_ * kSaStride + r;                                       \
-    const float sw0 = swf0[b_], sw1 = swf1[b_];                                            \
-    /* products of operand i are promoted while those of i + 1 run */                      \
-    v8i bx = load_v8i_ksplit(sB);                                                          \
-    v4f p0 = mfma_f8_16x16x128(wr[U][0], bx);                                              \
-    v4f p1 = mfma_f8_16x16x128(wr[U][1], bx);                                              \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                        \
-      v4f n0, n1;                                                                          \
-      if (i < 7) {                                                                         \
-        bx = load_v8i_ksplit(sB + (i + 1) * 16 * kLdsRow);                                 \
-        n0 = mfma_f8_16x16x128(wr[U][0], bx);                                              \
-        n1 = mfma_f8_16x16x128(wr[U][1], bx);                                              \
-      }                                                                                    \
-      const float sa = sa_b[i * 16];                                                       \
-      const float s0 = sa * sw0, s1 = sa * sw1;                                            \
-      _Pragma("unroll") for (int q = 0; q < 4; ++q) {                                      \
-        acc[0][i][q] += p0[q] * s0;                                                        \
-        acc[1][i][q] += p1[q] * s1;                                                        \
-      }                                                                                    \
-      if (i < 7) { p0 = n0; p1 = n1; }                                                     \
-    }                                                                                      \
+    const uint8_t* sB_ = smem + (j_ % 3) * kHalf;                                          \
+    sw0 = swf0[j_];                                                                        \
+    sw1 = swf1[j_];                                                                        \
+    _Pragma("unroll") for (int q = 0; q < 4; ++q) sa[q] = sa_lds[j_ * kSaStride + r32 + 32 * q]; \
+    MOE_PF_BREAD(0, sB_);                                                                  \
+    MOE_PF_BREAD(1, sB_);                                                                  \
     __builtin_amdgcn_sched_barrier(0);                                                     \
-    MOE_PF_ASTORE(((U) + 1) % kRing, (b_ + 1) & 1);                                        \
+  } while (0)
+  // The two MFMAs of one operand and K block are chained (the second adds
+  // onto the first), and a chained MFMA waits for its predecessor to finish;
+  // so operands are issued in pairs, each chained MFMA two MFMAs after its
+  // predecessor, and a pair is promoted while the next pair runs.
+#define MOE_PF_COMP(U, J)                                                                  \
+  do {                                                                                     \
+    const uint8_t* sB_ = smem + ((J) % 3) * kHalf;                                         \
+    v16f d[4];                                                                             \
+    _Pragma("unroll") for (int q = 0; q < 4; ++q) d[q] = v16f{};                           \
+    d[0] = mfma_f8_32x32x64(wr[U][0], bx[0][0], d[0]);                                     \
+    d[1] = mfma_f8_32x32x64(wr[U][0], bx[1][0], d[1]);                                     \
+    MOE_PF_BREAD(2, sB_);                                                                  \
+    MOE_PF_BREAD(3, sB_);                                                                  \
+    d[0] = mfma_f8_32x32x64(wr[U][1], bx[0][1], d[0]);                                     \
+    d[1] = mfma_f8_32x32x64(wr[U][1], bx[1][1], d[1]);                                     \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+    d[2] = mfma_f8_32x32x64(wr[U][0], bx[2][0], d[2]);                                     \
+    d[3] = mfma_f8_32x32x64(wr[U][0], bx[3][0], d[3]);                                     \
+    MOE_PF_PROMOTE(0, d[0]);                                                               \
+    d[2] = mfma_f8_32x32x64(wr[U][1], bx[2][1], d[2]);                                     \
+    d[3] = mfma_f8_32x32x64(wr[U][1], bx[3][1], d[3]);                                     \
+    MOE_PF_PROMOTE(1, d[1]);                                                               \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+    MOE_PF_PROMOTE(2, d[2]);                                                               \
+    MOE_PF_PROMOTE(3, d[3]);                                                               \
+    __builtin_amdgcn_sched_barrier(0);                                                     \
+  } while (0)
+#define MOE_PF_STEP(U, J)                                                                  \
+  do {                                                                                     \
+    MOE_PF_MEM(U, J);                                                                      \
+    __syncthreads();                                                                       \
+    MOE_PF_COMP(U, J);                                                                     \
     __syncthreads();                                                                       \
   } while (0)
 
+  MOE_PF_ALOAD(0);
 #pragma unroll
-  for (int s = 0; s < kRing - 1; ++s) {
-    MOE_PF_ALOAD(s, s < nb ? s : nb - 1);
-    MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
-  }
-  MOE_PF_ASTORE(0, 0);
+  for (int s = 0; s < kRing - 1; ++s) MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
+  MOE_PF_ASTORE(0);
+  MOE_PF_ALOAD(1);
   __syncthreads();
+  if (wave >= 4) __syncthreads();  // the lagging half starts one phase later (wave-uniform branch)
 
-  int b0 = 0;
-  for (; b0 + kRing <= nb; b0 += kRing) {
-    MOE_PF_STEP(0, b0);
-    MOE_PF_STEP(1, b0 + 1);
-    MOE_PF_STEP(2, b0 + 2);
-    MOE_PF_STEP(3, b0 + 3);
+  // kRing = 3 weight slots: three steps per loop iteration keep every slot
+  // index static.
+  int j0 = 0;
+  for (; j0 + kRing <= nb; j0 += kRing) {
+    MOE_PF_STEP(0, j0);
+    MOE_PF_STEP(1, j0 + 1);
+    MOE_PF_STEP(2, j0 + 2);
   }
-  if (b0 < nb) MOE_PF_STEP(0, b0);
-  if (b0 + 1 < nb) MOE_PF_STEP(1, b0 + 1);
-  if (b0 + 2 < nb) MOE_PF_STEP(2, b0 + 2);
+  if (j0 < nb) MOE_PF_STEP(0, j0);
+  if (j0 + 1 < nb) MOE_PF_STEP(1, j0 + 1);
+  if (wave < 4) __syncthreads();   // pairs with the lagging half's last barrier
 #undef MOE_PF_WLOAD
 #undef MOE_PF_ALOAD
 #undef MOE_PF_ASTORE
+#undef MOE_PF_PROMOTE
+#undef MOE_PF_BREAD
+#undef MOE_PF_MEM
+#undef MOE_PF_COMP
 #undef MOE_PF_STEP
 
   if (!GATEUP) {
-    // y[m0 + t][nt*256 + 32w + 16f + 4kq + q] for expert row t = 16i + r.
+    // y[m0 + t][nt*256 + 32w + 8*(i/4) + 4*g2 + i%4] for expert row t = 32j + r32.
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int t = i * 16 + r;
+    for (int j = 0; j < 4; ++j) {
+      const int t = j * 32 + r32;
       if (t < mc) {
-        float* dst = p.y + (int64_t)(m0 + t) * p.N + nt * kBN + wave * 32 + kq * 4;
+        float* dst = p.y + (int64_t)(m0 + t) * p.N + nt * kBN + wave * 32 + g2 * 4;
 #pragma unroll
-        for (int f = 0; f < 2; ++f) *reinterpret_cast<v4f*>(dst + f * 16) = acc[f][i];
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<v4f*>(dst + q * 8) = v4f{acc[j][4 * q], acc[j][4 * q + 1], acc[j][4 * q + 2], acc[j][4 * q + 3]};
       }
     }
     return;
   }
 
-  // GATEUP epilogue: h = SiLU(G) * U for channels 16w + 4kq + q of rows
-  // t = 16i + r; per-row amax over the lane's 4 channels, the 4 lanes of
-  // the row (kq) and the 8 waves.
-  float h[8][4];
+  // GATEUP epilogue: h = SiLU(G) * U for channels 16w + 8*(i/4) + 4*g2 + i%4
+  // (i < 8; the up value is acc[j][i + 8]) of rows t = 32j + r32; per-row
+  // amax over the lane's 8 channels, the other K-half lane (g2) and the 8
+  // waves.
+  float hv[4][8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int j = 0; j < 4; ++j) {
     float mx = 0.0f;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      h[i][q] = silu_mul(acc[0][i][q], acc[1][i][q]);
-      mx = fmaxf(mx, fabsf(h[i][q]));
+    for (int i = 0; i < 8; ++i) {
+      hv[j][i] = silu_mul(acc[j][i], acc[j][i + 8]);
+      mx = fmaxf(mx, fabsf(hv[j][i]));
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    if (kq == 0) rowmax[wave][i * 16 + r] = mx;
+    if (g2 == 0) rowmax[wave][j * 32 + r32] = mx;
   }
   __syncthreads();
-  uint8_t* qtile = smem;  // [kBM][kLdsRow], the K-loop buffers are free now
+  uint8_t* qtile = smem;  // [kBM][kLdsRow] swizzled, the K-loop buffers are free now
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int t = i * 16 + r;
+  for (int j = 0; j < 4; ++j) {
+    const int t = j * 32 + r32;
     float amax = rowmax[0][t];
 #pragma unroll
     for (int w = 1; w < 8; ++w) amax = fmaxf(amax, rowmax[w][t]);
     const float s = amax / kE4M3Max;
-    uint32_t packed = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) packed |= quantize_e4m3(h[i][q], s) << (8 * q);
-    *reinterpret_cast<uint32_t*>(qtile + t * kLdsRow + wave * 16 + kq * 4) = packed;
-    if (wave == 0 && kq == 0 && t < mc) p.sh[(int64_t)(m0 + t) * (p.N / kBlock) + nt] = s;
+    for (int half = 0; half < 2; ++half) {
+      uint32_t packed = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) packed |= quantize_e4m3(hv[j][4 * half + q], s) << (8 * q);
+      *reinterpret_cast<uint32_t*>(qtile + swz(t, wave) + 8 * half + 4 * g2) = packed;
+    }
+    if (wave == 0 && g2 == 0 && t < mc) p.sh[(int64_t)(m0 + t) * (p.N / kBlock) + nt] = s;
   }
   __syncthreads();
   // 128 rows x 128 bytes = 1024 16-byte chunks, 2 per thread.
@@ -329,7 +405,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     const int row = c >> 3, col = (c & 7) * 16;
     if (row < mc)
       *reinterpret_cast<uint4*>(p.qh + (int64_t)(m0 + row) * p.N + nt * kBlock + col) =
-          *reinterpret_cast<const uint4*>(qtile + row * kLdsRow + col);
+          *reinterpret_cast<const uint4*>(qtile + swz(row, c & 7));
   }
 }
 
@@ -340,7 +416,7 @@ moe_status_t launch_prefill(const PrefillArgs& a, int64_t max_mtiles, hipStream_
   if (grid > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: grid too large");
   if ((int64_t)a.N * a.K > 0x7fffffff)
     return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: one expert matrix (%d x %d) exceeds 2 GiB", a.N, a.K);
-  const size_t lds = 2 * (size_t)kStage + sizeof(float) * ((size_t)kSaStride + 2) * (a.K / kBlock);
+  const size_t lds = (size_t)kStages * kHalf + sizeof(float) * ((size_t)kSaStride + 2) * (a.K / kBlock);
   if (lds > 150 * 1024) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: K=%d needs %zu bytes of LDS", a.K, lds);
   const hipError_t ae = hipFuncSetAttribute(reinterpret_cast<const void*>(&ffn_prefill_kernel<GATEUP>),
                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -125,18 +125,20 @@ moe_status_t quant_rows(const InT* x, int32_t rows, int32_t cols, uint8_t* q, fl
 }
 
 // Row-major e4m3 [total_rows, cols] -> packed operand tiles (the layout is
-// described with kTileBytes).  One thread moves one 16-byte chunk: output
-// chunk c is lane l = c % 64 of half h = (c / 64) % 2 of tile c / 128.
+// described with packed_lane_offset).  One thread moves one 16-byte chunk:
+// output chunk c of tile c / 128 holds half h = (c >> 6) & 1, kq = 2 *
+// ((c >> 4) & 1) + ((c >> 5) & 1), row r = c & 15 of the tile.
 __global__ __launch_bounds__(256) void pack_weight_kernel(const uint8_t* __restrict__ q, int64_t chunks, int cols,
                                                           uint8_t* __restrict__ out) {
   const int nkb = cols / kBlock;
   for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < chunks; c += (int64_t)gridDim.x * blockDim.x) {
-    const int l = (int)(c & 63), h = (int)((c >> 6) & 1);
+    const int r = (int)(c & 15), h = (int)((c >> 6) & 1);
+    const int kq = 2 * (int)((c >> 4) & 1) + (int)((c >> 5) & 1);
     const int64_t tile = c >> 7;
     const int64_t g = tile / nkb;
     const int b = (int)(tile - g * nkb);
-    const int64_t row = g * 16 + (l & 15);
-    const int64_t col = (int64_t)b * kBlock + h * 64 + (l >> 4) * 16;
+    const int64_t row = g * 16 + r;
+    const int64_t col = (int64_t)b * kBlock + h * 64 + kq * 16;
     *reinterpret_cast<uint4*>(out + c * 16) = *reinterpret_cast<const uint4*>(q + row * cols + col);
   }
 }

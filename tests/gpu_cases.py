@@ -41,11 +41,12 @@ def bf16_dev(bits: np.ndarray):
 
 
 def pack_reference(q: np.ndarray) -> np.ndarray:
-    """The operand-tile layout of moe_pack_weight, by its definition: byte
-    h*1024 + 16*l + j of tile (g, b) holds q[16g + l%16, 128b + 64h + 16(l//16) + j]."""
+    """The operand-tile layout of moe_pack_weight, by its definition: the 16
+    bytes at 1024h + 512(kq%2) + 256(kq//2) + 16r of tile (g, b) hold
+    q[16g + r, 128b + 64h + 16kq + j], j = 0..15."""
     n, rows, cols = q.shape
-    t = q.reshape(n, rows // 16, 16, cols // 128, 2, 4, 16)   # n, g, r, b, h, kq, j
-    return np.ascontiguousarray(t.transpose(0, 1, 3, 4, 5, 2, 6)).reshape(n, rows, cols)
+    t = q.reshape(n, rows // 16, 16, cols // 128, 2, 2, 2, 16)   # n, g, r, b, h, kq//2, kq%2, j
+    return np.ascontiguousarray(t.transpose(0, 1, 3, 4, 6, 5, 2, 7)).reshape(n, rows, cols)
 
 
 def quantize_weights_gpu(moe, wg, wu, wd):

@@ -15,10 +15,13 @@ def test_pack_reference_matches_layout_rule_bytewise():
             for b in range(cols // 128):
                 base = (g * (cols // 128) + b) * 2048
                 for h in range(2):
-                    for lane in range(64):
-                        got = p[m, base + h * 1024 + 16 * lane: base + h * 1024 + 16 * lane + 16]
-                        want = q[m, 16 * g + lane % 16, 128 * b + 64 * h + 16 * (lane // 16): 128 * b + 64 * h + 16 * (lane // 16) + 16]
-                        assert np.array_equal(got, want)
+                    for kq in range(4):
+                        for r in range(16):
+                            off = base + 1024 * h + 512 * (kq % 2) + 256 * (kq // 2) + 16 * r
+                            got = p[m, off: off + 16]
+                            col = 128 * b + 64 * h + 16 * kq
+                            want = q[m, 16 * g + r, col: col + 16]
+                            assert np.array_equal(got, want)
 
 
 def test_pack_reference_is_a_permutation():
