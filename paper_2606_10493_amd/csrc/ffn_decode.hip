@@ -11,11 +11,17 @@
 // MFMA result, in fp32, as the paper's post-scaling does.
 //
 // Work item = (active expert, tile of 16*NT weight rows).  A 256-thread
-// workgroup (4 waves) splits K: wave w takes blocks b = w, w+4, ...; the
-// partial accumulators are summed through LDS in wave order (deterministic).
-// Every weight byte is read once; the weights are packed in operand tiles
-// (moe_pack_weight), so a wave reads one 16-row x 128-K operand as two
-// contiguous 1 KB loads.
+// workgroup (4 waves) splits K and sums the partial accumulators through
+// LDS in wave order (deterministic).  Gate/up waves stream contiguous K
+// ranges (for the long K of gate/up, strided blocks cost ~3%); down waves
+// (short K) take blocks wave, wave + 4, ...  With one 16-token operand
+// (MT = 1) the gate/up waves each stream one matrix (waves 0, 1: the K
+// halves of W_gate; 2, 3: those of W_up): one sequential stream per wave is
+// ~3% faster than two.  With more token operands every wave takes both
+// matrices over a K quarter, so the activation fragments are loaded once
+// per K block.  Every weight byte is read once; the weights are packed in
+// operand tiles (moe_pack_weight), so a wave reads one 16-row x 128-K
+// operand as two contiguous 1 KB loads.
 //
 // Latency is what limits a small GEMV, so the prologue before the first
 // weight load is short: every wave finds its expert with ballots over the
@@ -100,8 +106,10 @@ __device__ __forceinline__ ExpertRef find_expert(const int32_t* __restrict__ off
 template <int MT, int NT, bool GATEUP, bool QH, int U>
 __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   static_assert(!QH || (!GATEUP && MT == 1), "QH is the down projection with at most 16 rows");
-  constexpr int G = GATEUP ? 2 : 1;
-  constexpr int kPer = G * MT * NT * 4;
+  static_assert(!GATEUP || NT == 1, "a GATEUP tile is 16 rows of W_gate and of W_up");
+  constexpr bool kSplit = GATEUP && MT == 1;  // one matrix per wave (waves 0, 1 gate; 2, 3 up)
+  constexpr int G = (GATEUP && !kSplit) ? 2 : 1;  // weight matrices per wave
+  constexpr int kPer = G * MT * NT * 4;           // partial results per lane
   __shared__ float red[(kWaves - 1) * kPer * 64];
   __shared__ __attribute__((aligned(16))) uint8_t qh_lds[QH ? kQhRows * kQhMaxK : 16];
   __shared__ float sh_lds[QH ? kQhRows * (kQhMaxK / kBlock) : 1];
@@ -112,7 +120,18 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   const int r = lane & 15;   // row of the A / B fragment this lane loads
   const int kq = lane >> 4;  // K lane group: bytes [16 kq, +16) and [64 + 16 kq, +16) of a block
   const int tiles = p.N / (16 * NT);
-  const int nkw = (nb - wave + kWaves - 1) / kWaves;  // K blocks of this wave: wave, wave+4, ...
+  // K blocks of this wave: gate/up (long K) a contiguous half (kSplit) or
+  // quarter [kb0, kb0 + nkw); down (short K) blocks wave, wave + 4, ..., so
+  // the four waves read neighbouring tiles (measured faster for K = 2048).
+  // With kSplit the wave's matrix is W_up for waves 2, 3.
+  constexpr bool kContig = GATEUP;
+  const int kpart = kSplit ? (wave & 1) : wave, nparts = kSplit ? 2 : kWaves;
+  const int kb0 = kContig ? (kpart * nb) / nparts : wave;
+  const int kstride = kContig ? 1 : kWaves;
+  const int nkw = kContig ? ((kpart + 1) * nb) / nparts - kb0 : (nb - wave + kWaves - 1) / kWaves;
+  const bool up_wave = kSplit && (wave >> 1);
+  const uint8_t* wfirst_mat = up_wave ? p.w1 : p.w0;
+  const float* sfirst_mat = up_wave ? p.s1 : p.s0;
 
   ExpertRef ref = find_expert(p.offsets, p.E, blockIdx.x / tiles);
   const int64_t items = (int64_t)ref.n_active * tiles;
@@ -130,8 +149,8 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int64_t grp = ((int64_t)e * p.N + n0 + nt * 16) / 16;
-      wrow0[nt] = p.w0 + grp * nb * kTileBytes + packed_lane_offset(0, kq, r);
-      wrow1[nt] = GATEUP ? p.w1 + grp * nb * kTileBytes + packed_lane_offset(0, kq, r) : nullptr;
+      wrow0[nt] = wfirst_mat + grp * nb * kTileBytes + packed_lane_offset(0, kq, r);
+      wrow1[nt] = G == 2 ? p.w1 + grp * nb * kTileBytes + packed_lane_offset(0, kq, r) : nullptr;
     }
     const int64_t srow = ((int64_t)e * (p.N / kBlock) + n0 / kBlock) * nb;
 
@@ -141,15 +160,25 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       // whose outputs it holds (4*kq + i), or -1 beyond the expert's rows.
       // All index loads are issued before any of them is used (clamped
       // indices, no branches), so they cost one round trip together.
-      auto load_w = [&](int bk, v8i (&w)[G][NT], float (&ws)[G]) {
+      auto load_w = [&](int bk, v8i (&w)[G][NT]) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           w[0][nt] = load_v8i_packed(wrow0[nt] + bk * kTileBytes);
-          if (GATEUP) w[G - 1][nt] = load_v8i_packed(wrow1[nt] + bk * kTileBytes);
+          if (G == 2) w[G - 1][nt] = load_v8i_packed(wrow1[nt] + bk * kTileBytes);
         }
-        // Weight scales travel in the same in-order load stream as the weights.
-        ws[0] = p.s0[srow + bk];
-        if (GATEUP) ws[G - 1] = p.s1[srow + bk];
+      };
+      // The wave's weight scales, lane i holding the scale of its i-th K
+      // block (clamped), in one load ahead of the weight stream; the j-th
+      // block reads lane j.
+      float wsv[G];
+      {
+        const int sl = min(kb0 + kstride * min(lane, max(nkw - 1, 0)), nb - 1);
+        wsv[0] = sfirst_mat[srow + sl];
+        if (G == 2) wsv[G - 1] = p.s1[srow + sl];
+      }
+      auto scales_of = [&](int j, float (&ws)[G]) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) ws[g] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wsv[g]), j));
       };
       int ta[MT], ts[MT][4];
       int raw[MT][5];
@@ -187,8 +216,7 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       // without K blocks (nb < 4) loads nothing: its block index would lie
       // past the end of the rows.
       v8i wfirst[G][NT];
-      float wsfirst[G];
-      if (nkw > 0) load_w(wave, wfirst, wsfirst);
+      if (nkw > 0) load_w(kb0, wfirst);
       __builtin_amdgcn_sched_barrier(0);
       if (!QH) {
 #pragma unroll
@@ -270,17 +298,23 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       // K loop: block 0 was loaded above; each later block's loads are
       // issued at the top of its iteration and the unrolled copies let the
       // compiler hoist the next blocks' loads.
-      if (nkw > 0) compute_block(wave, wfirst, wsfirst);
+      if (nkw > 0) {
+        float ws[G];
+        scales_of(0, ws);
+        compute_block(kb0, wfirst, ws);
+      }
 #pragma unroll U
       for (int j = 1; j < nkw; ++j) {
-        const int bk = wave + kWaves * j;
+        const int bk = kb0 + kstride * j;
         v8i w[G][NT];
         float ws[G];
-        load_w(bk, w, ws);
+        load_w(bk, w);
+        scales_of(j, ws);
         compute_block(bk, w, ws);
       }
 
-      // Cross-wave reduction in wave order 0, 1, 2, 3.
+      // Cross-wave reduction in wave order 0, 1, 2, 3 (kSplit: gate = waves
+      // 0 + 1, up = waves 2 + 3).
       if (wave > 0) {
         float* dst = red + (wave - 1) * kPer * 64;
         int q = 0;
@@ -295,9 +329,11 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       }
       __syncthreads();
       if (wave == 0) {
-#pragma unroll
-        for (int w = 0; w < kWaves - 1; ++w) {
-          const float* src = red + w * kPer * 64;
+        v4f up[MT][NT];  // kSplit: the up result
+        {
+          const float* s1 = red + 0 * kPer * 64;
+          const float* s2 = red + 1 * kPer * 64;
+          const float* s3 = red + 2 * kPer * 64;
           int q = 0;
 #pragma unroll
           for (int g = 0; g < G; ++g)
@@ -306,7 +342,15 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
 #pragma unroll
               for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[g][mt][nt][i] += src[(q++) * 64 + lane];
+                for (int i = 0; i < 4; ++i, ++q) {
+                  acc[g][mt][nt][i] += s1[q * 64 + lane];
+                  if (kSplit) {
+                    up[mt][nt][i] = s2[q * 64 + lane] + s3[q * 64 + lane];
+                  } else {
+                    acc[g][mt][nt][i] += s2[q * 64 + lane];
+                    acc[g][mt][nt][i] += s3[q * 64 + lane];
+                  }
+                }
         }
         // Output layout of the 16x16 MFMA: lane l holds rows 4*(l/16)+i, column l%16.
 #pragma unroll
@@ -317,7 +361,10 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
             for (int i = 0; i < 4; ++i) {
               const int m = mt * 16 + 4 * kq + i;
               if (m < mc) {
-                const float v = GATEUP ? silu_mul(acc[0][mt][nt][i], acc[G - 1][mt][nt][i]) : acc[0][mt][nt][i];
+                float v;
+                if (kSplit) v = silu_mul(acc[0][mt][nt][i], up[mt][nt][i]);
+                else if (GATEUP) v = silu_mul(acc[0][mt][nt][i], acc[G - 1][mt][nt][i]);
+                else v = acc[0][mt][nt][i];
                 p.out[(int64_t)(p0 + mb + m) * p.N + n0 + nt * 16 + r] = v;
               }
             }
@@ -346,6 +393,11 @@ moe_status_t run_ffn_decode(const moe_dims_t& d, int32_t T, const uint8_t* qx, c
                             hipStream_t stream) {
   const int64_t R = (int64_t)T * d.topk;
   const int64_t max_active = R < d.n_experts ? R : d.n_experts;
+  // A wave's weight scales sit one per lane: at most 64 K blocks per wave.
+  // (gate/up waves may take K halves).
+  if (d.hidden / kBlock > 64 * 2 || d.inter / kBlock > 64 * kWaves)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "decode regime supports H <= %d and I <= %d", 64 * 2 * kBlock,
+                64 * kWaves * kBlock);
   DecodeArgs g{};
   g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = T;
   g.offsets = offsets; g.E = d.n_experts;
