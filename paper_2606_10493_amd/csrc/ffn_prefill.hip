@@ -38,12 +38,12 @@
 // writes fp32 in 16-byte pieces.
 //
 // Work items are (expert m-tile, n-tile) pairs; m-tiles of all experts are
-// numbered by an exclusive scan of ceil(M_e / 128) (prefill_tiles_kernel).
-// Work items are assigned XCD-major: the hardware deals workgroups to the 8
-// XCDs round-robin, so with n real items (read from the tile scan; the grid
-// is only an upper bound) item = (block % 8) * ceil(n / 8) + block / 8
-// keeps the n-tiles of one m-tile (which share the gathered activation
-// rows) and the m-tiles of one expert (which share weights) on one XCD's L2
+// numbered by an exclusive scan of ceil(M_e / 128) (prefill_tiles_kernel),
+// and an expert's items are ordered n-tile major, so the m-tiles sharing a
+// weight slice are neighbours.  Work items are assigned XCD-major: the
+// hardware deals workgroups to the 8 XCDs round-robin, so with n real items
+// (read from the tile scan; the grid is only an upper bound) item = (block
+// % 8) * ceil(n / 8) + block / 8 keeps an expert's items on one XCD's L2
 // while every XCD gets an equal share.
 #include "common.h"
 
@@ -111,7 +111,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ int arow[kBM];
   __shared__ float rowmax[8][kBM];
-  __shared__ int tile_info[3];
+  __shared__ int tile_info[4];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -126,21 +126,30 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   if (slot >= per) return;
   const int64_t item = (int64_t)(blockIdx.x % kXcd) * per + slot;
   if (item >= real) return;
-  const int64_t mt_global = item / p.n_tiles;
-  const int nt = (int)(item % p.n_tiles);
-  // Expert owning this m-tile: the e with mtile_start[e] <= mt_global <
-  // mtile_start[e+1] (empty experts own no m-tile), found by all threads in
-  // one round of loads; the owner also publishes the tile's row range.
+  // Expert e owns items [mtile_start[e], mtile_start[e+1]) * n_tiles, in
+  // n-tile-major order: item = mtile_start[e] * n_tiles + nt * mcount_e + mt.
+  // The m-tiles that read the same weight slice (same nt) are neighbours, so
+  // they run together on one XCD and the slice comes from HBM once (m-tile
+  // major order fetched the weights once per m-tile).  The owner e is the
+  // one with mtile_start[e] <= item / n_tiles < mtile_start[e+1] (empty
+  // experts own nothing), found by all threads in one round of loads; the
+  // owner also publishes the tile's row range and n-tile.
+  const int64_t eblk = item / p.n_tiles;
   if (tid == 0) tile_info[0] = -1;
   __syncthreads();
   for (int x = tid; x < p.E; x += kThreads) {
     const int s0 = p.mtile_start[x], s1 = p.mtile_start[x + 1];
     const int o0 = p.offsets[x], o1 = p.offsets[x + 1];
-    if (s0 <= mt_global && mt_global < s1) {
-      const int first = o0 + (int)(mt_global - s0) * kBM;
+    if (s0 <= eblk && eblk < s1) {
+      const int64_t local = item - (int64_t)s0 * p.n_tiles;
+      const int mcount = s1 - s0;
+      const int ntx = (int)(local / mcount);
+      const int mt = (int)(local - (int64_t)ntx * mcount);
+      const int first = o0 + mt * kBM;
       tile_info[0] = x;
       tile_info[1] = first;
       tile_info[2] = min(kBM, o1 - first);
+      tile_info[3] = ntx;
     }
   }
   __syncthreads();
@@ -148,6 +157,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   if (e < 0) return;            // no owner: inconsistent offsets, nothing to compute
   const int m0 = tile_info[1];  // first sorted row of the tile
   const int mc = tile_info[2];  // rows in the tile
+  const int nt = tile_info[3];  // n-tile
   const int nb = p.K / kBlock;
 
   float* sa_lds = reinterpret_cast<float*>(smem + kStages * kHalf);  // [nb][kSaStride]

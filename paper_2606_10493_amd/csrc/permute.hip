@@ -31,29 +31,43 @@ struct SlotCheck {
   uint32_t err;  // MOE_DEV_* bits, 0 if the slot is valid
 };
 
-__device__ __forceinline__ SlotCheck check_slot(const int32_t* __restrict__ ids, int64_t tok_base, int j, int E) {
+// The ids of one chunk (up to kChunk tokens x k) staged in LDS with one
+// coalesced pass, so the per-slot checks below read LDS, not global memory.
+// 16 bits hold any valid id (E <= 1024); ids outside [0, E) become -1.
+__device__ __forceinline__ void stage_ids(int16_t* sid, const int32_t* __restrict__ ids, int64_t chunk0, int64_t T,
+                                          int k, int E) {
+  const int64_t ntok = min((int64_t)kChunk, T - chunk0);
+  const int n = ntok > 0 ? (int)(ntok * k) : 0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int32_t id = ids[chunk0 * k + i];
+    sid[i] = (int16_t)((id >= 0 && id < E) ? id : -1);
+  }
+}
+
+// Slot j of the chunk's token lt (ids in LDS, sid = the chunk's ids).
+__device__ __forceinline__ SlotCheck check_slot(const int16_t* sid, int lt, int j, int k, int E) {
+  const int16_t* row = sid + lt * k;
   SlotCheck r;
-  r.expert = ids[tok_base + j];
+  r.expert = row[j];
   r.err = 0;
-  if (r.expert < 0 || r.expert >= E) {
+  if (r.expert < 0 || r.expert >= E) {  // staged as -1
     r.err = MOE_DEV_BAD_EXPERT_ID;
     return r;
   }
   for (int i = 0; i < j; ++i)
-    if (ids[tok_base + i] == r.expert) r.err = MOE_DEV_DUP_EXPERT_ID;
+    if (row[i] == r.expert) r.err = MOE_DEV_DUP_EXPERT_ID;
   return r;
 }
 
 // Fill the per-expert token masks of one chunk; returns this thread's error bits.
-__device__ __forceinline__ uint32_t build_masks(unsigned long long* mask, int* bad_count, const int32_t* ids,
+__device__ __forceinline__ uint32_t build_masks(unsigned long long* mask, int* bad_count, const int16_t* sid,
                                                 int64_t t, int64_t T, int k, int E) {
   uint32_t err = 0;
   if (t < T) {
-    const int64_t base = t * k;
     const unsigned long long bit = 1ull << (threadIdx.x & 63);
     const int word = threadIdx.x >> 6;
     for (int j = 0; j < k; ++j) {
-      const SlotCheck s = check_slot(ids, base, j, E);
+      const SlotCheck s = check_slot(sid, threadIdx.x, j, k, E);
       if (s.err == 0) {
         atomicOr(&mask[s.expert * 4 + word], bit);
       } else {
@@ -85,14 +99,14 @@ __device__ __forceinline__ void report(int32_t* dev_status, uint32_t err) {
 
 // Valid slots of this chunk go to base_e + rank; invalid ones, in slot order,
 // to bad_base + running index (walked by one thread: the error path only).
-__device__ __forceinline__ void scatter_chunk(const unsigned long long* mask, const int32_t* ids, int64_t chunk0,
+__device__ __forceinline__ void scatter_chunk(const unsigned long long* mask, const int16_t* sid, int64_t chunk0,
                                               int64_t T, int k, int E, const int32_t* base_of_e, int32_t bad_base,
                                               int bad_count, int32_t* sorted_src, int32_t* dest_row) {
   const int64_t t = chunk0 + threadIdx.x;
   if (t < T) {
     const int64_t tb = t * k;
     for (int j = 0; j < k; ++j) {
-      const SlotCheck s = check_slot(ids, tb, j, E);
+      const SlotCheck s = check_slot(sid, threadIdx.x, j, k, E);
       if (s.err) continue;
       const int32_t p = base_of_e[s.expert] + rank_in_chunk(mask, s.expert);
       dest_row[tb + j] = p;
@@ -104,7 +118,7 @@ __device__ __forceinline__ void scatter_chunk(const unsigned long long* mask, co
     const int64_t t1 = min(T, chunk0 + kChunk);
     for (int64_t tt = chunk0; tt < t1; ++tt)
       for (int j = 0; j < k; ++j) {
-        const SlotCheck s = check_slot(ids, tt * k, j, E);
+        const SlotCheck s = check_slot(sid, (int)(tt - chunk0), j, k, E);
         if (!s.err) continue;
         dest_row[tt * k + j] = p;
         sorted_src[p] = (int32_t)(tt * k + j);
@@ -120,12 +134,14 @@ __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __res
                                                             int32_t* __restrict__ dev_status) {
   __shared__ unsigned long long mask[kMaxExperts * 4];
   __shared__ int start[kMaxExperts];
+  __shared__ int16_t sid[kChunk * kMaxTopk];
   __shared__ int tmp[4];
   __shared__ int bad_count;
   for (int i = threadIdx.x; i < E * 4; i += 256) mask[i] = 0ull;
   if (threadIdx.x == 0) bad_count = 0;
+  stage_ids(sid, ids, 0, T, k, E);
   __syncthreads();
-  const uint32_t err = build_masks(mask, &bad_count, ids, threadIdx.x, T, k, E);
+  const uint32_t err = build_masks(mask, &bad_count, sid, threadIdx.x, T, k, E);
   __syncthreads();
   // Thread i owns experts 4i .. 4i+3 for the scan.
   int c[4], local = 0;
@@ -148,7 +164,7 @@ __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __res
   }
   if (threadIdx.x == 0) offsets[E] = total_valid;
   __syncthreads();
-  scatter_chunk(mask, ids, 0, T, k, E, start, total_valid, bad_count, sorted_src, dest_row);
+  scatter_chunk(mask, sid, 0, T, k, E, start, total_valid, bad_count, sorted_src, dest_row);
   report(dev_status, err);
 }
 
@@ -157,12 +173,14 @@ __global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __res
                                                             int32_t* __restrict__ counts,
                                                             int32_t* __restrict__ dev_status) {
   __shared__ unsigned long long mask[kMaxExperts * 4];
+  __shared__ int16_t sid[kChunk * kMaxTopk];
   __shared__ int bad_count;
   for (int i = threadIdx.x; i < E * 4; i += 256) mask[i] = 0ull;
   if (threadIdx.x == 0) bad_count = 0;
-  __syncthreads();
   const int64_t chunk0 = (int64_t)blockIdx.x * kChunk;
-  const uint32_t err = build_masks(mask, &bad_count, ids, chunk0 + threadIdx.x, T, k, E);
+  stage_ids(sid, ids, chunk0, T, k, E);
+  __syncthreads();
+  const uint32_t err = build_masks(mask, &bad_count, sid, chunk0 + threadIdx.x, T, k, E);
   __syncthreads();
   int32_t* row = counts + (int64_t)blockIdx.x * (E + 1);
   for (int e = threadIdx.x; e < E; e += 256) row[e] = mask_count(mask, e);
@@ -207,16 +225,18 @@ __global__ __launch_bounds__(256) void permute_scatter_kernel(const int32_t* __r
                                                               int32_t* __restrict__ sorted_src,
                                                               int32_t* __restrict__ dest_row) {
   __shared__ unsigned long long mask[kMaxExperts * 4];
+  __shared__ int16_t sid[kChunk * kMaxTopk];
   __shared__ int bad_count;
   for (int i = threadIdx.x; i < E * 4; i += 256) mask[i] = 0ull;
   if (threadIdx.x == 0) bad_count = 0;
-  __syncthreads();
   const int64_t chunk0 = (int64_t)blockIdx.x * kChunk;
-  build_masks(mask, &bad_count, ids, chunk0 + threadIdx.x, T, k, E);
+  stage_ids(sid, ids, chunk0, T, k, E);
+  __syncthreads();
+  build_masks(mask, &bad_count, sid, chunk0 + threadIdx.x, T, k, E);
   __syncthreads();
   const int32_t* brow = base + (int64_t)blockIdx.x * (E + 1);
   const int nbad = counts[(int64_t)blockIdx.x * (E + 1) + E];
-  scatter_chunk(mask, ids, chunk0, T, k, E, brow, brow[E], nbad, sorted_src, dest_row);
+  scatter_chunk(mask, sid, chunk0, T, k, E, brow, brow[E], nbad, sorted_src, dest_row);
 }
 
 int64_t n_chunks_of(int32_t T) { return ((int64_t)T + kChunk - 1) / kChunk; }
