@@ -36,8 +36,8 @@ METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
 # profiles/ffn_decode_gateup__deepseek_v3_decode_T1_hbm_traffic.md.  Valid only
 # while the kernel's source file is the one measured (sha256 prefix).
 TRAFFIC = {
-    ("decode1", "ffn_decode_gateup"): {"bytes": 235986944, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
-                                       "sha256_prefix": "f4b4c1d15d1e05c0"},
+    ("decode1", "ffn_decode_gateup"): {"bytes": 235616666, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
+                                       "sha256_prefix": "2dbf012cc1a872fd"},
 }
 
 

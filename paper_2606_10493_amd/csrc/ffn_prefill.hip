@@ -47,6 +47,8 @@
 // while every XCD gets an equal share.
 #include "common.h"
 
+#include <type_traits>
+
 namespace moe {
 
 namespace {
@@ -232,6 +234,18 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   u32x4 ra[2];       // this thread's two 16-byte chunks of one K block of expert rows (ext vectors stay in VGPRs)
   v8i bx[4][2];      // B operands of the step: [expert-row operand][K half]
   float sa[4], sw0 = 0.0f, sw1 = 0.0f;
+
+  // The K loop is instantiated for NQ = 1..4 expert-row operands: a tile
+  // whose rows fill only NQ of the four 32-row operands (the last tile of
+  // an expert) loads, reads and multiplies only those, so a tail tile of
+  // 1-32 rows costs its weight stream and a quarter of the MFMAs.  The
+  // accumulators of the skipped operands stay 0 and their rows are not
+  // written.  NQ is the same in the whole workgroup, so every wave passes
+  // the same barriers.
+  const int nq = (mc + 31) >> 5;
+  auto k_loop = [&](auto nq_tag) {
+    constexpr int NQ = decltype(nq_tag)::value;
+    constexpr int NA = NQ > 2 ? 2 : 1;  // 16-byte expert-row chunks per thread (chunk 1 holds rows 64-127)
 #define MOE_PF_WLOAD(SLOT, BLK)                                                            \
   do {                                                                                     \
     const uint8_t* w_ = wsrc + (int64_t)(BLK) * kTileBytes;                                \
@@ -245,14 +259,14 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 #define MOE_PF_ALOAD(BLK)                                                                  \
   do {                                                                                     \
     const int blk_ = (BLK) < nb ? (BLK) : nb - 1;                                          \
-    ra[0] = *reinterpret_cast<const u32x4*>(a_src[0] + (int64_t)blk_ * kBlock);            \
-    ra[1] = *reinterpret_cast<const u32x4*>(a_src[1] + (int64_t)blk_ * kBlock);            \
+    _Pragma("unroll") for (int i_ = 0; i_ < NA; ++i_)                                      \
+      ra[i_] = *reinterpret_cast<const u32x4*>(a_src[i_] + (int64_t)blk_ * kBlock);        \
   } while (0)
 #define MOE_PF_ASTORE(BLK)                                                                 \
   do {                                                                                     \
     uint8_t* st_ = smem + ((BLK) % 3) * kHalf;                                             \
-    *reinterpret_cast<u32x4*>(st_ + a_dst[0]) = ra[0];                                     \
-    *reinterpret_cast<u32x4*>(st_ + a_dst[1]) = ra[1];                                     \
+    _Pragma("unroll") for (int i_ = 0; i_ < NA; ++i_)                                      \
+      *reinterpret_cast<u32x4*>(st_ + a_dst[i_]) = ra[i_];                                 \
   } while (0)
 #define MOE_PF_BREAD(J, SB)                                                                \
   do {                                                                                     \
@@ -290,9 +304,9 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     const uint8_t* sB_ = smem + (j_ % 3) * kHalf;                                          \
     sw0 = swf0[j_];                                                                        \
     sw1 = swf1[j_];                                                                        \
-    _Pragma("unroll") for (int q = 0; q < 4; ++q) sa[q] = sa_lds[j_ * kSaStride + r32 + 32 * q]; \
+    _Pragma("unroll") for (int q = 0; q < NQ; ++q) sa[q] = sa_lds[j_ * kSaStride + r32 + 32 * q]; \
     MOE_PF_BREAD(0, sB_);                                                                  \
-    MOE_PF_BREAD(1, sB_);                                                                  \
+    if (NQ > 1) MOE_PF_BREAD(1, sB_);                                                      \
     __builtin_amdgcn_sched_barrier(0);                                                     \
   } while (0)
   // The two MFMAs of one operand and K block are chained (the second adds
@@ -305,21 +319,21 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     v16f d[4];                                                                             \
     _Pragma("unroll") for (int q = 0; q < 4; ++q) d[q] = v16f{};                           \
     d[0] = mfma_f8_32x32x64(wr[U][0], bx[0][0], d[0]);                                     \
-    d[1] = mfma_f8_32x32x64(wr[U][0], bx[1][0], d[1]);                                     \
-    MOE_PF_BREAD(2, sB_);                                                                  \
-    MOE_PF_BREAD(3, sB_);                                                                  \
+    if (NQ > 1) d[1] = mfma_f8_32x32x64(wr[U][0], bx[1][0], d[1]);                         \
+    if (NQ > 2) MOE_PF_BREAD(2, sB_);                                                      \
+    if (NQ > 3) MOE_PF_BREAD(3, sB_);                                                      \
     d[0] = mfma_f8_32x32x64(wr[U][1], bx[0][1], d[0]);                                     \
-    d[1] = mfma_f8_32x32x64(wr[U][1], bx[1][1], d[1]);                                     \
+    if (NQ > 1) d[1] = mfma_f8_32x32x64(wr[U][1], bx[1][1], d[1]);                         \
     __builtin_amdgcn_sched_barrier(0);                                                     \
-    d[2] = mfma_f8_32x32x64(wr[U][0], bx[2][0], d[2]);                                     \
-    d[3] = mfma_f8_32x32x64(wr[U][0], bx[3][0], d[3]);                                     \
+    if (NQ > 2) d[2] = mfma_f8_32x32x64(wr[U][0], bx[2][0], d[2]);                         \
+    if (NQ > 3) d[3] = mfma_f8_32x32x64(wr[U][0], bx[3][0], d[3]);                         \
     MOE_PF_PROMOTE(0, d[0]);                                                               \
-    d[2] = mfma_f8_32x32x64(wr[U][1], bx[2][1], d[2]);                                     \
-    d[3] = mfma_f8_32x32x64(wr[U][1], bx[3][1], d[3]);                                     \
-    MOE_PF_PROMOTE(1, d[1]);                                                               \
+    if (NQ > 2) d[2] = mfma_f8_32x32x64(wr[U][1], bx[2][1], d[2]);                         \
+    if (NQ > 3) d[3] = mfma_f8_32x32x64(wr[U][1], bx[3][1], d[3]);                         \
+    if (NQ > 1) MOE_PF_PROMOTE(1, d[1]);                                                   \
     __builtin_amdgcn_sched_barrier(0);                                                     \
-    MOE_PF_PROMOTE(2, d[2]);                                                               \
-    MOE_PF_PROMOTE(3, d[3]);                                                               \
+    if (NQ > 2) MOE_PF_PROMOTE(2, d[2]);                                                   \
+    if (NQ > 3) MOE_PF_PROMOTE(3, d[3]);                                                   \
     __builtin_amdgcn_sched_barrier(0);                                                     \
   } while (0)
 #define MOE_PF_STEP(U, J)                                                                  \
@@ -330,25 +344,25 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     __syncthreads();                                                                       \
   } while (0)
 
-  MOE_PF_ALOAD(0);
+    MOE_PF_ALOAD(0);
 #pragma unroll
-  for (int s = 0; s < kRing - 1; ++s) MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
-  MOE_PF_ASTORE(0);
-  MOE_PF_ALOAD(1);
-  __syncthreads();
-  if (wave >= 4) __syncthreads();  // the lagging half starts one phase later (wave-uniform branch)
+    for (int s = 0; s < kRing - 1; ++s) MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
+    MOE_PF_ASTORE(0);
+    MOE_PF_ALOAD(1);
+    __syncthreads();
+    if (wave >= 4) __syncthreads();  // the lagging half starts one phase later (wave-uniform branch)
 
-  // kRing = 3 weight slots: three steps per loop iteration keep every slot
-  // index static.
-  int j0 = 0;
-  for (; j0 + kRing <= nb; j0 += kRing) {
-    MOE_PF_STEP(0, j0);
-    MOE_PF_STEP(1, j0 + 1);
-    MOE_PF_STEP(2, j0 + 2);
-  }
-  if (j0 < nb) MOE_PF_STEP(0, j0);
-  if (j0 + 1 < nb) MOE_PF_STEP(1, j0 + 1);
-  if (wave < 4) __syncthreads();   // pairs with the lagging half's last barrier
+    // kRing = 3 weight slots: three steps per loop iteration keep every slot
+    // index static.
+    int j0 = 0;
+    for (; j0 + kRing <= nb; j0 += kRing) {
+      MOE_PF_STEP(0, j0);
+      MOE_PF_STEP(1, j0 + 1);
+      MOE_PF_STEP(2, j0 + 2);
+    }
+    if (j0 < nb) MOE_PF_STEP(0, j0);
+    if (j0 + 1 < nb) MOE_PF_STEP(1, j0 + 1);
+    if (wave < 4) __syncthreads();   // pairs with the lagging half's last barrier
 #undef MOE_PF_WLOAD
 #undef MOE_PF_ALOAD
 #undef MOE_PF_ASTORE
@@ -357,6 +371,13 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 #undef MOE_PF_MEM
 #undef MOE_PF_COMP
 #undef MOE_PF_STEP
+  };
+  switch (nq) {
+    case 1: k_loop(std::integral_constant<int, 1>{}); break;
+    case 2: k_loop(std::integral_constant<int, 2>{}); break;
+    case 3: k_loop(std::integral_constant<int, 3>{}); break;
+    default: k_loop(std::integral_constant<int, 4>{}); break;
+  }
 
   if (!GATEUP) {
     // y[m0 + t][nt*256 + 32w + 8*(i/4) + 4*g2 + i%4] for expert row t = 32j + r32.

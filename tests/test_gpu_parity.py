@@ -259,6 +259,41 @@ def test_layer_parity_small(moe, case, regime):
     assert out_err <= TOL
 
 
+def test_prefill_tail_tiles_of_every_operand_count(moe):
+    """Expert row counts whose 128-row tiles end with 1-32, 33-64, 65-96 and
+    97-128 rows, so the prefill K loop runs with 1, 2, 3 and 4 live 32-row
+    operands (and full tiles before the tails)."""
+    counts = [2, 32, 33, 64, 65, 96, 225, 257]
+    k = 2
+    t = sum(counts) // k
+    w = synth.Workload("tails", 512, 256, len(counts), k, t, "uniform", 0.0, "sigmoid", seed=5)
+    x = synth.activations(w)
+    _, wts = synth.routing(w)
+    # expert e fills counts[e] slots; slot t + j*T goes to token t, choice j
+    # (distinct experts per token since every count is at most T)
+    slots = np.repeat(np.arange(len(counts), dtype=np.int32), counts)
+    ids = np.ascontiguousarray(slots.reshape(k, t).T)
+    assert all(len(set(r)) == k for r in ids.tolist())
+    wg, wu, wd = synth.weights_host(w)
+    ow = oracle.prepare_weights(wg, wu, wd)
+    dweights = quantize_weights_gpu(moe, wg, wu, wd)
+    ref, inter = oracle.moe_layer(x, ids, wts, ow, want_intermediates=True)
+    assert np.diff(inter["offsets"]).tolist() == counts
+    buf = _gpu_layer(moe, w, x, ids, wts, dweights, moe.MOE_REGIME_PREFILL)
+    assert int(buf.dev_status.item()) == 0
+    y_err = rel_err(buf.y_rows.cpu().numpy(), inter["y"])
+    out_err = rel_err(bits_to_f32(buf.out), oracle.bf16_to_f32(ref))
+    log(f"  tails: y_rows rel err {y_err:.3e}  out rel err {out_err:.3e}")
+    assert y_err <= TOL
+    assert out_err <= TOL
+    # every expert row is checked on its own too, so a skipped operand cannot
+    # hide behind the global maximum
+    y = buf.y_rows.cpu().numpy().astype(np.float64)
+    for e in range(len(counts)):
+        o0, o1 = inter["offsets"][e], inter["offsets"][e + 1]
+        assert rel_err(y[o0:o1], inter["y"][o0:o1]) <= TOL, e
+
+
 @pytest.mark.parametrize("case", SMALL_CASES[:3], ids=lambda c: "x".join(map(str, c[:5])))
 def test_decode_and_prefill_kernels_agree(moe, case):
     w, x, ids, wts, (wg, wu, wd) = _small_layer(case, seed=3)
