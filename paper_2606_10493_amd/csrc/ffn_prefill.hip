@@ -98,11 +98,13 @@ __global__ __launch_bounds__(1024) void prefill_tiles_kernel(const int32_t* __re
 }
 
 // LDS byte offset of 16-byte chunk c (0..7) of row `row` in a 128-byte-row
-// tile: the chunk index is XOR-ed with row % 8, so the 16 rows that one
-// operand read touches spread over all LDS banks (measured on gfx950: a
-// swizzled b128 read costs what a contiguous one does, a 144-byte padded
-// row layout about 1.7 times as much).
-__device__ __forceinline__ int swz(int row, int c) { return row * kLdsRow + ((c ^ (row & 7)) << 4); }
+// tile.  gfx950's LDS serves 256 bytes per clock (64 four-byte banks), so
+// two consecutive 128-byte rows share one bank row; the chunk index is
+// XOR-ed with (row / 2) % 8, so the 16 rows that a quarter-wave b128 read
+// touches fill all 16 sixteen-byte bank slots (measured on gfx950: about
+// 195 B/clk per CU this way, 122 with the chunk XOR-ed by row % 8, whose
+// rows r and r + 8 collide, and 32 unswizzled).
+__device__ __forceinline__ int swz(int row, int c) { return row * kLdsRow + ((c ^ ((row >> 1) & 7)) << 4); }
 
 __device__ __forceinline__ v16f mfma_f8_32x32x64(const v8i& a, const v8i& b, const v16f& c) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
@@ -216,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   const float* swf0 = sw_lds + (GATEUP ? 0 : (wave >> 2)) * nb;  // scale of result rows 0-15
   const float* swf1 = sw_lds + (GATEUP ? 1 : (wave >> 2)) * nb;  // scale of result rows 16-31
   // LDS offsets of this lane's B operand pieces in expert row r32: K chunks
-  // 4h + 2 g2 + part; rows 32j + r32 share row % 8, hence the swizzle.
+  // 4h + 2 g2 + part; rows 32j + r32 share (row / 2) % 8, hence one offset.
   int bo[2][2];
 #pragma unroll
   for (int h = 0; h < 2; ++h)
