@@ -230,8 +230,12 @@ moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const flo
  * slots) bytes, the same three sub-rings of scales.  Experts are copied and
  * run in groups of consecutive experts (a divisor of the slot count) so
  * that each launch fills the GPU.  ctx: from moe_stream_ctx_create
- * with the same slot count (its events order the slots; one call at a time
- * per ctx).  x_bf16, topk_ids, topk_w, out_bf16 as in the other calls (device).
+ * with the same slot count.  Its per-slot events order the ring across
+ * calls: calls on one ctx (the layers of a model streamed through one ring)
+ * may be enqueued back to back without a host synchronisation; a slot is
+ * refilled only after the kernels of earlier calls that read it have run,
+ * and the next call's copies start as soon as slots free up.  A ctx must not
+ * be used by two host threads at once.  x_bf16, topk_ids, topk_w, out_bf16 as in the other calls (device).
  * ws: device, moe_ffn_streamed_workspace(dims, T, chunk_tokens) bytes, 256-byte
  * aligned (it holds the fp32 expert rows of all T*k slots).  compute and copy
  * should be distinct streams for the copies to overlap the kernels.

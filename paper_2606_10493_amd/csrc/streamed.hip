@@ -30,7 +30,8 @@
 
 struct moe_stream_ctx {
   int32_t slots;
-  std::vector<hipEvent_t> on, off;
+  std::vector<hipEvent_t> on, off;  // per ring slot
+  std::vector<char> off_recorded;   // off[s] holds the last kernels that read slot s (this call or an earlier one)
 };
 
 namespace moe {
@@ -99,6 +100,7 @@ extern "C" moe_status_t moe_stream_ctx_create(int32_t ring_slots, moe_stream_ctx
   c->slots = ring_slots;
   c->on.resize(ring_slots);
   c->off.resize(ring_slots);
+  c->off_recorded.assign(ring_slots, 0);
   for (int i = 0; i < ring_slots; ++i) {
     if (hipEventCreateWithFlags(&c->on[i], hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&c->off[i], hipEventDisableTiming) != hipSuccess) {
@@ -192,7 +194,6 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
     for (int g = (int)want; g >= 1; --g)
       if (R % g == 0) { G = g; break; }
   }
-  const int groups_in_ring = R / G;
   const moe_dims_t view{d.hidden, d.inter, G, d.topk};
   const int64_t max_mtiles = ((int64_t)L.chunk * k + 127) / 128 + G;  // G experts, at most chunk rows each
   uint8_t* ring_gate = dev_ring;
@@ -203,12 +204,11 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
   float* ring_sdown = dev_ring_scales + 2 * (size_t)R * smat;
   for (int64_t e0 = 0; e0 < E; e0 += G) {
     const int g_here = (int)((E - e0) < G ? (E - e0) : G);
-    const int64_t grp = e0 / G;
-    const int ev = (int)(grp % groups_in_ring);
     const int slot0 = (int)(e0 % R);
-    // Loader: the group's slots are free once the group that used them last ran.
-    if (grp >= groups_in_ring && hipStreamWaitEvent(copy, ctx->off[ev], 0) != hipSuccess)
-      return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait OFF");
+    // Loader: each slot of the group is free once the kernels that read it last ran.
+    for (int s = slot0; s < slot0 + g_here; ++s)
+      if (ctx->off_recorded[s] && hipStreamWaitEvent(copy, ctx->off[s], 0) != hipSuccess)
+        return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait OFF");
     const size_t nb_w = (size_t)g_here * wmat, nb_s = (size_t)g_here * smat * sizeof(float);
     if (hipMemcpyAsync(ring_gate + slot0 * wmat, host_w_gate + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
         hipMemcpyAsync(ring_up + slot0 * wmat, host_w_up + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
@@ -217,9 +217,9 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
         hipMemcpyAsync(ring_sup + slot0 * smat, host_s_up + e0 * smat, nb_s, hipMemcpyHostToDevice, copy) ||
         hipMemcpyAsync(ring_sdown + slot0 * smat, host_s_down + e0 * smat, nb_s, hipMemcpyHostToDevice, copy))
       return fail(MOE_ERR_HIP, "moe_ffn_streamed: copy of experts %lld..", (long long)e0);
-    if (hipEventRecord(ctx->on[ev], copy) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record ON");
+    if (hipEventRecord(ctx->on[slot0], copy) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record ON");
     // Model: the group's rows of every chunk, one launch set per chunk.
-    if (hipStreamWaitEvent(compute, ctx->on[ev], 0) != hipSuccess)
+    if (hipStreamWaitEvent(compute, ctx->on[slot0], 0) != hipSuccess)
       return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait ON");
     const moe_dims_t vd{view.hidden, view.inter, g_here, view.topk};
     for (int64_t c = 0; c < L.n_chunks; ++c) {
@@ -232,7 +232,10 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
                                 sh, tiles, compute);
       if (st != MOE_OK) return st;
     }
-    if (hipEventRecord(ctx->off[ev], compute) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record OFF");
+    for (int s = slot0; s < slot0 + g_here; ++s) {
+      if (hipEventRecord(ctx->off[s], compute) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record OFF");
+      ctx->off_recorded[s] = 1;
+    }
   }
 
   // Combine each chunk.

@@ -91,3 +91,44 @@ def test_streamed_32k_tokens_full_layer(moe):
     err = rel_err(bits_to_f32(got)[sample], oracle.bf16_to_f32(o))
     log(f"  sampled tokens {sample}: out rel err {err:.3e}")
     assert err <= 2e-2
+
+
+@pytest.mark.parametrize("slots", [2, 16])
+def test_streamed_layers_back_to_back_share_the_ring(moe, slots):
+    """Two layers with different weights streamed through one ring and one
+    context, the second call enqueued right after the first (no host sync),
+    the second layer's input being the first layer's output: a slot may be
+    refilled only after the first call's kernels that read it have run."""
+    import dataclasses
+    w0 = synth.Workload("streamed_two_layers", 512, 256, 16, 4, 700, "zipf", 0.8)
+    w1 = dataclasses.replace(w0, seed=1)
+    x = synth.activations(w0)
+    layers = []
+    for w in (w0, w1):
+        ids, wts = synth.routing(w)
+        dev_weights = quantize_weights_gpu(moe, *synth.weights_host(w))
+        layers.append((ids, wts, dev_weights, _pinned(dev_weights)))
+    log(f"two streamed layers back to back, slots={slots}")
+    dims = moe.MoeDims(w0.hidden, w0.inter, w0.n_experts, w0.topk)
+    chunk = 256
+    ctx = moe.StreamContext(slots)
+    ring = torch.empty(moe.moe_ring_bytes(dims, slots), dtype=torch.uint8, device="cuda")
+    ring_s = torch.empty(moe.moe_ring_scale_bytes(dims, slots) // 4, dtype=torch.float32, device="cuda")
+    ws = [torch.empty(moe.moe_ffn_streamed_workspace(dims, w0.tokens, chunk), dtype=torch.uint8, device="cuda")
+          for _ in range(2)]
+    outs = [torch.empty((w0.tokens, w0.hidden), dtype=torch.int16, device="cuda") for _ in range(2)]
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    copy_stream = torch.cuda.Stream()
+    inp = bf16_dev(x)
+    for i, (ids, wts, _, host_weights) in enumerate(layers):
+        moe.moe_ffn_streamed(dims, chunk, inp, to_dev(ids), to_dev(wts), host_weights, ring, ring_s, ctx, outs[i],
+                             status, ws[i], torch.cuda.current_stream(), copy_stream)
+        inp = outs[i]
+    torch.cuda.synchronize()
+    ctx.close()
+    assert int(status.item()) == 0
+    inp = x
+    for i, (ids, wts, dev_weights, _) in enumerate(layers):
+        ref = _resident_prefill(moe, w0, inp, ids, wts, dev_weights)
+        assert np.array_equal(outs[i].cpu().numpy(), ref.cpu().numpy()), f"layer {i}"
+        inp = ref.cpu().numpy().view(np.uint16)
