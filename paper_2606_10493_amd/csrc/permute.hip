@@ -79,12 +79,17 @@ __device__ __forceinline__ uint32_t build_masks(unsigned long long* mask, int* b
   return err;
 }
 
-__device__ __forceinline__ int rank_in_chunk(const unsigned long long* mask, int e) {
-  const int word = threadIdx.x >> 6;
-  const unsigned long long below = (1ull << (threadIdx.x & 63)) - 1ull;
+// Rank of token lt (chunk-local) among the chunk's tokens routed to e.
+__device__ __forceinline__ int rank_of(const unsigned long long* mask, int e, int lt) {
+  const int word = lt >> 6;
+  const unsigned long long below = (1ull << (lt & 63)) - 1ull;
   int r = __popcll(mask[e * 4 + word] & below);
   for (int w = 0; w < word; ++w) r += __popcll(mask[e * 4 + w]);
   return r;
+}
+
+__device__ __forceinline__ int rank_in_chunk(const unsigned long long* mask, int e) {
+  return rank_of(mask, e, threadIdx.x);
 }
 
 __device__ __forceinline__ int mask_count(const unsigned long long* mask, int e) {
@@ -127,6 +132,9 @@ __device__ __forceinline__ void scatter_chunk(const unsigned long long* mask, co
   }
 }
 
+// One chunk (T <= 256): mask, scan and scatter in one workgroup.  Threads
+// take slots, not tokens, so that a few tokens with k slots each (decode)
+// spread over k * T threads instead of a serial loop in T threads.
 __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
                                                             int32_t* __restrict__ offsets,
                                                             int32_t* __restrict__ sorted_src,
@@ -141,7 +149,18 @@ __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __res
   if (threadIdx.x == 0) bad_count = 0;
   stage_ids(sid, ids, 0, T, k, E);
   __syncthreads();
-  const uint32_t err = build_masks(mask, &bad_count, sid, threadIdx.x, T, k, E);
+  const int n = T * k;
+  uint32_t err = 0;
+  for (int f = threadIdx.x; f < n; f += 256) {
+    const int t = f / k, j = f - t * k;
+    const SlotCheck sc = check_slot(sid, t, j, k, E);
+    if (sc.err == 0) {
+      atomicOr(&mask[sc.expert * 4 + (t >> 6)], 1ull << (t & 63));
+    } else {
+      err |= sc.err;
+      atomicAdd(&bad_count, 1);
+    }
+  }
   __syncthreads();
   // Thread i owns experts 4i .. 4i+3 for the scan.
   int c[4], local = 0;
@@ -164,7 +183,25 @@ __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __res
   }
   if (threadIdx.x == 0) offsets[E] = total_valid;
   __syncthreads();
-  scatter_chunk(mask, sid, 0, T, k, E, start, total_valid, bad_count, sorted_src, dest_row);
+  for (int f = threadIdx.x; f < n; f += 256) {
+    const int t = f / k, j = f - t * k;
+    const SlotCheck sc = check_slot(sid, t, j, k, E);
+    if (sc.err) continue;
+    const int32_t p = start[sc.expert] + rank_of(mask, sc.expert, t);
+    dest_row[f] = p;
+    sorted_src[p] = f;
+  }
+  if (bad_count > 0 && threadIdx.x == 0) {  // error path: invalid slots in slot order after the valid rows
+    int32_t p = total_valid;
+    for (int f = 0; f < n; ++f) {
+      const int t = f / k;
+      const SlotCheck sc = check_slot(sid, t, f - t * k, k, E);
+      if (!sc.err) continue;
+      dest_row[f] = p;
+      sorted_src[p] = f;
+      ++p;
+    }
+  }
   report(dev_status, err);
 }
 
