@@ -156,39 +156,49 @@ def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache
 
 
 def time_streamed(moe, torch, synth, name, steps, warmup):
-    """Stream-loaded layer: weights in pinned host memory, ring of all experts."""
+    """Stream-loaded layers: weights in pinned host memory, streamed through a
+    ring of expert slots (all experts of a layer by default).  With several
+    layers (stream-loading across a stack, each layer with its own weights and
+    routing) every layer's output is the next layer's input and all layers
+    share one ring and one stream context."""
     import numpy as np
     w = synth.WORKLOADS[name]
+    n_layers = max(1, w.layers)
     x = synth.activations(w)
-    ids, wts = synth.routing(w)
-    log("drawing and quantizing the weight layer on the GPU, then pinning a host copy")
-    dev_layer = make_layer(moe, torch, synth, w, 0)
-    host = []
-    for t in dev_layer:
-        h = torch.empty(t.shape, dtype=t.dtype, pin_memory=True)
-        h.copy_(t)
-        host.append(h)
-    host = tuple(host)
-    del dev_layer
-    torch.cuda.empty_cache()
+    routes = [synth.routing(w, layer=l) for l in range(n_layers)]
+    host_layers = []
+    for l in range(n_layers):
+        log(f"drawing and quantizing weight layer {l} on the GPU, then pinning a host copy")
+        dev_layer = make_layer(moe, torch, synth, w, l)
+        host = []
+        for t in dev_layer:
+            h = torch.empty(t.shape, dtype=t.dtype, pin_memory=True)
+            h.copy_(t)
+            host.append(h)
+        host_layers.append(tuple(host))
+        del dev_layer
+        torch.cuda.empty_cache()
     dims = moe.MoeDims(w.hidden, w.inter, w.n_experts, w.topk)
-    slots = w.n_experts
+    slots = w.ring_slots or w.n_experts
     ctx = moe.StreamContext(slots)
     ring = torch.empty(moe.moe_ring_bytes(dims, slots), dtype=torch.uint8, device="cuda")
     ring_s = torch.empty(moe.moe_ring_scale_bytes(dims, slots) // 4, dtype=torch.float32, device="cuda")
     ws = torch.empty(moe.moe_ffn_streamed_workspace(dims, w.tokens, w.chunk_tokens), dtype=torch.uint8,
                      device="cuda")
-    out = torch.empty((w.tokens, w.hidden), dtype=torch.int16, device="cuda")
+    outs = [torch.empty((w.tokens, w.hidden), dtype=torch.int16, device="cuda") for _ in range(2)]
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
     dx = torch.from_numpy(x.view(np.int16)).cuda()
-    dids = torch.from_numpy(ids).cuda()
-    dw = torch.from_numpy(wts).cuda()
+    dids = [torch.from_numpy(ids).cuda() for ids, _ in routes]
+    dws = [torch.from_numpy(wts).cuda() for _, wts in routes]
     compute = torch.cuda.current_stream()
     copy = torch.cuda.Stream()
 
     def step():
-        moe.moe_ffn_streamed(dims, w.chunk_tokens, dx, dids, dw, host, ring, ring_s, ctx, out, status, ws,
-                             compute, copy)
+        inp = dx
+        for l in range(n_layers):
+            moe.moe_ffn_streamed(dims, w.chunk_tokens, inp, dids[l], dws[l], host_layers[l], ring, ring_s, ctx,
+                                 outs[l % 2], status, ws, compute, copy)
+            inp = outs[l % 2]
 
     def timed(fn, n):
         torch.cuda.synchronize()
@@ -205,21 +215,26 @@ def time_streamed(moe, torch, synth, name, steps, warmup):
     ms = timed(step, steps)
     if int(status.item()) != 0:
         raise RuntimeError("device status reported bad routing ids")
-    # Copy-only reference: the same bytes host -> device as six whole-tensor
-    # copies on the copy stream (the pinned-copy peak of this link).
-    flat_ring = [ring[i * (ring.numel() // 3):(i + 1) * (ring.numel() // 3)] for i in range(3)]
-    flat_scales = [ring_s[i * (ring_s.numel() // 3):(i + 1) * (ring_s.numel() // 3)] for i in range(3)]
+    # Copy-only reference: the same bytes host -> device through the same
+    # ring (slot-sized pieces, wrapping) on the copy stream, no kernels.
+    per_slot = [ring.numel() // 3 // slots, ring_s.numel() // 3 // slots]
+    ring_parts = [ring[i * (ring.numel() // 3):(i + 1) * (ring.numel() // 3)] for i in range(3)]
+    scale_parts = [ring_s[i * (ring_s.numel() // 3):(i + 1) * (ring_s.numel() // 3)] for i in range(3)]
 
     def copies():
         with torch.cuda.stream(copy):
-            for m in range(3):
-                flat_ring[m].copy_(host[2 * m].view(-1), non_blocking=True)
-                flat_scales[m].copy_(host[2 * m + 1].view(-1), non_blocking=True)
+            for host in host_layers:
+                for e0 in range(0, w.n_experts, slots):
+                    n = min(slots, w.n_experts - e0)
+                    for m in range(3):
+                        ring_parts[m][: n * per_slot[0]].copy_(host[2 * m][e0:e0 + n].view(-1), non_blocking=True)
+                        scale_parts[m][: n * per_slot[1]].copy_(host[2 * m + 1][e0:e0 + n].view(-1),
+                                                               non_blocking=True)
         compute.wait_stream(copy)
 
-    copy_ms = timed(copies, 2)
-    # Kernel durations of one streamed layer with the library's launch events.
-    moe.moe_profile_begin(20000)
+    copy_ms = timed(copies, 1)
+    # Kernel durations of one step with the library's launch events.
+    moe.moe_profile_begin(20000 * n_layers)
     step()
     prof = moe.moe_profile_end()
     torch.cuda.synchronize()
@@ -228,8 +243,9 @@ def time_streamed(moe, torch, synth, name, steps, warmup):
         kern.setdefault(kname, []).append(kms)
     kern_total_ms = {k: sum(v) for k, v in kern.items()}
     ctx.close()
-    h2d_bytes = sum(t.numel() * t.element_size() for t in host)
-    return w, ids, wts, x, ms, copy_ms, h2d_bytes, kern_total_ms
+    h2d_bytes = sum(t.numel() * t.element_size() for host in host_layers for t in host)
+    ids_all = np.concatenate([ids for ids, _ in routes])
+    return w, ids_all, routes[0][1], x, ms, copy_ms, h2d_bytes, kern_total_ms
 
 
 def cpu_baseline(torch, synth, w, x, ids, wts, budget_s):
@@ -366,7 +382,8 @@ def main():
 def main_streamed(args, moe, torch, synth):
     w, ids, wts, x, ms, copy_ms, h2d_bytes, kern_ms = time_streamed(moe, torch, synth, args.workload, args.steps,
                                                                      args.warmup)
-    alg = algorithmic(w, ids)
+    n_layers = max(1, w.layers)
+    alg = algorithmic(w.with_tokens(w.tokens * n_layers), ids)
     gu_ms = kern_ms.get("ffn_prefill_gateup", 0.0)
     dn_ms = kern_ms.get("ffn_prefill_down", 0.0)
     gemm_tflops = (alg["gateup_flops"] + alg["down_flops"]) / ((gu_ms + dn_ms) * 1e-3) / 1e12
@@ -381,16 +398,17 @@ def main_streamed(args, moe, torch, synth):
         "scaling": "weak", "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
         "config": {"workload": args.workload, "hidden": w.hidden, "inter": w.inter, "n_experts": w.n_experts,
                    "topk": w.topk, "tokens": w.tokens, "chunk_tokens": w.chunk_tokens, "routing": w.routing,
-                   "zipf_s": w.zipf_s, "ring_slots": w.n_experts},
+                   "zipf_s": w.zipf_s, "layers": n_layers, "ring_slots": w.ring_slots or w.n_experts},
         "streaming": {"h2d_bytes": h2d_bytes, "copy_only_ms": round(copy_ms, 3),
                       "h2d_GBps_copy_only": round(h2d_gbs, 2),
                       "h2d_GBps_in_layer": round(h2d_bytes / (ms * 1e-3) / 1e9, 2),
+                      "layer_tokens_per_s": round(n_layers * w.tokens / (ms / 1000.0), 1),
                       "exposed_compute_ms": round(ms - copy_ms, 3),
                       "gemm_kernel_ms": round(gu_ms + dn_ms, 3)},
         "roofline": {"kernel": "ffn_prefill_gateup + ffn_prefill_down (per expert and chunk)", "bound": "mfma",
                      "achieved": round(gemm_tflops, 1), "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4), "traffic": None},
-        "kernel_ms_per_layer": {k: round(v, 3) for k, v in kern_ms.items()},
+        "kernel_ms_per_step": {k: round(v, 3) for k, v in kern_ms.items()},
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

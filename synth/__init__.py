@@ -51,6 +51,8 @@ class Workload:
     weight_rule: str = "sigmoid"  # "softmax" | "sigmoid"
     chunk_tokens: int = 0   # >0: processed in chunks with streamed weights
     seed: int = 0
+    layers: int = 1         # >1: a stack of layers streamed through one ring
+    ring_slots: int = 0     # streamed: ring size in experts (0: all experts of a layer)
 
     def with_tokens(self, t: int) -> "Workload":
         return dataclasses.replace(self, tokens=t)
@@ -67,11 +69,15 @@ WORKLOADS = {
     "prefill8k": Workload("prefill8k", 7168, 2048, 256, 8, 8192, "uniform"),
     "prefill32k_streamed": Workload("prefill32k_streamed", 7168, 2048, 256, 8, 32768,
                                     "zipf", 0.8, chunk_tokens=4096),
+    # Four DeepSeek-V3-shaped layers, each with its own weights and routing,
+    # streamed one after the other through a ring of 32 expert slots.
+    "slp4_ring32": Workload("slp4_ring32", 7168, 2048, 256, 8, 4096, "zipf", 0.8, chunk_tokens=4096,
+                            layers=4, ring_slots=32),
 }
 
 
-def _seeds(seed: int):
-    ss = np.random.SeedSequence(seed)
+def _seeds(seed: int, layer: int = 0):
+    ss = np.random.SeedSequence(seed) if layer == 0 else np.random.SeedSequence([seed, layer])
     kids = ss.spawn(5)
     return dict(zip(("x", "routing", "w_gate", "w_up", "w_down"), kids))
 
@@ -91,11 +97,11 @@ def activations(w: Workload, tokens: int | None = None) -> np.ndarray:
     return bf16_bits_from_f32(x)
 
 
-def routing(w: Workload, tokens: int | None = None):
+def routing(w: Workload, tokens: int | None = None, layer: int = 0):
     """(topk_ids int32 [T,k], topk_w fp32 [T,k]) per the workload's law."""
     t = w.tokens if tokens is None else tokens
     e, k = w.n_experts, w.topk
-    rng = np.random.default_rng(_seeds(w.seed)["routing"])
+    rng = np.random.default_rng(_seeds(w.seed, layer)["routing"])
     if w.routing == "uniform":
         logp = np.zeros(e)
         rank_to_id = np.arange(e)
