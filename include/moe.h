@@ -208,6 +208,40 @@ moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const flo
                          hipStream_t stream);
 
 /*
+ * Router (gate): the step before moe_permute.  The paper's Background on
+ * Mixture-of-Experts names top-k and grouped top-k gating and SmallEP runs
+ * the gate locally before sorting tokens; it fixes no formula, so the rule
+ * is the DeepSeek-V3 gate:
+ *   logits[t,e] = sum_i x[t,i] * W_r[e,i]    (bf16 inputs, fp32 accumulation)
+ *   s = 1 / (1 + exp(-logits)),  key = s + bias[e]
+ *   the E experts form n_group contiguous groups scored by the sum of their
+ *   two largest keys; the topk_group best groups are kept; the k largest
+ *   keys among their experts are chosen, listed by decreasing key;
+ *   equal values go to the lower group / expert index;
+ *   topk_w[t,j] = s[id_j] / (s[id_0] + ... + s[id_k-1]) * routed_scaling.
+ * n_group = topk_group = 1 is plain top-k.
+ *
+ * x_bf16: device [T, H] bf16, 16-byte aligned; w_router_bf16: device [E, H]
+ * bf16, 16-byte aligned; bias: device fp32 [E] or NULL (zero).
+ * topk_ids: device int32 [T, k]; topk_w: device fp32 [T, k].
+ * ws: device, moe_router_workspace(T, H, E) bytes (partial logits).
+ * Requires H % 32 == 0, 1 <= E <= 1024, n_group <= 64 dividing E with at
+ * least two experts per group when n_group > 1, 1 <= topk_group <= n_group,
+ * 1 <= k <= min(32, topk_group * E / n_group), routed_scaling > 0; else
+ * MOE_ERR_INVALID_ARG before any launch.  Inputs must be finite.
+ */
+typedef struct {
+  int32_t n_group;       /* expert groups (1: no group limit) */
+  int32_t topk_group;    /* groups kept per token */
+  float routed_scaling;  /* factor on the normalised weights */
+} moe_router_cfg_t;
+size_t moe_router_workspace(int32_t T, int32_t H, int32_t E);
+moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H, const uint16_t* w_router_bf16,
+                        const float* bias, int32_t E, int32_t k, moe_router_cfg_t cfg,
+                        int32_t* topk_ids, float* topk_w, void* ws, size_t ws_bytes,
+                        hipStream_t stream);
+
+/*
  * Stream-loaded layer (System Design, Stream-loading Prefill: a loader
  * stages each expert's weights from host memory into a device experts ring
  * buffer and sets an ON event, the model waits for ON, runs the expert and

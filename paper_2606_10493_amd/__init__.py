@@ -14,7 +14,8 @@ import os
 from ._lib import (  # noqa: F401
     LIB_PATH, MoEError, lib, MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED_SHAPE,
     MOE_ERR_WORKSPACE, MOE_ERR_HIP, MOE_REGIME_AUTO, MOE_REGIME_DECODE, MOE_REGIME_PREFILL,
-    MOE_DEV_BAD_EXPERT_ID, MOE_DEV_DUP_EXPERT_ID, MOE_DECODE_MAX_TOKENS, MoeDims, EXPORTED_SYMBOLS,
+    MOE_DEV_BAD_EXPERT_ID, MOE_DEV_DUP_EXPERT_ID, MOE_DECODE_MAX_TOKENS, MoeDims, MoeRouterCfg,
+    EXPORTED_SYMBOLS,
 )
 from ._lib import check as _check
 
@@ -108,6 +109,24 @@ def moe_expert_ffn(dims: MoeDims, T: int, regime: int, qx, sx, expert_offsets, s
     _check(lib.moe_expert_ffn(dims, T, regime, _ptr(qx), _ptr(sx), _ptr(expert_offsets), _ptr(sorted_src),
                               _ptr(w_gate), _ptr(s_gate), _ptr(w_up), _ptr(s_up), _ptr(w_down),
                               _ptr(s_down), _ptr(y_rows), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def moe_router_workspace(T: int, H: int, E: int) -> int:
+    return int(lib.moe_router_workspace(T, H, E))
+
+
+def moe_router(x_bf16, w_router_bf16, bias, topk_ids, topk_w, n_group=1, topk_group=1, routed_scaling=1.0,
+               ws=None, stream=None):
+    """x_bf16 [T, H], w_router_bf16 [E, H] (bf16 or 16-bit views), bias fp32 [E] or None
+    -> topk_ids int32 [T, k], topk_w fp32 [T, k]."""
+    _need(x_bf16, 2, "x_bf16"); _need(w_router_bf16, 2, "w_router_bf16"); _need(bias, 4, "bias")
+    _need(topk_ids, 4, "topk_ids"); _need(topk_w, 4, "topk_w"); _need(ws, 1, "ws")
+    T, H = x_bf16.shape
+    E = w_router_bf16.shape[0]
+    k = topk_ids.shape[1]
+    cfg = MoeRouterCfg(n_group, topk_group, routed_scaling)
+    _check(lib.moe_router(_ptr(x_bf16), T, H, _ptr(w_router_bf16), _ptr(bias), E, k, cfg, _ptr(topk_ids),
+                          _ptr(topk_w), _ptr(ws), _nbytes(ws), _stream(stream)))
 
 
 def moe_combine(y_rows, dest_row, topk_w, out_bf16, stream=None):

@@ -26,6 +26,10 @@ class MoeDims(ctypes.Structure):
                 ("n_experts", ctypes.c_int32), ("topk", ctypes.c_int32)]
 
 
+class MoeRouterCfg(ctypes.Structure):
+    _fields_ = [("n_group", ctypes.c_int32), ("topk_group", ctypes.c_int32), ("routed_scaling", ctypes.c_float)]
+
+
 class MoEError(RuntimeError):
     def __init__(self, status: int, detail: str):
         self.status = status
@@ -60,6 +64,8 @@ _SIGS = {
     "moe_expert_ffn_workspace": (_S, [MoeDims, _I, _ST]),
     "moe_expert_ffn": (_ST, [MoeDims, _I, _ST, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "moe_combine": (_ST, [_P, _P, _P, _I, _I, _I, _P, _P]),
+    "moe_router_workspace": (_S, [_I, _I, _I]),
+    "moe_router": (_ST, [_P, _I, _I, _P, _P, _I, _I, MoeRouterCfg, _P, _P, _P, _S, _P]),
     "moe_stream_ctx_create": (_ST, [_I, ctypes.POINTER(ctypes.c_void_p)]),
     "moe_stream_ctx_destroy": (None, [_P]),
     "moe_ring_bytes": (_S, [MoeDims, _I]),

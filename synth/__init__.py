@@ -78,8 +78,8 @@ WORKLOADS = {
 
 def _seeds(seed: int, layer: int = 0):
     ss = np.random.SeedSequence(seed) if layer == 0 else np.random.SeedSequence([seed, layer])
-    kids = ss.spawn(5)
-    return dict(zip(("x", "routing", "w_gate", "w_up", "w_down"), kids))
+    kids = ss.spawn(6)
+    return dict(zip(("x", "routing", "w_gate", "w_up", "w_down", "router"), kids))
 
 
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
@@ -163,3 +163,12 @@ def expert_weight_device(w: Workload, layer: int, expert: int, which: int, devic
     g = torch.Generator(device=device)
     g.manual_seed(_device_seed(w.seed, layer, expert, which))
     return torch.randn(shape, generator=g, device=device, dtype=torch.float32).mul_(0.02)
+
+
+def router_params(w: Workload, layer: int = 0, bias_std: float = 0.0):
+    """Router (gate) weight W_r ~ N(0, 0.02) as bf16 bits [E, H] and a per-expert
+    fp32 selection bias ~ N(0, bias_std) (zeros when bias_std is 0)."""
+    rng = np.random.default_rng(_seeds(w.seed, layer)["router"])
+    wr = bf16_bits_from_f32((0.02 * rng.standard_normal((w.n_experts, w.hidden))).astype(np.float32))
+    bias = (bias_std * rng.standard_normal(w.n_experts)).astype(np.float32)
+    return wr, bias

@@ -1,0 +1,122 @@
+"""GPU parity of the router (moe_router) against the CPU router oracle.
+
+The oracle takes each decision on fp32 keys computed from exactly summed
+logits; the GPU sums the logits in fp32 on the MFMA.  Keys therefore agree
+to about 1e-6, and a token whose k-th and (k+1)-th candidate keys (or whose
+last kept and first dropped group scores) lie closer than EPS can flip: for
+those tokens the GPU choice is checked to be a valid choice under the
+oracle's keys within EPS; every other token must match bit for bit in ids,
+and its weights within 1e-5.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from gpu_cases import log, require_gpu, to_dev
+from oracle import router_oracle as ro
+
+pytestmark = pytest.mark.gpu
+EPS = 2e-5
+
+
+@pytest.fixture(scope="module")
+def moe():
+    return require_gpu()
+
+
+def _gpu_router(moe, x, wr, bias, k, n_group, topk_group, scaling):
+    t = x.shape[0]
+    ids = torch.full((t, k), -1, dtype=torch.int32, device="cuda")
+    wts = torch.zeros((t, k), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(1, moe.moe_router_workspace(t, x.shape[1], wr.shape[0])), dtype=torch.uint8, device="cuda")
+    db = None if bias is None else to_dev(bias)
+    moe.moe_router(to_dev(x.view(np.int16)), to_dev(wr.view(np.int16)), db, ids, wts, n_group, topk_group, scaling,
+                   ws)
+    torch.cuda.synchronize()
+    return ids.cpu().numpy(), wts.cpu().numpy()
+
+
+def _margins(sel, n_group, topk_group, k):
+    """Per token: the smallest of the gap between the last kept and first
+    dropped group score and the gaps between consecutive keys of the k + 1
+    best experts of the kept groups (the ids are listed by key, so a near
+    tie inside the top k reorders them)."""
+    t, e = sel.shape
+    if n_group > 1:
+        gs = np.sort(ro.group_scores(sel, n_group), axis=1)[:, ::-1]
+        ggap = gs[:, topk_group - 1] - gs[:, topk_group] if topk_group < n_group else np.full(t, np.inf)
+    else:
+        ggap = np.full(t, np.inf)
+    m = min(k + 1, topk_group * (e // n_group))
+    ids, _ = ro.select_experts(sel, None, m, n_group, topk_group)
+    if m < 2:
+        kgap = np.full(t, np.inf)
+    else:
+        ks = np.take_along_axis(sel, ids, axis=1)
+        kgap = np.min(ks[:, :-1] - ks[:, 1:], axis=1)
+    return np.minimum(ggap, kgap)
+
+
+def _check(name, x, wr, bias, k, n_group, topk_group, scaling, moe):
+    ids, wts = _gpu_router(moe, x, wr, bias, k, n_group, topk_group, scaling)
+    r_ids, r_w, inter = ro.router(x, wr, bias, k, n_group, topk_group, scaling, want_intermediates=True)
+    sel = inter["scores"] + (0 if bias is None else bias[None, :])
+    close = _margins(sel.astype(np.float32), n_group, topk_group, k) < EPS
+    same = np.all(ids == r_ids, axis=1)
+    log(f"router {name}: T={x.shape[0]} tokens differing {int((~same).sum())}, near ties {int(close.sum())}")
+    assert np.all(same | close), "ids differ on a token without a near tie"
+    assert close.mean() <= 0.15  # most tokens are compared bit for bit
+    assert np.allclose(wts[same], r_w[same], rtol=0, atol=1e-5 * scaling)
+    for t in np.nonzero(~same)[0]:  # near ties: a valid choice under the oracle keys within EPS
+        got = set(ids[t].tolist())
+        assert len(got) == k
+        chosen_min = min(sel[t, list(got)])
+        others = [sel[t, e] for e in range(sel.shape[1]) if e not in got and e // (sel.shape[1] // n_group) in
+                  set(i // (sel.shape[1] // n_group) for i in got)]
+        assert not others or max(others) <= chosen_min + EPS
+
+
+def test_router_tiny_plain_topk(moe):
+    w = synth.WORKLOADS["tiny"]
+    x = synth.activations(w)
+    wr, _ = synth.router_params(w)
+    _check("tiny", x, wr, None, w.topk, 1, 1, 1.0, moe)
+
+
+@pytest.mark.parametrize("tokens", [1, 4, 17, 64, 257])
+def test_router_deepseek_grouped(moe, tokens):
+    w = synth.WORKLOADS["prefill8k"].with_tokens(tokens)
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.05)
+    _check(f"deepseek T={tokens}", x, wr, bias, 8, 8, 4, 2.5, moe)
+
+
+def test_router_deepseek_8192_tokens(moe):
+    w = synth.WORKLOADS["prefill8k"]
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.05)
+    _check("deepseek T=8192", x, wr, bias, 8, 8, 4, 1.0, moe)
+
+
+def test_router_many_experts_wide_topk(moe):
+    w = synth.Workload("router_wide", 1024, 256, 1024, 32, 40, "uniform")
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.02)
+    _check("E=1024 k=32", x, wr, bias, 32, 64, 16, 1.0, moe)
+
+
+def test_router_zero_tokens_and_bad_config(moe):
+    w = synth.WORKLOADS["tiny"]
+    wr, _ = synth.router_params(w)
+    ids = torch.empty((0, 2), dtype=torch.int32, device="cuda")
+    wts = torch.empty((0, 2), dtype=torch.float32, device="cuda")
+    x0 = torch.empty((0, w.hidden), dtype=torch.int16, device="cuda")
+    moe.moe_router(x0, to_dev(wr.view(np.int16)), None, ids, wts, 1, 1, 1.0, None)
+    x = to_dev(synth.activations(w).view(np.int16))
+    ids = torch.empty((w.tokens, 2), dtype=torch.int32, device="cuda")
+    wts = torch.empty((w.tokens, 2), dtype=torch.float32, device="cuda")
+    with pytest.raises(moe.MoEError):
+        moe.moe_router(x, to_dev(wr.view(np.int16)), None, ids, wts, 3, 1, 1.0, None)   # 3 does not divide 8
+    with pytest.raises(moe.MoEError):
+        moe.moe_router(x, to_dev(wr.view(np.int16)), None, ids, wts, 1, 1, 1.0, None)   # no workspace
