@@ -223,17 +223,25 @@ moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const flo
  *
  * x_bf16: device [T, H] bf16, 16-byte aligned; w_router_bf16: device [E, H]
  * bf16, 16-byte aligned; bias: device fp32 [E] or NULL (zero).
- * topk_ids: device int32 [T, k]; topk_w: device fp32 [T, k].
+ * topk_ids: device int32 [T, k]; topk_w: device fp32 [T, k].  With
+ * cfg.shared_expert >= 0 (the model's shared expert, always active, the
+ * paper's Background on DeepSeek's shared experts) both are [T, k + 1] and
+ * slot k holds (shared_expert, 1.0): with that expert's weights at index
+ * shared_expert of the stacks (E + 1 experts in moe_permute and
+ * moe_expert_ffn) the rest of the path adds it after the routed experts,
+ * out = bf16(sum_j w_j y_j + y_shared), with no other change.
  * ws: device, moe_router_workspace(T, H, E) bytes (partial logits).
  * Requires H % 32 == 0, 1 <= E <= 1024, n_group <= 64 dividing E with at
  * least two experts per group when n_group > 1, 1 <= topk_group <= n_group,
- * 1 <= k <= min(32, topk_group * E / n_group), routed_scaling > 0; else
+ * 1 <= k <= min(32, topk_group * E / n_group) (k <= 31 with a shared
+ * expert), routed_scaling > 0; else
  * MOE_ERR_INVALID_ARG before any launch.  Inputs must be finite.
  */
 typedef struct {
   int32_t n_group;       /* expert groups (1: no group limit) */
   int32_t topk_group;    /* groups kept per token */
   float routed_scaling;  /* factor on the normalised weights */
+  int32_t shared_expert; /* < 0: none; else this id is appended as slot k with weight 1.0 */
 } moe_router_cfg_t;
 size_t moe_router_workspace(int32_t T, int32_t H, int32_t E);
 moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H, const uint16_t* w_router_bf16,

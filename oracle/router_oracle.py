@@ -25,6 +25,11 @@ design notes:
   in slot order in fp32.
 
 n_group = topk_group = 1 is plain top-k.
+
+Shared expert (Background: DeepSeek's always-active shared experts): with
+shared_expert >= 0 the gate appends that id with weight 1.0 as slot k, so
+the rest of the layer adds the shared expert's output after the routed
+ones, out = bf16(sum_j w_j y_j + y_shared).
 """
 from __future__ import annotations
 
@@ -93,12 +98,21 @@ def check_router_config(e: int, k: int, n_group: int, topk_group: int):
         raise ValueError("k must be at most the number of experts in the kept groups")
 
 
+def append_shared(ids: np.ndarray, w: np.ndarray, shared_expert: int):
+    """Slot k := (shared_expert, 1.0)."""
+    t = ids.shape[0]
+    return (np.concatenate([ids, np.full((t, 1), shared_expert, np.int32)], axis=1),
+            np.concatenate([w, np.ones((t, 1), f32)], axis=1))
+
+
 def router(x_bf16, w_bf16, bias, k: int, n_group: int = 1, topk_group: int = 1, scaling: float = 1.0,
-           want_intermediates: bool = False):
+           want_intermediates: bool = False, shared_expert: int = -1):
     """Full gate: bf16 tokens [T, H] and bf16 router weights [E, H] -> ids, weights."""
     logits = router_logits(x_bf16, w_bf16)
     scores = sigmoid_f32(logits)
     ids, w = select_experts(scores, bias, k, n_group, topk_group, scaling)
+    if shared_expert >= 0:
+        ids, w = append_shared(ids, w, shared_expert)
     if want_intermediates:
         return ids, w, {"logits": logits, "scores": scores}
     return ids, w

@@ -116,15 +116,18 @@ def moe_router_workspace(T: int, H: int, E: int) -> int:
 
 
 def moe_router(x_bf16, w_router_bf16, bias, topk_ids, topk_w, n_group=1, topk_group=1, routed_scaling=1.0,
-               ws=None, stream=None):
+               ws=None, stream=None, shared_expert=-1):
     """x_bf16 [T, H], w_router_bf16 [E, H] (bf16 or 16-bit views), bias fp32 [E] or None
-    -> topk_ids int32 [T, k], topk_w fp32 [T, k]."""
+    -> topk_ids int32 [T, k], topk_w fp32 [T, k]; with shared_expert >= 0 both are
+    [T, k + 1] and the last slot is (shared_expert, 1.0)."""
     _need(x_bf16, 2, "x_bf16"); _need(w_router_bf16, 2, "w_router_bf16"); _need(bias, 4, "bias")
     _need(topk_ids, 4, "topk_ids"); _need(topk_w, 4, "topk_w"); _need(ws, 1, "ws")
     T, H = x_bf16.shape
     E = w_router_bf16.shape[0]
-    k = topk_ids.shape[1]
-    cfg = MoeRouterCfg(n_group, topk_group, routed_scaling)
+    k = topk_ids.shape[1] - (1 if shared_expert >= 0 else 0)
+    if topk_w.shape != topk_ids.shape:
+        raise ValueError("topk_w must have the shape of topk_ids")
+    cfg = MoeRouterCfg(n_group, topk_group, routed_scaling, shared_expert)
     _check(lib.moe_router(_ptr(x_bf16), T, H, _ptr(w_router_bf16), _ptr(bias), E, k, cfg, _ptr(topk_ids),
                           _ptr(topk_w), _ptr(ws), _nbytes(ws), _stream(stream)))
 

@@ -27,7 +27,8 @@ class MoeDims(ctypes.Structure):
 
 
 class MoeRouterCfg(ctypes.Structure):
-    _fields_ = [("n_group", ctypes.c_int32), ("topk_group", ctypes.c_int32), ("routed_scaling", ctypes.c_float)]
+    _fields_ = [("n_group", ctypes.c_int32), ("topk_group", ctypes.c_int32), ("routed_scaling", ctypes.c_float),
+                ("shared_expert", ctypes.c_int32)]
 
 
 class MoEError(RuntimeError):

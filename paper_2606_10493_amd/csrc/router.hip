@@ -75,10 +75,12 @@ __device__ __forceinline__ bool beats(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
+// ids / wts rows have k_out = k (+1 with a shared expert) columns.
 __global__ __launch_bounds__(256) void router_select_kernel(const float* __restrict__ part, int KS, int T, int E,
                                                             const float* __restrict__ bias, int k, int n_group,
-                                                            int topk_group, float scaling,
+                                                            int topk_group, float scaling, int shared,
                                                             int32_t* __restrict__ ids, float* __restrict__ wts) {
+  const int k_out = k + (shared >= 0 ? 1 : 0);
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // the whole wave
@@ -166,15 +168,20 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
       if (lane * per + i == bi) key[i] = -INFINITY;
     total += bs;
     if (lane == 0) {
-      ids[(int64_t)t * k + j] = bi;
-      wts[(int64_t)t * k + j] = bs;
+      ids[(int64_t)t * k_out + j] = bi;
+      wts[(int64_t)t * k_out + j] = bs;
     }
   }
-  if (lane == 0)
+  if (lane == 0) {
     for (int j = 0; j < k; ++j) {
-      float* p = wts + (int64_t)t * k + j;
+      float* p = wts + (int64_t)t * k_out + j;
       *p = (*p / total) * scaling;
     }
+    if (shared >= 0) {
+      ids[(int64_t)t * k_out + k] = shared;
+      wts[(int64_t)t * k_out + k] = 1.0f;
+    }
+  }
 }
 
 // K slices of the logits: enough workgroups for a few tokens, each slice at
@@ -213,6 +220,7 @@ extern "C" moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H,
     return fail(MOE_ERR_INVALID_ARG, "moe_router: k=%d n_group=%d topk_group=%d for E=%d", k, cfg.n_group,
                 cfg.topk_group, E);
   if (!(cfg.routed_scaling > 0.0f)) return fail(MOE_ERR_INVALID_ARG, "moe_router: routed_scaling must be > 0");
+  if (cfg.shared_expert >= 0 && k > 31) return fail(MOE_ERR_INVALID_ARG, "moe_router: k + 1 slots exceed 32");
   if (T == 0) return MOE_OK;
   if (!x_bf16 || !w_router_bf16 || !topk_ids || !topk_w) return fail(MOE_ERR_INVALID_ARG, "moe_router: null pointer");
   if (!aligned(x_bf16, 16) || !aligned(w_router_bf16, 16))
@@ -228,6 +236,6 @@ extern "C" moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H,
   moe_status_t st = check_launch("moe_router");
   if (st != MOE_OK) return st;
   MOE_LAUNCH("router_select", router_select_kernel, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, stream, part, ks, T,
-             E, bias, k, cfg.n_group, cfg.topk_group, cfg.routed_scaling, topk_ids, topk_w);
+             E, bias, k, cfg.n_group, cfg.topk_group, cfg.routed_scaling, cfg.shared_expert, topk_ids, topk_w);
   return check_launch("moe_router");
 }

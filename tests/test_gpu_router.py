@@ -120,3 +120,39 @@ def test_router_zero_tokens_and_bad_config(moe):
         moe.moe_router(x, to_dev(wr.view(np.int16)), None, ids, wts, 3, 1, 1.0, None)   # 3 does not divide 8
     with pytest.raises(moe.MoEError):
         moe.moe_router(x, to_dev(wr.view(np.int16)), None, ids, wts, 1, 1, 1.0, None)   # no workspace
+
+
+@pytest.mark.parametrize("tokens,regime", [(48, "decode"), (300, "prefill")])
+def test_router_shared_expert_full_layer(moe, tokens, regime):
+    """Router with the shared expert appended as slot k (id E, weight 1.0)
+    feeding the whole layer on E + 1 expert stacks, against the oracle gate
+    and layer; tokens whose routing matches exactly are compared."""
+    import oracle
+    from gpu_cases import bits_to_f32, quantize_weights_gpu, rel_err
+    E, k = 16, 4
+    w = synth.Workload("router_shared", 512, 256, E, k, tokens, "uniform")
+    w_stack = synth.Workload("router_shared_stack", 512, 256, E + 1, k, tokens, "uniform")
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.05)
+    ids_ref, w_ref = ro.router(x, wr, bias, k, 4, 2, 2.5, shared_expert=E)
+    d_ids = torch.empty((tokens, k + 1), dtype=torch.int32, device="cuda")
+    d_w = torch.empty((tokens, k + 1), dtype=torch.float32, device="cuda")
+    ws = torch.empty(moe.moe_router_workspace(tokens, w.hidden, E), dtype=torch.uint8, device="cuda")
+    moe.moe_router(to_dev(x.view(np.int16)), to_dev(wr.view(np.int16)), to_dev(bias), d_ids, d_w, 4, 2, 2.5, ws,
+                   shared_expert=E)
+    wg, wu, wd = synth.weights_host(w_stack)
+    dev_weights = quantize_weights_gpu(moe, wg, wu, wd)
+    reg = moe.MOE_REGIME_DECODE if regime == "decode" else moe.MOE_REGIME_PREFILL
+    buf = moe.MoELayerBuffers(w.hidden, w.inter, E + 1, k + 1, tokens, reg)
+    moe.run_layer(buf, to_dev(x.view(np.int16)), d_ids, d_w, dev_weights)
+    torch.cuda.synchronize()
+    assert int(buf.dev_status.item()) == 0
+    got_ids = d_ids.cpu().numpy()
+    assert np.all(got_ids[:, k] == E) and np.all(d_w.cpu().numpy()[:, k] == 1.0)
+    same = np.all(got_ids == ids_ref, axis=1)
+    log(f"router + shared expert, {regime}: tokens with identical routing {int(same.sum())}/{tokens}")
+    assert same.mean() >= 0.9
+    ref = oracle.bf16_to_f32(oracle.moe_layer(x, ids_ref, w_ref, oracle.prepare_weights(wg, wu, wd)))
+    err = rel_err(bits_to_f32(buf.out)[same], ref[same])
+    log(f"  out rel err vs oracle {err:.3e}")
+    assert err <= 2e-2

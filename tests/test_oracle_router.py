@@ -129,3 +129,28 @@ def test_bad_configs_raise():
         k, g, tg = args
         with pytest.raises(ValueError):
             ro.select_experts(s, None, k, g, tg)
+
+
+def test_shared_expert_slot_is_routed_sum_plus_shared():
+    """The shared slot (id E, weight 1.0, last) gives bf16(routed fp32 sum + shared rows)."""
+    import oracle
+    import synth
+    w = synth.WORKLOADS["tiny"]
+    x = synth.activations(w)
+    ids, wts = synth.routing(w)
+    wg, wu, wd = synth.weights_host(w)
+    rng = np.random.default_rng(11)
+    shared = [(0.02 * rng.standard_normal(m.shape[1:])).astype(np.float32)[None] for m in (wg, wu, wd)]
+    routed = oracle.prepare_weights(wg, wu, wd)
+    both = oracle.prepare_weights(*[np.concatenate([m, s], axis=0) for m, s in zip((wg, wu, wd), shared)])
+    ids_s, w_s = ro.append_shared(ids, wts, w.n_experts)
+    out = oracle.moe_layer(x, ids_s, w_s, both)
+    _, inter = oracle.moe_layer(x, ids, wts, routed, want_intermediates=True)
+    t, k = ids.shape
+    dest = inter["dest_row"].reshape(t, k)
+    acc = np.zeros((t, w.hidden), np.float32)
+    for j in range(k):
+        acc = (acc + (wts[:, j][:, None] * inter["y"][dest[:, j]]).astype(np.float32)).astype(np.float32)
+    sq = oracle.prepare_weights(*shared)
+    y_sh = oracle.expert_rows(inter["qx"], inter["sx"], sq[0][0], sq[1][0], sq[2][0], sq[3][0], sq[4][0], sq[5][0])
+    assert np.array_equal(out, oracle.f32_to_bf16((acc + y_sh).astype(np.float32)))
