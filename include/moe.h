@@ -194,6 +194,29 @@ moe_status_t moe_expert_ffn(moe_dims_t dims, int32_t T, moe_regime_t regime,
                             float* y_rows, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * W8A16 expert FFN, decode regime (T <= MOE_DECODE_MAX_TOKENS): the paper's
+ * own GEMV numerics (AVX-512 FP8 GEMV Kernel, post-scaling and scale-block
+ * loop): bf16 activations, FP8 weights expanded to bf16, bf16 x bf16
+ * products accumulated in fp32 over each 128-K block, the block's weight
+ * scale applied once to the block sum, blocks summed in fp32:
+ *   G[p,n] = sum_b s_gate_e[n/128,b] * (sum_{i in b} x[t,i] * W_gate_e[n,i])
+ *   U likewise, h = bf16_rne(G * sigmoid(G) * U)   (bf16, the activation of down)
+ *   y_rows[p,n] = sum_b s_down_e[n/128,b] * (sum_{i in b} h[p,i] * W_down_e[n,i])
+ * No activation quantization: x_bf16 replaces qx/sx.  Other arguments as
+ * in moe_expert_ffn (packed weight stacks, expert_offsets, sorted_src,
+ * y_rows in expert-sorted order).  ws: moe_expert_ffn_w8a16_workspace(dims,
+ * T) bytes, 256-byte aligned (bf16 h rows).  Errors as moe_expert_ffn;
+ * T > MOE_DECODE_MAX_TOKENS is MOE_ERR_INVALID_ARG.
+ */
+size_t moe_expert_ffn_w8a16_workspace(moe_dims_t dims, int32_t T);
+moe_status_t moe_expert_ffn_w8a16(moe_dims_t dims, int32_t T, const uint16_t* x_bf16,
+                                  const int32_t* expert_offsets, const int32_t* sorted_src,
+                                  const uint8_t* w_gate, const float* s_gate,
+                                  const uint8_t* w_up, const float* s_up,
+                                  const uint8_t* w_down, const float* s_down,
+                                  float* y_rows, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * Router-weighted combine (Operator Fusion for Quantized Inference: the
  * expert outputs are accumulated with the router weights in F32 and
  * converted back to the hidden type):

@@ -339,6 +339,66 @@ def moe_layer(x_bf16, topk_ids, topk_w, weights, want_intermediates=False):
     return out
 
 
+# --------------------------------------------------------------------------
+# W8A16 -- the paper's CPU GEMV numerics (AVX-512 FP8 GEMV Kernel: FP8 weights
+# expanded to BF16, BF16 x BF16 dot products accumulated in FP32, the block's
+# scale applied once to the accumulated block sum; Tiling and Scale-Block
+# Optimizations: K walked in 128-element blocks).  Activations stay bf16; h
+# is rounded to bf16 (the hidden type) before the down projection.
+# --------------------------------------------------------------------------
+def block_scaled_matmul_w8a16(a_bf16, w_q, w_s) -> np.ndarray:
+    """C[m,n] = sum_b fl32(w_s[n/128,b] * fl32(exact sum_{i in b} a[m,i]*w[n,i])).
+
+    a_bf16 uint16 bf16 bits [M,K]; w_q u8 [N,K]; w_s f32 [N/128, K/128].
+    A bf16 x e4m3 product has at most 12 significant bits, so fp64 holds the
+    block sums exactly for activations within a 2^40 range of one another
+    (any realistic data); blocks are accumulated in ascending order in fp32.
+    """
+    a = bf16_to_f32(a_bf16).astype(np.float64)
+    w = e4m3_decode(w_q)
+    m, k = a.shape
+    n = w.shape[0]
+    acc = np.zeros((m, n), dtype=np.float32)
+    for b in range(k // BLOCK):
+        sl = slice(b * BLOCK, (b + 1) * BLOCK)
+        d = (a[:, sl] @ w[:, sl].T).astype(np.float32)
+        scale = np.repeat(w_s[:, b], BLOCK)[None, :].astype(np.float32)
+        acc = (acc + (d * scale).astype(np.float32)).astype(np.float32)
+    return acc
+
+
+def expert_rows_w8a16(x_bf16, q_gate, s_gate, q_up, s_up, q_down, s_down, want_intermediates=False):
+    """One expert on bf16 activation rows: gate, up, h = bf16(SiLU(G) * U), down."""
+    g = block_scaled_matmul_w8a16(x_bf16, q_gate, s_gate)
+    u = block_scaled_matmul_w8a16(x_bf16, q_up, s_up)
+    h = f32_to_bf16(silu_mul(g, u))
+    y = block_scaled_matmul_w8a16(h, q_down, s_down)
+    if want_intermediates:
+        return y, dict(g=g, u=u, h=h)
+    return y
+
+
+def expert_ffn_w8a16(x_bf16, expert_offsets, sorted_src, topk, weights, experts=None):
+    """W8A16 expert FFN over the expert-sorted rows (same layout as expert_ffn)."""
+    qg, sg, qu, su, qd, sd = weights
+    n_rows = int(expert_offsets[-1])
+    y = np.zeros((n_rows, qd.shape[1]), dtype=np.float32)
+    for e in range(len(expert_offsets) - 1) if experts is None else experts:
+        p0, p1 = int(expert_offsets[e]), int(expert_offsets[e + 1])
+        if p1 == p0:
+            continue
+        tok = np.asarray(sorted_src[p0:p1]) // topk
+        y[p0:p1] = expert_rows_w8a16(x_bf16[tok], qg[e], sg[e], qu[e], su[e], qd[e], sd[e])
+    return y
+
+
+def moe_layer_w8a16(x_bf16, topk_ids, topk_w, weights):
+    """The routed-expert layer with W8A16 numerics: permute -> expert FFN -> combine."""
+    offsets, sorted_src, dest_row = permute(topk_ids, weights[0].shape[0])
+    y = expert_ffn_w8a16(np.asarray(x_bf16), offsets, sorted_src, topk_ids.shape[1], weights)
+    return combine(y, dest_row, topk_w)
+
+
 def moe_layer_dense(x_bf16, topk_ids, topk_w, weights):
     """Every expert on every token, masked by routing; no permutation.
 

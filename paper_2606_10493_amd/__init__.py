@@ -111,6 +111,22 @@ def moe_expert_ffn(dims: MoeDims, T: int, regime: int, qx, sx, expert_offsets, s
                               _ptr(s_down), _ptr(y_rows), _ptr(ws), _nbytes(ws), _stream(stream)))
 
 
+def moe_expert_ffn_w8a16_workspace(dims: MoeDims, T: int) -> int:
+    return int(lib.moe_expert_ffn_w8a16_workspace(dims, T))
+
+
+def moe_expert_ffn_w8a16(dims: MoeDims, T: int, x_bf16, expert_offsets, sorted_src,
+                         w_gate, s_gate, w_up, s_up, w_down, s_down, y_rows, ws, stream=None):
+    """Decode-regime expert FFN with bf16 activations (the W8A16 GEMV numerics)."""
+    for t, nb, n in ((x_bf16, 2, "x_bf16"), (expert_offsets, 4, "expert_offsets"), (sorted_src, 4, "sorted_src"),
+                     (w_gate, 1, "w_gate"), (s_gate, 4, "s_gate"), (w_up, 1, "w_up"), (s_up, 4, "s_up"),
+                     (w_down, 1, "w_down"), (s_down, 4, "s_down"), (y_rows, 4, "y_rows"), (ws, 1, "ws")):
+        _need(t, nb, n)
+    _check(lib.moe_expert_ffn_w8a16(dims, T, _ptr(x_bf16), _ptr(expert_offsets), _ptr(sorted_src), _ptr(w_gate),
+                                    _ptr(s_gate), _ptr(w_up), _ptr(s_up), _ptr(w_down), _ptr(s_down), _ptr(y_rows),
+                                    _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
 def moe_router_workspace(T: int, H: int, E: int) -> int:
     return int(lib.moe_router_workspace(T, H, E))
 

@@ -44,6 +44,11 @@ moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, 
 
 size_t prefill_tile_workspace(const moe_dims_t& d, int32_t T);
 
+moe_status_t run_ffn_decode_w8a16(const moe_dims_t& d, int32_t T, const uint16_t* x, const int32_t* offsets,
+                                  const int32_t* sorted_src, const uint8_t* w_gate, const float* s_gate,
+                                  const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
+                                  const float* s_down, float* y_rows, uint16_t* h16, hipStream_t stream);
+
 namespace {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -124,4 +129,34 @@ extern "C" moe_status_t moe_expert_ffn(moe_dims_t d, int32_t T, moe_regime_t reg
                           y_rows, reinterpret_cast<float*>(rest), qh, sh, stream);
   return run_ffn_prefill(d, T, qx, sx, expert_offsets, sorted_src, w_gate, s_gate, w_up, s_up, w_down, s_down, y_rows,
                          qh, sh, reinterpret_cast<int32_t*>(rest), stream);
+}
+
+extern "C" size_t moe_expert_ffn_w8a16_workspace(moe_dims_t d, int32_t T) {
+  if (T < 0 || d.inter <= 0 || d.topk <= 0) return 0;
+  return align256((size_t)T * d.topk * d.inter * sizeof(uint16_t));
+}
+
+extern "C" moe_status_t moe_expert_ffn_w8a16(moe_dims_t d, int32_t T, const uint16_t* x_bf16,
+                                             const int32_t* expert_offsets, const int32_t* sorted_src,
+                                             const uint8_t* w_gate, const float* s_gate, const uint8_t* w_up,
+                                             const float* s_up, const uint8_t* w_down, const float* s_down,
+                                             float* y_rows, void* ws, size_t ws_bytes, hipStream_t stream) {
+  moe_status_t st = check_dims(d, "moe_expert_ffn_w8a16");
+  if (st != MOE_OK) return st;
+  if (T < 0 || T > MOE_DECODE_MAX_TOKENS)
+    return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn_w8a16: decode regime needs 0 <= T <= %d (T=%d)",
+                MOE_DECODE_MAX_TOKENS, T);
+  if (T == 0) return MOE_OK;
+  if (!x_bf16 || !expert_offsets || !sorted_src || !w_gate || !s_gate || !w_up || !s_up || !w_down || !s_down ||
+      !y_rows)
+    return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn_w8a16: null pointer");
+  if (!aligned(x_bf16, 16) || !aligned(w_gate, 16) || !aligned(w_up, 16) || !aligned(w_down, 16) ||
+      !aligned(y_rows, 16))
+    return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn_w8a16: misaligned pointer (16 bytes needed)");
+  const size_t need = moe_expert_ffn_w8a16_workspace(d, T);
+  if (!ws || ws_bytes < need)
+    return fail(MOE_ERR_WORKSPACE, "moe_expert_ffn_w8a16: workspace %zu bytes < %zu", ws_bytes, need);
+  if (!aligned(ws, 256)) return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn_w8a16: workspace must be 256-byte aligned");
+  return run_ffn_decode_w8a16(d, T, x_bf16, expert_offsets, sorted_src, w_gate, s_gate, w_up, s_up, w_down, s_down,
+                              y_rows, static_cast<uint16_t*>(ws), stream);
 }

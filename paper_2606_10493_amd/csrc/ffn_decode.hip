@@ -30,8 +30,17 @@
 // fragments, weight scales and activation scales, all vector loads in one
 // in-order stream, so waiting for block j never waits for a later load.
 //
+// W8A16 (A16): the paper's own GEMV numerics (AVX-512 FP8 GEMV Kernel,
+// post-scaling): bf16 activations, the FP8 weights expanded to bf16
+// (v_cvt_scalef32_pk_bf16_fp8, exact), bf16 x bf16 products accumulated in
+// fp32 over a 128-K block (four MFMA 16x16x32 bf16; the lane's 32 weight
+// bytes are split into four 8-element sub-steps and the activations are
+// read at the same K positions), and the block's weight scale applied once
+// to the block sum.  h is written in bf16 and is the down projection's
+// activation.
+//
 // GATEUP: the tile holds the same 16*NT rows of W_gate and W_up, and the
-// epilogue writes h = SiLU(G) * U in fp32.  Down: h is quantized per row per
+// epilogue writes h = SiLU(G) * U in fp32 (bf16 with A16).  Down: h is quantized per row per
 // 128 (QH: in this kernel's prologue, for at most kQhRows rows per expert;
 // else by a separate launch) and the epilogue writes the fp32 expert rows.
 #include "common.h"
@@ -40,6 +49,7 @@ namespace moe {
 
 struct DecodeArgs {
   const uint8_t* a;           // e4m3 [a_rows, K]
+  const uint16_t* a16;        // A16: bf16 activations [a_rows, K] (a, sa unused)
   const float* sa;            // fp32 [a_rows, K/128]
   const int32_t* sorted_src;  // row p of the expert-sorted order reads A row sorted_src[p]/topk; NULL: A row p
   int topk;
@@ -52,6 +62,7 @@ struct DecodeArgs {
   const float* s1;
   int N, K;
   float* out;                 // fp32 [rows, N]
+  uint16_t* out16;            // A16 GATEUP: bf16 h [rows, N] (out unused)
   const float* hf;            // QH: fp32 h rows [rows, K] quantized in the prologue
 };
 
@@ -103,9 +114,22 @@ __device__ __forceinline__ ExpertRef find_expert(const int32_t* __restrict__ off
   return ref;
 }
 
-template <int MT, int NT, bool GATEUP, bool QH, int U>
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Eight e4m3 weight bytes (two dwords) -> eight bf16 values, byte order kept.
+__device__ __forceinline__ bf16x8 e4m3x8_to_bf16(int d0, int d1) {
+  const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((unsigned)d0, 1.0f, false);
+  const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((unsigned)d0, 1.0f, true);
+  const bf16x2 c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((unsigned)d1, 1.0f, false);
+  const bf16x2 e = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((unsigned)d1, 1.0f, true);
+  return bf16x8{a[0], a[1], b[0], b[1], c[0], c[1], e[0], e[1]};
+}
+
+template <int MT, int NT, bool GATEUP, bool QH, int U, bool A16 = false>
 __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   static_assert(!QH || (!GATEUP && MT == 1), "QH is the down projection with at most 16 rows");
+  static_assert(!(A16 && QH), "W8A16 reads bf16 h rows directly");
   static_assert(!GATEUP || NT == 1, "a GATEUP tile is 16 rows of W_gate and of W_up");
   constexpr bool kSplit = GATEUP && MT == 1;  // one matrix per wave (waves 0, 1 gate; 2, 3 up)
   constexpr int G = (GATEUP && !kSplit) ? 2 : 1;  // weight matrices per wave
@@ -274,7 +298,7 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
             const int row = 4 * kq + i;
             sa[0][i] = row < kQhRows ? sh_lds[row * (kQhMaxK / kBlock) + bk] : 0.0f;
           }
-        } else {
+        } else if (!A16) {
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
             afrag[mt] = ta[mt] >= 0 ? load_v8i_ksplit(p.a + (int64_t)ta[mt] * p.K + bk * kBlock + kq * 16)
@@ -283,16 +307,52 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
             for (int i = 0; i < 4; ++i) sa[mt][i] = ts[mt][i] >= 0 ? p.sa[(int64_t)ts[mt][i] * nb + bk] : 0.0f;
           }
         }
+        if constexpr (A16) {
+          // Activations at the weight bytes' K positions: sub-step s covers
+          // weight dwords 2s, 2s+1, i.e. K 16kq + [0,8), 16kq + [8,16),
+          // 64 + 16kq + [0,8), 64 + 16kq + [8,16) of the block.
+          bf16x8 a16[MT][4];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+          for (int mt = 0; mt < MT; ++mt) {
+            if (ta[mt] >= 0) {
+              const uint16_t* src = p.a16 + (int64_t)ta[mt] * p.K + bk * kBlock + 16 * kq;
+              a16[mt][0] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(src));
+              a16[mt][1] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(src + 8));
+              a16[mt][2] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(src + 64));
+              a16[mt][3] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(src + 72));
+            } else {
+#pragma unroll
+              for (int q = 0; q < 4; ++q) a16[mt][q] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
+            }
+          }
 #pragma unroll
           for (int g = 0; g < G; ++g)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
-              const v4f part = mfma_f8_16x16x128(afrag[mt], w[g][nt]);
+              bf16x8 wb[4];
 #pragma unroll
-              for (int i = 0; i < 4; ++i) acc[g][mt][nt][i] += part[i] * (sa[mt][i] * ws[g]);
+              for (int q = 0; q < 4; ++q) wb[q] = e4m3x8_to_bf16(w[g][nt][2 * q], w[g][nt][2 * q + 1]);
+#pragma unroll
+              for (int mt = 0; mt < MT; ++mt) {
+                v4f part = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) part = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a16[mt][q], wb[q], part, 0, 0, 0);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[g][mt][nt][i] += part[i] * ws[g];
+              }
             }
+        } else {
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+              for (int nt = 0; nt < NT; ++nt) {
+                const v4f part = mfma_f8_16x16x128(afrag[mt], w[g][nt]);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[g][mt][nt][i] += part[i] * (sa[mt][i] * ws[g]);
+              }
+        }
       };
 
       // K loop: block 0 was loaded above; each later block's loads are
@@ -365,7 +425,9 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
                 if (kSplit) v = silu_mul(acc[0][mt][nt][i], up[mt][nt][i]);
                 else if (GATEUP) v = silu_mul(acc[0][mt][nt][i], acc[G - 1][mt][nt][i]);
                 else v = acc[0][mt][nt][i];
-                p.out[(int64_t)(p0 + mb + m) * p.N + n0 + nt * 16 + r] = v;
+                const int64_t at = (int64_t)(p0 + mb + m) * p.N + n0 + nt * 16 + r;
+                if (A16 && GATEUP) p.out16[at] = f32_to_bf16_rne(v);
+                else p.out[at] = v;
               }
             }
       }
@@ -374,13 +436,14 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   }
 }
 
-template <int MT, int NT, bool GATEUP, bool QH, int U>
+template <int MT, int NT, bool GATEUP, bool QH, int U, bool A16 = false>
 moe_status_t launch_decode(const DecodeArgs& a, int64_t max_items, hipStream_t stream) {
   const int64_t grid = max_items < 2048 ? max_items : 2048;
   if (grid <= 0) return MOE_OK;
-  MOE_LAUNCH(GATEUP ? "ffn_decode_gateup" : "ffn_decode_down", (ffn_decode_kernel<MT, NT, GATEUP, QH, U>),
-             dim3((unsigned)grid), dim3(256), 0, stream, a);
-  return check_launch(GATEUP ? "ffn_decode_gateup" : "ffn_decode_down");
+  const char* name = A16 ? (GATEUP ? "ffn_decode_w8a16_gateup" : "ffn_decode_w8a16_down")
+                         : (GATEUP ? "ffn_decode_gateup" : "ffn_decode_down");
+  MOE_LAUNCH(name, (ffn_decode_kernel<MT, NT, GATEUP, QH, U, A16>), dim3((unsigned)grid), dim3(256), 0, stream, a);
+  return check_launch(name);
 }
 
 }  // namespace
@@ -424,6 +487,38 @@ moe_status_t run_ffn_decode(const moe_dims_t& d, int32_t T, const uint8_t* qx, c
   if (T <= 16) return launch_decode<1, 2, false, false, 4>(dn, dn_items, stream);
   if (T <= 32) return launch_decode<2, 2, false, false, 2>(dn, dn_items, stream);
   return launch_decode<4, 2, false, false, 2>(dn, dn_items, stream);
+}
+
+// W8A16 decode FFN: bf16 activations, gate/up -> h (bf16) -> down.
+moe_status_t run_ffn_decode_w8a16(const moe_dims_t& d, int32_t T, const uint16_t* x, const int32_t* offsets,
+                                  const int32_t* sorted_src, const uint8_t* w_gate, const float* s_gate,
+                                  const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
+                                  const float* s_down, float* y_rows, uint16_t* h16, hipStream_t stream) {
+  const int64_t R = (int64_t)T * d.topk;
+  const int64_t max_active = R < d.n_experts ? R : d.n_experts;
+  if (d.hidden / kBlock > 64 * 2 || d.inter / kBlock > 64 * kWaves)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "decode regime supports H <= %d and I <= %d", 64 * 2 * kBlock,
+                64 * kWaves * kBlock);
+  DecodeArgs g{};
+  g.a16 = x; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = T;
+  g.offsets = offsets; g.E = d.n_experts;
+  g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
+  g.N = d.inter; g.K = d.hidden; g.out16 = h16;
+  const int64_t gu_items = max_active * (d.inter / 16);
+  moe_status_t st;
+  if (T <= 16) st = launch_decode<1, 1, true, false, 3, true>(g, gu_items, stream);
+  else if (T <= 32) st = launch_decode<2, 1, true, false, 2, true>(g, gu_items, stream);
+  else st = launch_decode<4, 1, true, false, 2, true>(g, gu_items, stream);
+  if (st != MOE_OK) return st;
+  DecodeArgs dn{};
+  dn.a16 = h16; dn.sorted_src = nullptr; dn.topk = d.topk; dn.a_rows = (int)R;
+  dn.offsets = offsets; dn.E = d.n_experts;
+  dn.w0 = w_down; dn.s0 = s_down;
+  dn.N = d.hidden; dn.K = d.inter; dn.out = y_rows;
+  const int64_t dn_items = max_active * (d.hidden / 32);
+  if (T <= 16) return launch_decode<1, 2, false, false, 4, true>(dn, dn_items, stream);
+  if (T <= 32) return launch_decode<2, 2, false, false, 2, true>(dn, dn_items, stream);
+  return launch_decode<4, 2, false, false, 2, true>(dn, dn_items, stream);
 }
 
 }  // namespace moe

@@ -2,7 +2,9 @@
 
 ``MoELayerBuffers`` owns the device buffers of one (dims, tokens) shape;
 ``run_layer`` enqueues moe_quant_act -> moe_permute -> moe_expert_ffn ->
-moe_combine on one stream.  Nothing is computed in Python.
+moe_combine on one stream (with ``w8a16``: moe_permute ->
+moe_expert_ffn_w8a16 -> moe_combine, bf16 activations, decode regime).
+Nothing is computed in Python.
 """
 from __future__ import annotations
 
@@ -14,7 +16,7 @@ from ._lib import MoeDims
 
 class MoELayerBuffers:
     def __init__(self, hidden: int, inter: int, n_experts: int, topk: int, tokens: int,
-                 regime: int = _lib.MOE_REGIME_AUTO, device="cuda", with_status: bool = True):
+                 regime: int = _lib.MOE_REGIME_AUTO, device="cuda", with_status: bool = True, w8a16: bool = False):
         self.dims = MoeDims(hidden, inter, n_experts, topk)
         self.tokens = tokens
         self.regime = regime
@@ -28,7 +30,9 @@ class MoELayerBuffers:
         self.dev_status = torch.zeros(1, dtype=torch.int32, device=dev) if with_status else None
         pws = _lib.lib.moe_permute_workspace(t, k, e)
         self.perm_ws = torch.empty(max(pws, 1), dtype=torch.uint8, device=dev)
-        fws = _lib.lib.moe_expert_ffn_workspace(self.dims, t, regime)
+        self.w8a16 = w8a16
+        fws = (_lib.lib.moe_expert_ffn_w8a16_workspace(self.dims, t) if w8a16
+               else _lib.lib.moe_expert_ffn_workspace(self.dims, t, regime))
         self.ffn_ws = torch.empty(max(fws, 256), dtype=torch.uint8, device=dev)
         self.y_rows = torch.empty((t * k, h), dtype=torch.float32, device=dev)
         self.out = torch.empty((t, h), dtype=torch.int16, device=dev)
@@ -36,12 +40,17 @@ class MoELayerBuffers:
 
 def run_layer(buf: MoELayerBuffers, x_bf16, topk_ids, topk_w, weights, stream=None):
     """weights = (w_gate, s_gate, w_up, s_up, w_down, s_down) device tensors."""
-    from . import moe_quant_act, moe_permute, moe_expert_ffn, moe_combine
+    from . import moe_quant_act, moe_permute, moe_expert_ffn, moe_expert_ffn_w8a16, moe_combine
     wg, sg, wu, su, wd, sd = weights
-    moe_quant_act(x_bf16, buf.qx, buf.sx, stream)
+    if not buf.w8a16:
+        moe_quant_act(x_bf16, buf.qx, buf.sx, stream)
     moe_permute(topk_ids, buf.dims.n_experts, buf.expert_offsets, buf.sorted_src, buf.dest_row,
                 buf.dev_status, buf.perm_ws, stream)
-    moe_expert_ffn(buf.dims, buf.tokens, buf.regime, buf.qx, buf.sx, buf.expert_offsets, buf.sorted_src,
-                   wg, sg, wu, su, wd, sd, buf.y_rows, buf.ffn_ws, stream)
+    if buf.w8a16:
+        moe_expert_ffn_w8a16(buf.dims, buf.tokens, x_bf16, buf.expert_offsets, buf.sorted_src,
+                             wg, sg, wu, su, wd, sd, buf.y_rows, buf.ffn_ws, stream)
+    else:
+        moe_expert_ffn(buf.dims, buf.tokens, buf.regime, buf.qx, buf.sx, buf.expert_offsets, buf.sorted_src,
+                       wg, sg, wu, su, wd, sd, buf.y_rows, buf.ffn_ws, stream)
     moe_combine(buf.y_rows, buf.dest_row, topk_w, buf.out, stream)
     return buf.out

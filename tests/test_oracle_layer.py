@@ -236,3 +236,82 @@ def test_tiny_config_layer_output_is_finite_and_nontrivial():
     out = oracle.bf16_to_f32(oracle.moe_layer(x, ids, wts, weights))
     assert out.shape == (w.tokens, w.hidden)
     assert np.all(np.isfinite(out)) and np.std(out) > 0
+
+
+# ------------------------------------------------------------------- W8A16
+def test_w8a16_matmul_exact_on_grid_with_power_of_two_scales():
+    """bf16 small integers times small-integer e4m3 codes with 2^j block
+    scales: exact at every step, equal to the fp64 double sum."""
+    rng = np.random.default_rng(17)
+    m, n, k = 3, 256, 384
+    ints = np.array([-4, -3, -2, -1, 0, 1, 2, 3, 4], dtype=np.float32)
+    a = rng.choice(ints, size=(m, k)) * np.float32(1.5)     # bf16-exact
+    w = rng.choice(ints, size=(n, k))
+    a_bits = synth.bf16_bits_from_f32(a)
+    w_q = oracle.e4m3_encode(w)
+    w_s = np.ldexp(1.0, rng.integers(-3, 4, size=(n // 128, k // 128))).astype(np.float32)
+    got = oracle.block_scaled_matmul_w8a16(a_bits, w_q, w_s)
+    ref = np.zeros((m, n))
+    for i in range(m):
+        for j in range(n):
+            ref[i, j] = sum(float(np.dot(a[i, b * 128:(b + 1) * 128].astype(np.float64),
+                                         w[j, b * 128:(b + 1) * 128].astype(np.float64))) * float(w_s[j // 128, b])
+                            for b in range(k // 128))
+    assert np.array_equal(got.astype(np.float64), ref)
+
+
+def test_w8a16_matmul_close_to_fp64_dequantized_product():
+    rng = np.random.default_rng(18)
+    x = synth.bf16_bits_from_f32(rng.standard_normal((7, 512)).astype(np.float32))
+    w = (0.02 * rng.standard_normal((256, 512))).astype(np.float32)
+    w_q, w_s = oracle.quantize_weight(w)
+    w_deq = torch.from_numpy(w_q).view(torch.float8_e4m3fn).double().numpy() \
+        * np.kron(w_s.astype(np.float64), np.ones((128, 128)))
+    xd = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).double().numpy()
+    ref = xd @ w_deq.T
+    got = oracle.block_scaled_matmul_w8a16(x, w_q, w_s)
+    assert np.max(np.abs(got - ref)) / np.max(np.abs(ref)) < 1e-6
+
+
+def test_w8a16_single_expert_identity_against_independent_dense_ffn():
+    """E = 1, k = 1, w = 1: bf16(FFN(x)) with bf16 activations, torch casts, fp64 GEMMs."""
+    rng = np.random.default_rng(19)
+    t, hdim, idim = 12, 384, 256
+    x = synth.bf16_bits_from_f32(rng.standard_normal((t, hdim)).astype(np.float32))
+    mats = [(0.02 * rng.standard_normal(s)).astype(np.float32) for s in ((1, idim, hdim), (1, idim, hdim),
+                                                                         (1, hdim, idim))]
+    weights = oracle.prepare_weights(*mats)
+    out = oracle.bf16_to_f32(oracle.moe_layer_w8a16(x, np.zeros((t, 1), np.int32), np.ones((t, 1), np.float32),
+                                                    weights))
+
+    def deq(m32):
+        n, k = m32.shape
+        blk = torch.from_numpy(m32).reshape(n // 128, 128, k // 128, 128)
+        s = blk.abs().amax(dim=(1, 3), keepdim=True) / torch.tensor(448.0)
+        return ((blk / s).clamp(-448, 448).to(torch.float8_e4m3fn).double() * s.double()).reshape(n, k)
+
+    xt = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).double()
+    g = xt @ deq(mats[0][0]).T
+    u = xt @ deq(mats[1][0]).T
+    h = (g * torch.sigmoid(g) * u).to(torch.bfloat16).double()
+    ref = (h @ deq(mats[2][0]).T).numpy()
+    err = np.max(np.abs(out - ref)) / np.max(np.abs(ref))
+    assert err < 5e-3, err
+
+
+def test_w8a16_and_w8a8_differ_by_the_activation_quantization_only():
+    """With activations already on the e4m3 grid of their row scales (block
+    amax 448, so qx = x exactly) and h likewise, W8A8 and W8A16 agree within
+    fp32 rounding: the modes differ only in where the activations are rounded."""
+    rng = np.random.default_rng(20)
+    m, k, n = 4, 256, 128
+    a = oracle.e4m3_decode(oracle.e4m3_encode((rng.standard_normal((m, k)) * 64).astype(np.float32)))
+    a[:, 0] = 448.0
+    a[:, 128] = 448.0
+    a_bits = synth.bf16_bits_from_f32(a.astype(np.float32))   # e4m3 values are bf16-exact
+    a_q, a_s = oracle.quantize_rows(a.astype(np.float32))
+    assert np.all(a_s == 1.0)
+    w_q, w_s = oracle.quantize_weight((0.02 * rng.standard_normal((n, k))).astype(np.float32))
+    r8 = oracle.block_scaled_matmul(a_q, a_s, w_q, w_s)
+    r16 = oracle.block_scaled_matmul_w8a16(a_bits, w_q, w_s)
+    assert np.array_equal(r8, r16)
