@@ -33,11 +33,13 @@ METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
 
 # HBM bytes per launch of a kernel, from rocprofv3 FETCH_SIZE and WRITE_SIZE
 # runs scaled by a plain 1 GiB copy (FETCH x2.000, WRITE x1.000), recorded in
-# profiles/ffn_decode_gateup__deepseek_v3_decode_T1_hbm_traffic.md.  Valid only
-# while the kernel's source file is the one measured (sha256 prefix).
+# profiles/*_hbm_traffic.md.  Valid only while the kernel's source file is the
+# one measured (sha256 prefix).
 TRAFFIC = {
-    ("decode1", "ffn_decode_gateup"): {"bytes": 235616666, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
-                                       "sha256_prefix": "2dbf012cc1a872fd"},
+    ("decode1", "ffn_decode_gateup"): {"bytes": 235601715, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
+                                       "sha256_prefix": "39c437a5dfceacb3"},
+    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9573711565, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
+                                          "sha256_prefix": "79d78fd7c93d1996"},
 }
 
 
@@ -59,7 +61,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="decode1")
     ap.add_argument("--layers", type=int, default=0, help="weight layers to rotate over (0: auto)")
-    ap.add_argument("--also", default="decode4", help="comma list of extra workloads (summary only)")
+    ap.add_argument("--also", default="decode4,decode1_w8a16,router",
+                    help="comma list of extra workloads (summary only); NAME_w8a16 runs the W8A16 decode FFN, "
+                         "router times the gate on the main workload's tokens")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -108,7 +112,7 @@ def algorithmic(w, ids):
     }
 
 
-def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache):
+def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache, w8a16=False):
     import numpy as np
     w = synth.WORKLOADS[name]
     if w.chunk_tokens:
@@ -122,7 +126,7 @@ def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache
         log(f"drawing and quantizing weight layer {len(layers_cache)} on the GPU")
         layers_cache.append(make_layer(moe, torch, synth, w, len(layers_cache)))
     layers = layers_cache[:layers_n]
-    buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, with_status=False)
+    buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, with_status=False, w8a16=w8a16)
     stream = torch.cuda.current_stream()
 
     def step(i):
@@ -153,6 +157,38 @@ def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache
     if not np.all(np.isfinite((out.view(np.uint16).astype(np.uint32) << 16).view(np.float32))):
         raise RuntimeError("non-finite output")
     return w, ids, wts, x, ms, kern_us
+
+
+def time_router(moe, torch, synth, w, steps, warmup):
+    """The gate (moe_router) on the workload's tokens: DeepSeek-V3 grouping
+    (8 groups, 4 kept), bf16 router weight [E, H], per-expert bias."""
+    import numpy as np
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.05)
+    dx = torch.from_numpy(x.view(np.int16)).cuda()
+    dwr = torch.from_numpy(wr.view(np.int16)).cuda()
+    db = torch.from_numpy(bias).cuda()
+    ids = torch.empty((w.tokens, w.topk), dtype=torch.int32, device="cuda")
+    wts = torch.empty((w.tokens, w.topk), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(1, moe.moe_router_workspace(w.tokens, w.hidden, w.n_experts)), dtype=torch.uint8,
+                     device="cuda")
+    groups = 8 if w.n_experts % 8 == 0 and w.n_experts >= 16 else 1
+
+    def call():
+        moe.moe_router(dx, dwr, db, ids, wts, groups, min(4, groups), 1.0, ws)
+
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    moe.moe_profile_begin(4 * steps)
+    for _ in range(steps):
+        call()
+    prof = moe.moe_profile_end()
+    torch.cuda.synchronize()
+    kern = {}
+    for kname, kms in prof:
+        kern.setdefault(kname, []).append(kms)
+    return {kk: round(1000.0 * sum(v) / len(v), 2) for kk, v in kern.items()}
 
 
 def time_streamed(moe, torch, synth, name, steps, warmup):
@@ -341,15 +377,21 @@ def main():
         us = kern_us[dom]
         achieved = alg["gateup_flops"] / (us * 1e-6) / 1e12
         roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": FP8_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
+                "traffic": measured_traffic(args.workload, dom),
                 "per_launch": {"algorithmic_flops": alg["gateup_flops"], "avg_us": round(us, 2)}}
     layer_gbs = alg["layer_weight_bytes"] / (ms * 1e-3) / 1e9
     layer_tflops = (alg["gateup_flops"] + alg["down_flops"]) / (ms * 1e-3) / 1e12
     also = {}
     for extra in [a for a in args.also.split(",") if a and a != args.workload]:
+        if extra == "router":
+            also["router"] = {"tokens": w.tokens, "kernel_us": time_router(moe, torch, synth, w, args.steps,
+                                                                          args.warmup)}
+            continue
+        base_name, w8a16 = (extra[:-len("_w8a16")], True) if extra.endswith("_w8a16") else (extra, False)
         try:
-            we, ide, _, _, mse, kue = time_workload(moe, torch, synth, extra, args.steps, args.warmup,
-                                                    layers_n, cache)
+            we, ide, _, _, mse, kue = time_workload(moe, torch, synth, base_name, args.steps, args.warmup,
+                                                    layers_n, cache, w8a16=w8a16)
         except SystemExit as exc:
             also[extra] = {"skipped": str(exc)}
             continue

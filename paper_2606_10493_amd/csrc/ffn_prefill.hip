@@ -39,8 +39,9 @@
 //
 // Work items are (expert m-tile, n-tile) pairs; m-tiles of all experts are
 // numbered by an exclusive scan of ceil(M_e / 128) (prefill_tiles_kernel),
-// and an expert's items are ordered n-tile major, so the m-tiles sharing a
-// weight slice are neighbours.  Work items are assigned XCD-major: the
+// an expert's 32-row groups are dealt evenly over its m-tiles, and its
+// items are ordered n-tile major, so the m-tiles sharing a weight slice are
+// neighbours of similar size.  Work items are assigned XCD-major: the
 // hardware deals workgroups to the 8 XCDs round-robin, so with n real items
 // (read from the tile scan; the grid is only an upper bound) item = (block
 // % 8) * ceil(n / 8) + block / 8 keeps an expert's items on one XCD's L2
@@ -149,10 +150,21 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
       const int mcount = s1 - s0;
       const int ntx = (int)(local / mcount);
       const int mt = (int)(local - (int64_t)ntx * mcount);
-      const int first = o0 + mt * kBM;
+      // The expert's ceil(M/32) row groups are dealt evenly over its
+      // mcount tiles (tile mt gets q/mcount groups, one more for mt <
+      // q % mcount): the same MFMA work as full tiles plus a tail, but
+      // tiles of similar size, which advance through their shared weight
+      // slice at similar speed, so the slice is fetched from HBM once and
+      // read by the others from L2 (a 1-32-row tail tile ran about 3.6
+      // times faster than the full tiles and fetched the slice ahead of
+      // them; gate/up read 1.7 times its algorithmic bytes).
+      const int q = (o1 - o0 + 31) >> 5;
+      const int base = q / mcount, extra = q - base * mcount;
+      const int first = o0 + 32 * (mt * base + min(mt, extra));
+      const int groups = base + (mt < extra ? 1 : 0);
       tile_info[0] = x;
       tile_info[1] = first;
-      tile_info[2] = min(kBM, o1 - first);
+      tile_info[2] = min(32 * groups, o1 - first);
       tile_info[3] = ntx;
     }
   }

@@ -81,6 +81,7 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
                                                             int topk_group, float scaling, int shared,
                                                             int32_t* __restrict__ ids, float* __restrict__ wts) {
   const int k_out = k + (shared >= 0 ? 1 : 0);
+  __shared__ float chosen[4][32];  // the chosen experts' scores of each wave's token
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // the whole wave
@@ -93,8 +94,16 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
     s[i] = 0.0f;
     key[i] = -INFINITY;
     if (i < per && e < E) {
+      // Slices summed in slice order; the loads of 16 slices go out together.
       float l = 0.0f;
-      for (int q = 0; q < KS; ++q) l += part[((int64_t)q * T + t) * E + e];
+      for (int q0 = 0; q0 < KS; q0 += 16) {
+        float v[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) v[q] = q0 + q < KS ? part[((int64_t)(q0 + q) * T + t) * E + e] : 0.0f;
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          if (q0 + q < KS) l += v[q];
+      }
       s[i] = 1.0f / (1.0f + expf(-l));
       key[i] = s[i] + (bias ? bias[e] : 0.0f);
     }
@@ -169,14 +178,11 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
     total += bs;
     if (lane == 0) {
       ids[(int64_t)t * k_out + j] = bi;
-      wts[(int64_t)t * k_out + j] = bs;
+      chosen[threadIdx.x >> 6][j] = bs;
     }
   }
   if (lane == 0) {
-    for (int j = 0; j < k; ++j) {
-      float* p = wts + (int64_t)t * k_out + j;
-      *p = (*p / total) * scaling;
-    }
+    for (int j = 0; j < k; ++j) wts[(int64_t)t * k_out + j] = (chosen[threadIdx.x >> 6][j] / total) * scaling;
     if (shared >= 0) {
       ids[(int64_t)t * k_out + k] = shared;
       wts[(int64_t)t * k_out + k] = 1.0f;
