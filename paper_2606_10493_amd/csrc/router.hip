@@ -75,7 +75,9 @@ __device__ __forceinline__ bool beats(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
-// ids / wts rows have k_out = k (+1 with a shared expert) columns.
+// ids / wts rows have k_out = k (+1 with a shared expert) columns.  PER:
+// experts per lane (lane l holds experts l*PER .. l*PER + PER - 1).
+template <int PER>
 __global__ __launch_bounds__(256) void router_select_kernel(const float* __restrict__ part, int KS, int T, int E,
                                                             const float* __restrict__ bias, int k, int n_group,
                                                             int topk_group, float scaling, int shared,
@@ -85,8 +87,29 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // the whole wave
-  const int per = (E + 63) / 64;  // experts per lane: lane l holds l*per .. l*per + per - 1
+  constexpr int per = PER;
   const int epg = E / n_group;
+  // Logits: the KS slices summed in slice order; QB slices of all the lane's
+  // experts are loaded before any is added (a few tokens have many slices).
+  constexpr int QB = 128 / PER;
+  float lg[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) lg[i] = 0.0f;
+  for (int q0 = 0; q0 < KS; q0 += QB) {
+    float v[QB][PER];
+#pragma unroll
+    for (int q = 0; q < QB; ++q)
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int e = lane * PER + i;
+        v[q][i] = (q0 + q < KS && e < E) ? part[((int64_t)(q0 + q) * T + t) * E + e] : 0.0f;
+      }
+#pragma unroll
+    for (int q = 0; q < QB; ++q)
+#pragma unroll
+      for (int i = 0; i < PER; ++i)
+        if (q0 + q < KS) lg[i] += v[q][i];
+  }
   float s[kRouterMaxPerLane], key[kRouterMaxPerLane];
 #pragma unroll
   for (int i = 0; i < kRouterMaxPerLane; ++i) {
@@ -94,17 +117,7 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
     s[i] = 0.0f;
     key[i] = -INFINITY;
     if (i < per && e < E) {
-      // Slices summed in slice order; the loads of 16 slices go out together.
-      float l = 0.0f;
-      for (int q0 = 0; q0 < KS; q0 += 16) {
-        float v[16];
-#pragma unroll
-        for (int q = 0; q < 16; ++q) v[q] = q0 + q < KS ? part[((int64_t)(q0 + q) * T + t) * E + e] : 0.0f;
-#pragma unroll
-        for (int q = 0; q < 16; ++q)
-          if (q0 + q < KS) l += v[q];
-      }
-      s[i] = 1.0f / (1.0f + expf(-l));
+      s[i] = 1.0f / (1.0f + expf(-lg[i]));
       key[i] = s[i] + (bias ? bias[e] : 0.0f);
     }
   }
@@ -241,7 +254,16 @@ extern "C" moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H,
              part);
   moe_status_t st = check_launch("moe_router");
   if (st != MOE_OK) return st;
-  MOE_LAUNCH("router_select", router_select_kernel, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, stream, part, ks, T,
-             E, bias, k, cfg.n_group, cfg.topk_group, cfg.routed_scaling, cfg.shared_expert, topk_ids, topk_w);
+  const int per = (E + 63) / 64;
+  const dim3 sgrid((unsigned)((T + 3) / 4));
+#define MOE_ROUTER_SELECT(P)                                                                                  \
+  MOE_LAUNCH("router_select", router_select_kernel<P>, sgrid, dim3(256), 0, stream, part, ks, T, E, bias, k,  \
+             cfg.n_group, cfg.topk_group, cfg.routed_scaling, cfg.shared_expert, topk_ids, topk_w)
+  if (per <= 1) MOE_ROUTER_SELECT(1);
+  else if (per <= 2) MOE_ROUTER_SELECT(2);
+  else if (per <= 4) MOE_ROUTER_SELECT(4);
+  else if (per <= 8) MOE_ROUTER_SELECT(8);
+  else MOE_ROUTER_SELECT(16);
+#undef MOE_ROUTER_SELECT
   return check_launch("moe_router");
 }
