@@ -24,8 +24,8 @@ computes, written from the paper:
   Parallelism: tokens are sorted by expert into per-expert token lists.
 
 Readings where the paper is silent (each also listed in the design notes):
-OCP E4M3 with max 448 and NaN at S.1111.111 (the paper's "without NaNs" is
-read as "no infinities"); the scale is a multiplicative dequantization
+OCP E4M3 with max 448 and NaN at S.1111.111 (the paper describes the
+format as free of NaNs; read as free of infinities, the OCP "FN" variant); the scale is a multiplicative dequantization
 factor s = amax/448; x/s is a correctly rounded fp32 division; rounding to
 e4m3 is to nearest with ties to the even code, |v| > 448 saturates to 448,
 the sign of zero is kept; an all-zero block gets s = 0 and signed-zero

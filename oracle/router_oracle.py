@@ -3,12 +3,11 @@
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import or run this module; the GPU library never does.
 
-The paper (Background, Mixture-of-Experts) states only that a learned gating
-mechanism picks a small subset of experts per token, "top-k or grouped
-top-k", and that SmallEP evaluates the gate and sorts tokens locally.  It
-gives no formula, tie-break or group rule, so this oracle follows one
-reading, the DeepSeek-V3 gate the paper's target models use, listed in the
-design notes:
+The paper (Background, Mixture-of-Experts) says only that a learned gate
+picks a few experts per token by plain or grouped top-k selection, and that
+SmallEP evaluates the gate and sorts tokens locally.  It gives no formula,
+tie-break or group rule, so this oracle follows one reading, the DeepSeek-V3
+gate of the paper's target models:
 
 * logits[t, e] = sum_i x[t, i] * W_r[e, i], x and W_r bf16, the sum taken
   exactly (fp64 holds every bf16 x bf16 product exactly) and rounded once to

@@ -1,7 +1,7 @@
 """CPU pins of the router (gate) oracle.
 
-The paper gives no gate formula or example (Background, Mixture-of-Experts:
-"top-k or grouped top-k"), so the selection is pinned to hand-worked cases
+The paper gives no gate formula or example (Background, Mixture-of-Experts
+names only plain and grouped top-k), so the selection is pinned to hand-worked cases
 of the reading (tests/golden/router_select_cases.txt), to a brute-force
 statement by pairwise comparisons on small inputs, and to plain top-k
 (numpy's sort) when there is one group; the logits to torch's fp64 matmul
