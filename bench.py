@@ -4,7 +4,9 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload decode1]
 
 A step is one pass of the whole path over one batch already resident in
-HBM: moe_quant_act -> moe_permute -> moe_expert_ffn -> moe_combine.  The
+HBM: quantize -> permute -> expert FFN -> combine, as one moe_ffn_layer call
+(--unfused: the four calls moe_quant_act, moe_permute, moe_expert_ffn,
+moe_combine).  The
 default workload is DeepSeek-V3-shaped decode with one token (hidden 7168,
 expert intermediate 2048, 256 experts, top-8, FP8 e4m3 weights with
 128x128 fp32 block scales, synthetic data).  Decode steps rotate over
@@ -64,6 +66,9 @@ def parse():
     ap.add_argument("--also", default="decode4,decode1_w8a16,router",
                     help="comma list of extra workloads (summary only); NAME_w8a16 runs the W8A16 decode FFN, "
                          "router times the gate on the main workload's tokens")
+    ap.add_argument("--unfused", action="store_true",
+                    help="run the layer as four library calls (quantize, permute, expert FFN, combine) instead "
+                         "of one moe_ffn_layer call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -112,7 +117,7 @@ def algorithmic(w, ids):
     }
 
 
-def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache, w8a16=False):
+def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache, w8a16=False, fused=True):
     import numpy as np
     w = synth.WORKLOADS[name]
     if w.chunk_tokens:
@@ -126,7 +131,8 @@ def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache
         log(f"drawing and quantizing weight layer {len(layers_cache)} on the GPU")
         layers_cache.append(make_layer(moe, torch, synth, w, len(layers_cache)))
     layers = layers_cache[:layers_n]
-    buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, with_status=False, w8a16=w8a16)
+    buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, with_status=False, w8a16=w8a16,
+                              fused=fused and not w8a16)
     stream = torch.cuda.current_stream()
 
     def step(i):
@@ -361,7 +367,7 @@ def main():
     layers_n = args.layers or (4 if decode else 1)
     cache = []
     w, ids, wts, x, ms, kern_us = time_workload(moe, torch, synth, args.workload, args.steps, args.warmup,
-                                                layers_n, cache)
+                                                layers_n, cache, fused=not args.unfused)
     alg = algorithmic(w, ids)
     tok_s = w.tokens / (ms / 1000.0)
     if decode:
@@ -391,7 +397,7 @@ def main():
         base_name, w8a16 = (extra[:-len("_w8a16")], True) if extra.endswith("_w8a16") else (extra, False)
         try:
             we, ide, _, _, mse, kue = time_workload(moe, torch, synth, base_name, args.steps, args.warmup,
-                                                    layers_n, cache, w8a16=w8a16)
+                                                    layers_n, cache, w8a16=w8a16, fused=not args.unfused)
         except SystemExit as exc:
             also[extra] = {"skipped": str(exc)}
             continue
@@ -410,7 +416,8 @@ def main():
         "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
         "config": {"workload": args.workload, "hidden": w.hidden, "inter": w.inter, "n_experts": w.n_experts,
                    "topk": w.topk, "tokens": w.tokens, "routing": w.routing,
-                   "weight_layers_rotated": layers_n, "active_experts": alg["active_experts"]},
+                   "weight_layers_rotated": layers_n, "active_experts": alg["active_experts"],
+                   "entry": "four calls" if args.unfused else "moe_ffn_layer"},
         "layer": {"weight_GBps": round(layer_gbs, 1), "frac_hbm": round(layer_gbs / HBM_PEAK_GBS, 4),
                   "TFLOPs": round(layer_tflops, 2)},
         "roofline": roof,

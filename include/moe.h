@@ -231,6 +231,35 @@ moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const flo
                          hipStream_t stream);
 
 /*
+ * Whole resident layer in one call: moe_quant_act -> moe_permute ->
+ * moe_expert_ffn -> moe_combine on one stream, with the same arithmetic and
+ * bit-identical results (the FP8 routed-expert FFN of System Design, run
+ * from device memory), in fewer launches:
+ *   T <= 256: quantization and the slot sort run as one launch;
+ *   DECODE regime with T * k <= 32 and I <= 2048: the down projection and
+ *   the combine run as one launch (a workgroup computes 32 output columns
+ *   for every active expert and combines them per token in LDS).
+ * x_bf16: device [T, H] bf16 bits; topk_ids: device int32 [T, k];
+ * topk_w: device fp32 [T, k]; weight stacks as in moe_expert_ffn (packed);
+ * out_bf16: device [T, H] bf16 bits; dev_status: optional device int32
+ * word, routing errors OR-ed in as by moe_permute (their outputs are
+ * unspecified).  ws: moe_ffn_layer_workspace(dims, T, regime) bytes,
+ * 256-byte aligned, owned by the caller; it holds the intermediate tensors
+ * (qx, sx, expert offsets, sorted_src, dest_row, fp32 expert rows).  A
+ * workspace must not be shared by calls that may overlap.  Argument errors
+ * are returned before anything is enqueued (MOE_ERR_INVALID_ARG,
+ * MOE_ERR_UNSUPPORTED_SHAPE, MOE_ERR_WORKSPACE); T == 0 does nothing.
+ */
+size_t moe_ffn_layer_workspace(moe_dims_t dims, int32_t T, moe_regime_t regime);
+moe_status_t moe_ffn_layer(moe_dims_t dims, int32_t T, moe_regime_t regime, const uint16_t* x_bf16,
+                           const int32_t* topk_ids, const float* topk_w,
+                           const uint8_t* w_gate, const float* s_gate,
+                           const uint8_t* w_up, const float* s_up,
+                           const uint8_t* w_down, const float* s_down,
+                           uint16_t* out_bf16, int32_t* dev_status,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * Router (gate): the step before moe_permute.  The paper's Background on
  * Mixture-of-Experts names top-k and grouped top-k gating and SmallEP runs
  * the gate locally before sorting tokens; it fixes no formula, so the rule

@@ -157,6 +157,23 @@ def moe_combine(y_rows, dest_row, topk_w, out_bf16, stream=None):
                            _stream(stream)))
 
 
+def moe_ffn_layer_workspace(dims: MoeDims, T: int, regime: int = MOE_REGIME_AUTO) -> int:
+    return int(lib.moe_ffn_layer_workspace(dims, T, regime))
+
+
+def moe_ffn_layer(dims: MoeDims, T: int, regime: int, x_bf16, topk_ids, topk_w, w_gate, s_gate, w_up, s_up,
+                  w_down, s_down, out_bf16, dev_status, ws, stream=None):
+    """The whole resident layer in one library call (see include/moe.h)."""
+    for t, nb, n in ((x_bf16, 2, "x_bf16"), (topk_ids, 4, "topk_ids"), (topk_w, 4, "topk_w"),
+                     (w_gate, 1, "w_gate"), (s_gate, 4, "s_gate"), (w_up, 1, "w_up"), (s_up, 4, "s_up"),
+                     (w_down, 1, "w_down"), (s_down, 4, "s_down"), (out_bf16, 2, "out_bf16"),
+                     (dev_status, 4, "dev_status"), (ws, 1, "ws")):
+        _need(t, nb, n)
+    _check(lib.moe_ffn_layer(dims, T, regime, _ptr(x_bf16), _ptr(topk_ids), _ptr(topk_w), _ptr(w_gate),
+                             _ptr(s_gate), _ptr(w_up), _ptr(s_up), _ptr(w_down), _ptr(s_down), _ptr(out_bf16),
+                             _ptr(dev_status), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
 class StreamContext:
     """Owns the per-slot ON/OFF events of moe_ffn_streamed (created once, at setup)."""
 

@@ -65,6 +65,8 @@ _SIGS = {
     "moe_expert_ffn_workspace": (_S, [MoeDims, _I, _ST]),
     "moe_expert_ffn": (_ST, [MoeDims, _I, _ST, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "moe_combine": (_ST, [_P, _P, _P, _I, _I, _I, _P, _P]),
+    "moe_ffn_layer_workspace": (_S, [MoeDims, _I, _ST]),
+    "moe_ffn_layer": (_ST, [MoeDims, _I, _ST, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "moe_expert_ffn_w8a16_workspace": (_S, [MoeDims, _I]),
     "moe_expert_ffn_w8a16": (_ST, [MoeDims, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "moe_router_workspace": (_S, [_I, _I, _I]),

@@ -36,6 +36,20 @@ moe_status_t run_ffn_decode(const moe_dims_t& d, int32_t T, const uint8_t* qx, c
                             const float* s_down, float* y_rows, float* h, uint8_t* qh, float* sh,
                             hipStream_t stream);
 
+moe_status_t run_ffn_decode_gateup(const moe_dims_t& d, int32_t T, const uint8_t* qx, const float* sx,
+                                   const int32_t* offsets, const int32_t* sorted_src, const uint8_t* w_gate,
+                                   const float* s_gate, const uint8_t* w_up, const float* s_up, float* h,
+                                   hipStream_t stream);
+
+bool decode_down_combine_fits(const moe_dims_t& d, int32_t T);
+moe_status_t run_ffn_decode_down_combine(const moe_dims_t& d, int32_t T, const float* h, const int32_t* offsets,
+                                         const uint8_t* w_down, const float* s_down, const int32_t* dest_row,
+                                         const float* topk_w, uint16_t* out, hipStream_t stream);
+
+moe_status_t launch_layer_prologue(const uint16_t* x, int32_t T, int32_t H, const int32_t* topk_ids, int32_t k,
+                                   int32_t E, uint8_t* qx, float* sx, int32_t* offsets, int32_t* sorted_src,
+                                   int32_t* dest_row, int32_t* dev_status, hipStream_t stream);
+
 moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, const float* sx,
                              const int32_t* offsets, const int32_t* sorted_src, const uint8_t* w_gate,
                              const float* s_gate, const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
@@ -43,6 +57,8 @@ moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, 
                              hipStream_t stream);
 
 size_t prefill_tile_workspace(const moe_dims_t& d, int32_t T);
+moe_status_t prefill_shape_check(const moe_dims_t& d);
+moe_status_t decode_shape_check(const moe_dims_t& d);
 
 moe_status_t run_ffn_decode_w8a16(const moe_dims_t& d, int32_t T, const uint16_t* x, const int32_t* offsets,
                                   const int32_t* sorted_src, const uint8_t* w_gate, const float* s_gate,
@@ -159,4 +175,105 @@ extern "C" moe_status_t moe_expert_ffn_w8a16(moe_dims_t d, int32_t T, const uint
   if (!aligned(ws, 256)) return fail(MOE_ERR_INVALID_ARG, "moe_expert_ffn_w8a16: workspace must be 256-byte aligned");
   return run_ffn_decode_w8a16(d, T, x_bf16, expert_offsets, sorted_src, w_gate, s_gate, w_up, s_up, w_down, s_down,
                               y_rows, static_cast<uint16_t*>(ws), stream);
+}
+
+// ---------------------------------------------------------------- whole layer
+
+namespace {
+
+// moe_ffn_layer workspace: the intermediate tensors of the layer, each
+// 256-byte aligned, then the permutation and expert-FFN workspaces.
+struct LayerLayout {
+  size_t qx, sx, offsets, sorted_src, dest_row, y, perm, ffn, total;
+};
+
+LayerLayout layer_layout(const moe_dims_t& d, int32_t T, moe_regime_t rg) {
+  LayerLayout L{};
+  const size_t R = (size_t)T * d.topk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align256(bytes);
+    return at;
+  };
+  L.qx = take((size_t)T * d.hidden);
+  L.sx = take((size_t)T * (d.hidden / kBlock) * sizeof(float));
+  L.offsets = take((size_t)(d.n_experts + 1) * sizeof(int32_t));
+  L.sorted_src = take(R * sizeof(int32_t));
+  L.dest_row = take(R * sizeof(int32_t));
+  L.y = take(R * d.hidden * sizeof(float));
+  L.perm = take(moe_permute_workspace(T, d.topk, d.n_experts));
+  L.ffn = take(moe_expert_ffn_workspace(d, T, rg));
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+extern "C" size_t moe_ffn_layer_workspace(moe_dims_t d, int32_t T, moe_regime_t regime) {
+  if (check_dims(d, "moe_ffn_layer_workspace") != MOE_OK || T < 0) return 0;
+  return layer_layout(d, T, resolve(regime, T)).total;
+}
+
+extern "C" moe_status_t moe_ffn_layer(moe_dims_t d, int32_t T, moe_regime_t regime, const uint16_t* x_bf16,
+                                      const int32_t* topk_ids, const float* topk_w, const uint8_t* w_gate,
+                                      const float* s_gate, const uint8_t* w_up, const float* s_up,
+                                      const uint8_t* w_down, const float* s_down, uint16_t* out_bf16,
+                                      int32_t* dev_status, void* ws, size_t ws_bytes, hipStream_t stream) {
+  moe_status_t st = check_dims(d, "moe_ffn_layer");
+  if (st != MOE_OK) return st;
+  if (T < 0) return fail(MOE_ERR_INVALID_ARG, "moe_ffn_layer: T=%d", T);
+  if (regime != MOE_REGIME_AUTO && regime != MOE_REGIME_DECODE && regime != MOE_REGIME_PREFILL)
+    return fail(MOE_ERR_INVALID_ARG, "moe_ffn_layer: regime=%d", (int)regime);
+  const moe_regime_t rg = resolve(regime, T);
+  if (rg == MOE_REGIME_DECODE && T > MOE_DECODE_MAX_TOKENS)
+    return fail(MOE_ERR_INVALID_ARG, "moe_ffn_layer: decode regime needs T <= %d (T=%d)", MOE_DECODE_MAX_TOKENS, T);
+  if ((int64_t)T * d.topk > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_ffn_layer: T*k overflows");
+  if (T == 0) return MOE_OK;
+  if (!x_bf16 || !topk_ids || !topk_w || !w_gate || !s_gate || !w_up || !s_up || !w_down || !s_down || !out_bf16)
+    return fail(MOE_ERR_INVALID_ARG, "moe_ffn_layer: null pointer");
+  if (!aligned(x_bf16, 16) || !aligned(out_bf16, 16) || !aligned(w_gate, 16) || !aligned(w_up, 16) ||
+      !aligned(w_down, 16))
+    return fail(MOE_ERR_INVALID_ARG, "moe_ffn_layer: misaligned pointer (16 bytes needed)");
+  st = rg == MOE_REGIME_DECODE ? decode_shape_check(d) : prefill_shape_check(d);
+  if (st != MOE_OK) return st;
+  const LayerLayout L = layer_layout(d, T, rg);
+  if (!ws || ws_bytes < L.total)
+    return fail(MOE_ERR_WORKSPACE, "moe_ffn_layer: workspace %zu bytes < %zu", ws_bytes, L.total);
+  if (!aligned(ws, 256)) return fail(MOE_ERR_INVALID_ARG, "moe_ffn_layer: workspace must be 256-byte aligned");
+  uint8_t* b = static_cast<uint8_t*>(ws);
+  uint8_t* qx = b + L.qx;
+  float* sx = reinterpret_cast<float*>(b + L.sx);
+  int32_t* offsets = reinterpret_cast<int32_t*>(b + L.offsets);
+  int32_t* sorted_src = reinterpret_cast<int32_t*>(b + L.sorted_src);
+  int32_t* dest_row = reinterpret_cast<int32_t*>(b + L.dest_row);
+  float* y = reinterpret_cast<float*>(b + L.y);
+  const size_t R = (size_t)T * d.topk;
+
+  // Quantize and sort: one launch for a single chunk of tokens.
+  if (T <= 256) {
+    st = launch_layer_prologue(x_bf16, T, d.hidden, topk_ids, d.topk, d.n_experts, qx, sx, offsets, sorted_src,
+                               dest_row, dev_status, stream);
+  } else {
+    st = moe_quant_act(x_bf16, T, d.hidden, qx, sx, stream);
+    if (st == MOE_OK)
+      st = moe_permute(topk_ids, T, d.topk, d.n_experts, offsets, sorted_src, dest_row, dev_status, b + L.perm,
+                       moe_permute_workspace(T, d.topk, d.n_experts), stream);
+  }
+  if (st != MOE_OK) return st;
+
+  if (rg == MOE_REGIME_DECODE && decode_down_combine_fits(d, T)) {
+    // Gate/up, then the down projection and the combine in one launch (the
+    // fp32 expert rows stay in LDS).
+    uint8_t* qh = b + L.ffn;
+    float* sh = reinterpret_cast<float*>(qh + align256(R * d.inter));
+    float* h = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(sh) + align256(R * (d.inter / kBlock) * sizeof(float)));
+    st = run_ffn_decode_gateup(d, T, qx, sx, offsets, sorted_src, w_gate, s_gate, w_up, s_up, h, stream);
+    if (st != MOE_OK) return st;
+    return run_ffn_decode_down_combine(d, T, h, offsets, w_down, s_down, dest_row, topk_w, out_bf16, stream);
+  }
+  st = moe_expert_ffn(d, T, rg, qx, sx, offsets, sorted_src, w_gate, s_gate, w_up, s_up, w_down, s_down, y,
+                      b + L.ffn, moe_expert_ffn_workspace(d, T, rg), stream);
+  if (st != MOE_OK) return st;
+  return moe_combine(y, dest_row, topk_w, T, d.topk, d.hidden, out_bf16, stream);
 }

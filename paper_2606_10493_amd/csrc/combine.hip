@@ -2,8 +2,8 @@
 // router weights in fp32, in slot order from +0.0, then rounded once to bf16
 // (the paper's router-weighted F32 accumulation followed by conversion back
 // to the hidden type).  Products and sums are rounded separately (FMA
-// contraction is switched off in this kernel), which is the exact order of
-// the definition, so the result is bit-identical to it for given rows.
+// contraction is switched off in combine8), which is the exact order of the
+// definition, so the result is bit-identical to it for given rows.
 //
 // Memory bound: k * 4 bytes read + 2 bytes written per output element.
 // Thread = 8 consecutive outputs (two 16-byte loads per slot, one 16-byte
@@ -16,29 +16,10 @@ namespace {
 __global__ __launch_bounds__(128) void combine_kernel(const float* __restrict__ y, const int32_t* __restrict__ dest,
                                                       const float* __restrict__ w, int k, int H, int blocks_per_tok,
                                                       uint16_t* __restrict__ out) {
-  // The definition rounds the product and the sum separately: no FMA here.
-#pragma clang fp contract(off)
   const int64_t t = blockIdx.x / blocks_per_tok;
   const int n = ((int)(blockIdx.x - t * blocks_per_tok) * 128 + (int)threadIdx.x) * 8;
   if (n >= H) return;
-  float acc[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
-  for (int j = 0; j < k; ++j) {
-    const int64_t p = dest[t * k + j];
-    const float wj = w[t * k + j];
-    const float4 a = *reinterpret_cast<const float4*>(y + p * H + n);
-    const float4 b = *reinterpret_cast<const float4*>(y + p * H + n + 4);
-    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = acc[i] + wj * v[i];
-  }
-  uint4 o;
-  o.x = (uint32_t)f32_to_bf16_rne(acc[0]) | ((uint32_t)f32_to_bf16_rne(acc[1]) << 16);
-  o.y = (uint32_t)f32_to_bf16_rne(acc[2]) | ((uint32_t)f32_to_bf16_rne(acc[3]) << 16);
-  o.z = (uint32_t)f32_to_bf16_rne(acc[4]) | ((uint32_t)f32_to_bf16_rne(acc[5]) << 16);
-  o.w = (uint32_t)f32_to_bf16_rne(acc[6]) | ((uint32_t)f32_to_bf16_rne(acc[7]) << 16);
-  *reinterpret_cast<uint4*>(out + t * H + n) = o;
+  *reinterpret_cast<uint4*>(out + t * H + n) = combine8(y, dest, w, k, H, t, n);
 }
 
 }  // namespace

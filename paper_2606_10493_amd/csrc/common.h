@@ -108,6 +108,85 @@ __device__ __forceinline__ float silu_mul(float g, float u) {
   return (g * (1.0f / (1.0f + expf(-g)))) * u;
 }
 
+// Eight consecutive values of a row as fp32 (one 16-byte load of bf16, two of fp32).
+__device__ __forceinline__ void load8_f32(const uint16_t* p, float (&v)[8]) {
+  const uint4 raw = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = bf16_to_f32(w[i] & 0xffffu);
+    v[2 * i + 1] = bf16_to_f32(w[i] >> 16);
+  }
+}
+__device__ __forceinline__ void load8_f32(const float* p, float (&v)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+// Activation block quantization (one scale per row per 128 columns): group g
+// of a [rows, 128 * groups_per_row] matrix is held by 16 consecutive lanes
+// (lane sub of the group: columns 8 sub .. 8 sub + 7).  The block amax is
+// reduced over the 16 lanes, s = amax / 448, and the lane writes its 8
+// codes; lane 0 of the group writes s.
+template <typename InT>
+__device__ __forceinline__ void quant_row_group(const InT* __restrict__ x, int64_t g, int sub, int groups_per_row,
+                                                uint8_t* __restrict__ q, float* __restrict__ s) {
+  const int64_t row = g / groups_per_row;
+  const int64_t col = (g - row * groups_per_row) * kBlock + sub * 8;
+  const int64_t idx = row * (int64_t)groups_per_row * kBlock + col;
+  float v[8];
+  load8_f32(x + idx, v);
+  float amax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
+#pragma unroll
+  for (int m = 8; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
+  const float sc = amax / kE4M3Max;
+  uint32_t lo = 0, hi = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) lo |= quantize_e4m3(v[i], sc) << (8 * i);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) hi |= quantize_e4m3(v[4 + i], sc) << (8 * i);
+  *reinterpret_cast<uint2*>(q + idx) = make_uint2(lo, hi);
+  if (sub == 0) s[g] = sc;
+}
+
+// Router-weighted combine of 8 consecutive outputs of token t:
+// bf16(sum_j w[t, j] * row_of(dest[t*k + j])[i]) over j = 0 .. k-1 in slot
+// order from +0.0, every product and sum rounded separately (no FMA: the
+// definition's order), then one round to bf16.  row_of(p) points at the 8
+// values of expert row p.  Returns the 8 bf16 values.
+template <typename RowOf>
+__device__ __forceinline__ uint4 combine8_of(RowOf row_of, const int32_t* __restrict__ dest,
+                                             const float* __restrict__ w, int k, int64_t t) {
+#pragma clang fp contract(off)
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
+  for (int j = 0; j < k; ++j) {
+    const int64_t p = dest[t * k + j];
+    const float wj = w[t * k + j];
+    float v[8];
+    load8_f32(row_of(p), v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = acc[i] + wj * v[i];
+  }
+  uint4 o;
+  o.x = (uint32_t)f32_to_bf16_rne(acc[0]) | ((uint32_t)f32_to_bf16_rne(acc[1]) << 16);
+  o.y = (uint32_t)f32_to_bf16_rne(acc[2]) | ((uint32_t)f32_to_bf16_rne(acc[3]) << 16);
+  o.z = (uint32_t)f32_to_bf16_rne(acc[4]) | ((uint32_t)f32_to_bf16_rne(acc[5]) << 16);
+  o.w = (uint32_t)f32_to_bf16_rne(acc[6]) | ((uint32_t)f32_to_bf16_rne(acc[7]) << 16);
+  return o;
+}
+
+// The same for outputs n .. n+7 of fp32 expert rows y [rows, H] in memory.
+__device__ __forceinline__ uint4 combine8(const float* __restrict__ y, const int32_t* __restrict__ dest,
+                                          const float* __restrict__ w, int k, int H, int64_t t, int n) {
+  return combine8_of([&](int64_t p) { return y + p * H + n; }, dest, w, k, t);
+}
+
 // Exclusive prefix sum of v over the whole workgroup (blockDim.x a multiple
 // of 64, at most 1024): shuffle scan inside each wave, wave totals through
 // LDS (wave_tot holds blockDim.x/64 ints).  Returns the exclusive prefix and

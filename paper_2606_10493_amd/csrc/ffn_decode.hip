@@ -448,6 +448,35 @@ moe_status_t launch_decode(const DecodeArgs& a, int64_t max_items, hipStream_t s
 
 }  // namespace
 
+// Shapes the decode kernels take: a wave's weight scales sit one per lane,
+// so at most 64 K blocks per wave (gate/up waves may take K halves).
+moe_status_t decode_shape_check(const moe_dims_t& d) {
+  if (d.hidden / kBlock > 64 * 2 || d.inter / kBlock > 64 * kWaves)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "decode regime supports H <= %d and I <= %d", 64 * 2 * kBlock,
+                64 * kWaves * kBlock);
+  return MOE_OK;
+}
+
+// Decode-regime gate/up: h = SiLU(G) * U in fp32, one row per expert-sorted slot.
+moe_status_t run_ffn_decode_gateup(const moe_dims_t& d, int32_t T, const uint8_t* qx, const float* sx,
+                                   const int32_t* offsets, const int32_t* sorted_src, const uint8_t* w_gate,
+                                   const float* s_gate, const uint8_t* w_up, const float* s_up, float* h,
+                                   hipStream_t stream) {
+  const int64_t R = (int64_t)T * d.topk;
+  const int64_t max_active = R < d.n_experts ? R : d.n_experts;
+  moe_status_t st0 = decode_shape_check(d);
+  if (st0 != MOE_OK) return st0;
+  DecodeArgs g{};
+  g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = T;
+  g.offsets = offsets; g.E = d.n_experts;
+  g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
+  g.N = d.inter; g.K = d.hidden; g.out = h;
+  const int64_t gu_items = max_active * (d.inter / 16);
+  if (T <= 16) return launch_decode<1, 1, true, false, 3>(g, gu_items, stream);
+  if (T <= 32) return launch_decode<2, 1, true, false, 2>(g, gu_items, stream);
+  return launch_decode<4, 1, true, false, 2>(g, gu_items, stream);
+}
+
 // Decode-regime FFN: gate/up -> h (fp32) -> quantize h -> down.
 moe_status_t run_ffn_decode(const moe_dims_t& d, int32_t T, const uint8_t* qx, const float* sx,
                             const int32_t* offsets, const int32_t* sorted_src, const uint8_t* w_gate,
@@ -456,21 +485,7 @@ moe_status_t run_ffn_decode(const moe_dims_t& d, int32_t T, const uint8_t* qx, c
                             hipStream_t stream) {
   const int64_t R = (int64_t)T * d.topk;
   const int64_t max_active = R < d.n_experts ? R : d.n_experts;
-  // A wave's weight scales sit one per lane: at most 64 K blocks per wave.
-  // (gate/up waves may take K halves).
-  if (d.hidden / kBlock > 64 * 2 || d.inter / kBlock > 64 * kWaves)
-    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "decode regime supports H <= %d and I <= %d", 64 * 2 * kBlock,
-                64 * kWaves * kBlock);
-  DecodeArgs g{};
-  g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = T;
-  g.offsets = offsets; g.E = d.n_experts;
-  g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
-  g.N = d.inter; g.K = d.hidden; g.out = h;
-  moe_status_t st;
-  const int64_t gu_items = max_active * (d.inter / 16);
-  if (T <= 16) st = launch_decode<1, 1, true, false, 3>(g, gu_items, stream);
-  else if (T <= 32) st = launch_decode<2, 1, true, false, 2>(g, gu_items, stream);
-  else st = launch_decode<4, 1, true, false, 2>(g, gu_items, stream);
+  moe_status_t st = run_ffn_decode_gateup(d, T, qx, sx, offsets, sorted_src, w_gate, s_gate, w_up, s_up, h, stream);
   if (st != MOE_OK) return st;
 
   DecodeArgs dn{};
@@ -496,9 +511,8 @@ moe_status_t run_ffn_decode_w8a16(const moe_dims_t& d, int32_t T, const uint16_t
                                   const float* s_down, float* y_rows, uint16_t* h16, hipStream_t stream) {
   const int64_t R = (int64_t)T * d.topk;
   const int64_t max_active = R < d.n_experts ? R : d.n_experts;
-  if (d.hidden / kBlock > 64 * 2 || d.inter / kBlock > 64 * kWaves)
-    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "decode regime supports H <= %d and I <= %d", 64 * 2 * kBlock,
-                64 * kWaves * kBlock);
+  moe_status_t st0 = decode_shape_check(d);
+  if (st0 != MOE_OK) return st0;
   DecodeArgs g{};
   g.a16 = x; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = T;
   g.offsets = offsets; g.E = d.n_experts;

@@ -1,0 +1,265 @@
+// Decode down projection fused with the router-weighted combine, for small
+// batches (R = T * k expert rows in all, R <= kDcMaxRows, K = I <= kDcMaxK).
+//
+// One workgroup owns 16 NT output columns [n0, n0 + 16 NT) of the layer and
+// computes them for every active expert, so the expert rows of the whole
+// batch never leave the workgroup: it combines them per token in LDS and
+// writes only the bf16 layer output (the fp32 expert rows are not written).
+// No workgroup depends on another.
+//
+// Per expert the arithmetic is the decode down kernel's (Fine-grained CPU
+// Parallelism: down after SiLU(gate) * up; FP8 Block Scaling Format):
+//   * h rows quantized per row per 128 (as moe_quant_rows_f32) into LDS;
+//   * one FP8 MFMA 16x16x128 per 128-K block (A: the expert's token rows,
+//     B: 16 W_down rows), promoted as acc += d * (sh[row, b] * s_down[n/128, b]);
+//   * the K blocks split over four waves as kw, kw + 4, kw + 8, ... and the
+//     four partials summed in wave order;
+// and the combine is the definition's order (combine8_of).  The output is
+// therefore bit-identical to the decode down kernel followed by moe_combine.
+//
+// Waves: 16 = (expert slot s = wave / 4) x (K part kw = wave % 4); wave
+// (s, kw) takes experts s, s + 4, ... and streams their K blocks kw, kw + 4,
+// ... as one list of items through a window of W items in registers,
+// with no barrier inside the loop.  At the end of each expert it stores the
+// expert's rows of its partial sum in LDS by expert row; after one barrier
+// the four partials of each row are summed in wave order.
+#include "common.h"
+
+namespace moe {
+
+namespace {
+
+constexpr int kDcMaxRows = 32;                // R = T * k
+constexpr int kDcMaxTokens = 16;              // rows of one expert: one 16-row MFMA operand
+constexpr int kDcMaxK = 2048;                 // I
+constexpr int kDcThreads = 1024;
+
+struct DownCombineArgs {
+  const float* h;           // fp32 [R, K]: SiLU(G) * U rows in expert-sorted order
+  const int32_t* offsets;   // [E+1]
+  int E;
+  const uint8_t* w;         // W_down [E, N, K], packed tiles
+  const float* s;           // [E, N/128, K/128]
+  int N, K;
+  const int32_t* dest_row;  // [T * k]
+  const float* topk_w;      // [T * k]
+  int topk, tokens;
+  uint16_t* out;            // bf16 [T, N]
+};
+
+// NT: 16-column operands per workgroup; HQ: h row blocks per 16-lane group
+// (R * K / 128 <= 64 HQ), all loaded before the weight window; W: items in
+// the weight window.
+template <int NT, int HQ, int W>
+__global__ __launch_bounds__(kDcThreads) void ffn_decode_down_combine_kernel(DownCombineArgs p) {
+  constexpr int kCols = 16 * NT;
+  __shared__ __attribute__((aligned(16))) uint8_t qh[kDcMaxRows * kDcMaxK];
+  __shared__ float sh[kDcMaxRows * (kDcMaxK / kBlock)];
+  __shared__ float part[4 * kDcMaxRows * kCols];  // [K part][expert row][column]
+  __shared__ __attribute__((aligned(16))) float yl[kDcMaxRows * kCols];
+  __shared__ float wsc[kDcThreads / 64][64];  // per wave: the weight scale of item i
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int sub = wave >> 2, kw = wave & 3;
+  const int r = lane & 15, kq = lane >> 4;
+  const int nb = p.K / kBlock;
+  const int R = p.tokens * p.topk;
+  const int n0 = blockIdx.x * kCols;
+
+  // This thread's h values (row blocks g = tid/16, tid/16 + 64, ...) go out
+  // first; they are quantized once the weight loads are in flight.
+  constexpr int kHq = HQ;
+  float hv[kHq][8];
+#pragma unroll
+  for (int q = 0; q < kHq; ++q) {
+    const int g = (tid >> 4) + q * (kDcThreads / 16);
+    if (g < R * nb) {
+      const int row = g / nb, b = g - row * nb;
+      load8_f32(p.h + (int64_t)row * p.K + b * kBlock + (tid & 15) * 8, hv[q]);
+    }
+  }
+
+  // Active experts, found by every wave on its own with ballots over the
+  // offsets (no barrier): lane g takes expert a = sub + 4 g, the a-th
+  // expert with rows (expert order), with its first row and row count.
+  int v_e = 0, v_p0 = 0, v_m = 0, n_act = 0;
+  {
+    const int a = sub + 4 * lane;
+    for (int c0 = 0; c0 < p.E; c0 += 64) {
+      const int e = c0 + lane;
+      const int lo = e < p.E ? p.offsets[e] : 0;
+      const int hi = e < p.E ? p.offsets[e + 1] : 0;
+      const unsigned long long bal = __ballot(hi > lo);
+      const int cnt = __popcll(bal);
+      // the (a - n_act)-th set bit of bal, for the lanes whose expert is in this chunk
+      unsigned long long mk = bal;
+      int n = a - n_act, pos = 0;
+#pragma unroll
+      for (int w = 32; w >= 1; w >>= 1) {
+        const int c = __popcll(mk & ((1ull << w) - 1ull));
+        if (n >= c) {
+          n -= c;
+          mk >>= w;
+          pos += w;
+        }
+      }
+      const int lo_b = __shfl(lo, pos), hi_b = __shfl(hi, pos);
+      if (a >= n_act && a < n_act + cnt) {
+        v_e = c0 + pos;
+        v_p0 = lo_b;
+        v_m = hi_b - lo_b;
+      }
+      n_act += cnt;
+    }
+  }
+
+  // Items of this wave: (expert a = sub + 4 g, block j) for g < n_mine, j < nkw.
+  const int nkw = (nb - kw + 3) / 4;
+  const int n_mine = n_act > sub ? (n_act - sub + 3) / 4 : 0;
+  const int n_items = n_mine * nkw;
+  auto uni = [](int v, int l) { return __builtin_amdgcn_readlane(v, l); };
+  // Lane i: the weight scale of item i (loaded before the weight window).
+  {
+    const int g = lane / max(nkw, 1), j = lane - g * max(nkw, 1);
+    const int e_g = __shfl(v_e, min(g, 63));
+    const float wsv = lane < n_items ? p.s[((int64_t)e_g * (p.N / kBlock) + n0 / kBlock) * nb + kw + 4 * j] : 0.0f;
+    wsc[wave][lane] = wsv;
+  }
+  v8i wbuf[W][NT];
+  // Item it (clamped into the list; a wave without items loads expert 0's
+  // first block, which is never used).
+  auto load_item = [&](int it, v8i (&w)[NT]) {
+    const int g = it / max(nkw, 1), j = it - g * max(nkw, 1);
+    const int e = n_items > 0 ? uni(v_e, g) : 0;
+    const int bk = min(kw + 4 * j, nb - 1);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      w[nt] = load_v8i_packed(p.w + (((int64_t)e * p.N + n0 + 16 * nt) / 16 * nb + bk) * kTileBytes +
+                              packed_lane_offset(0, kq, r));
+  };
+  // The window is refilled with the same number of loads on every item
+  // (past the end: the last item again), so the wait before each item's
+  // MFMA is a fixed count that leaves the later items' loads in flight.
+#pragma unroll
+  for (int u = 0; u < W; ++u) load_item(min(u, max(n_items - 1, 0)), wbuf[u]);
+
+  // h quantized per 128 into LDS (16 lanes per row block).
+#pragma unroll
+  for (int q = 0; q < kHq; ++q) {
+    const int g = (tid >> 4) + q * (kDcThreads / 16);
+    if (g < R * nb) {  // whole 16-lane groups
+      const int row = g / nb, b = g - row * nb, q16 = tid & 15;
+      float amax = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(hv[q][i]));
+#pragma unroll
+      for (int m = 8; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
+      const float sc = amax / kE4M3Max;
+      uint32_t lo = 0, hi = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) lo |= quantize_e4m3(hv[q][i], sc) << (8 * i);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) hi |= quantize_e4m3(hv[q][4 + i], sc) << (8 * i);
+      *reinterpret_cast<uint2*>(qh + row * p.K + b * kBlock + q16 * 8) = make_uint2(lo, hi);
+      if (q16 == 0) sh[row * nb + b] = sc;
+    }
+  }
+  // Partials start at zero: a wave without K blocks (K < 512) adds +0.0, as
+  // the decode down kernel's does.
+  for (int i = tid; i < 4 * kDcMaxRows * kCols; i += kDcThreads) part[i] = 0.0f;
+  __syncthreads();
+
+  v4f acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = v4f{0.f, 0.f, 0.f, 0.f};
+  for (int it0 = 0; it0 < n_items; it0 += W) {
+#pragma unroll
+    for (int u = 0; u < W; ++u) {
+      const int it = it0 + u;
+      if (it < n_items) {
+        const int g = it / nkw, j = it - g * nkw;
+        const int p0 = uni(v_p0, g), m = uni(v_m, g);
+        const int bk = kw + 4 * j;
+        const float ws = wsc[wave][it];
+        // A rows beyond the expert's m rows read a valid row; their outputs are never kept.
+        const v8i afrag = load_v8i_ksplit(qh + (p0 + min(r, m - 1)) * p.K + bk * kBlock + kq * 16);
+        float sa[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = 4 * kq + i;
+          sa[i] = row < m ? sh[(p0 + row) * nb + bk] : 0.0f;
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const v4f d = mfma_f8_16x16x128(afrag, wbuf[u][nt]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[nt][i] += d[i] * (sa[i] * ws);
+        }
+        if (j == nkw - 1) {  // the expert's last block: keep its rows, restart
+          float* dst = part + kw * kDcMaxRows * kCols;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = 4 * kq + i;  // MFMA output: lane holds rows 4 kq + i, column r
+              if (row < m) dst[(p0 + row) * kCols + nt * 16 + r] = acc[nt][i];
+              acc[nt][i] = 0.0f;
+            }
+        }
+      }
+      load_item(min(it + W, n_items - 1), wbuf[u]);
+    }
+  }
+  __syncthreads();
+  // Rows of the active experts: the four K parts summed in wave order.
+  for (int i = tid; i < R * kCols; i += kDcThreads) {
+    float v = part[i];
+    v += part[kDcMaxRows * kCols + i];
+    v += part[2 * kDcMaxRows * kCols + i];
+    v += part[3 * kDcMaxRows * kCols + i];
+    yl[i] = v;
+  }
+  __syncthreads();
+
+  // Combine: 8 columns per thread.
+  constexpr int kPerTok = kCols / 8;
+  for (int idx = tid; idx < p.tokens * kPerTok; idx += kDcThreads) {
+    const int t = idx / kPerTok;
+    const int c = (idx - t * kPerTok) * 8;
+    *reinterpret_cast<uint4*>(p.out + (int64_t)t * p.N + n0 + c) =
+        combine8_of([&](int64_t row) { return yl + row * kCols + c; }, p.dest_row, p.topk_w, p.topk, t);
+  }
+}
+
+}  // namespace
+
+// True when the fused down + combine takes this batch.
+bool decode_down_combine_fits(const moe_dims_t& d, int32_t T) {
+  return T >= 1 && T <= kDcMaxTokens && (int64_t)T * d.topk <= kDcMaxRows && d.inter <= kDcMaxK &&
+         d.n_experts <= kDcThreads && d.hidden % 32 == 0;
+}
+
+// y = down(h) of every active expert combined per token into out (bf16 [T, H]).
+moe_status_t run_ffn_decode_down_combine(const moe_dims_t& d, int32_t T, const float* h, const int32_t* offsets,
+                                         const uint8_t* w_down, const float* s_down, const int32_t* dest_row,
+                                         const float* topk_w, uint16_t* out, hipStream_t stream) {
+  if (!decode_down_combine_fits(d, T))
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "decode down+combine: T=%d (max %d), T*k=%d (max %d), I=%d (max %d)", T,
+                kDcMaxTokens, T * d.topk, kDcMaxRows, d.inter, kDcMaxK);
+  DownCombineArgs a{};
+  a.h = h; a.offsets = offsets; a.E = d.n_experts;
+  a.w = w_down; a.s = s_down; a.N = d.hidden; a.K = d.inter;
+  a.dest_row = dest_row; a.topk_w = topk_w; a.topk = d.topk; a.tokens = T; a.out = out;
+  const int groups = T * d.topk * (d.inter / kBlock);  // h row blocks
+  const dim3 grid((unsigned)(d.hidden / 32)), block(kDcThreads);
+  if (groups <= 128)
+    MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<2, 2, 4>), grid, block, 0, stream, a);
+  else if (groups <= 256)
+    MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<2, 4, 3>), grid, block, 0, stream, a);
+  else
+    MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<2, 8, 1>), grid, block, 0, stream, a);
+  return check_launch("ffn_decode_down_combine");
+}
+
+}  // namespace moe

@@ -472,6 +472,18 @@ moe_status_t launch_prefill(const PrefillArgs& a, int64_t max_mtiles, hipStream_
 
 }  // namespace
 
+// Shapes the prefill kernels take (checked before anything is enqueued).
+moe_status_t prefill_shape_check(const moe_dims_t& d) {
+  if (d.hidden % kBN) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "prefill regime needs H %% 256 == 0 (H=%d)", d.hidden);
+  if ((int64_t)d.inter * d.hidden > 0x7fffffff)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: one expert matrix (%d x %d) exceeds 2 GiB", d.inter,
+                d.hidden);
+  const int kmax = d.hidden > d.inter ? d.hidden : d.inter;
+  const size_t lds = (size_t)kStages * kHalf + sizeof(float) * ((size_t)kSaStride + 2) * (kmax / kBlock);
+  if (lds > 150 * 1024) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: K=%d needs %zu bytes of LDS", kmax, lds);
+  return MOE_OK;
+}
+
 size_t prefill_tile_workspace(const moe_dims_t& d, int32_t T) {
   (void)T;
   return sizeof(int32_t) * (size_t)(d.n_experts + 1);
@@ -485,7 +497,8 @@ moe_status_t run_ffn_prefill_view(const moe_dims_t& d, int64_t max_mtiles, int32
                                   const uint8_t* w_gate, const float* s_gate, const uint8_t* w_up, const float* s_up,
                                   const uint8_t* w_down, const float* s_down, float* y_rows, uint8_t* qh, float* sh,
                                   int32_t* tiles, hipStream_t stream) {
-  if (d.hidden % kBN) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "prefill regime needs H %% 256 == 0 (H=%d)", d.hidden);
+  moe_status_t st0 = prefill_shape_check(d);
+  if (st0 != MOE_OK) return st0;
   MOE_LAUNCH("prefill_tiles", prefill_tiles_kernel, dim3(1), dim3(1024), 0, stream, offsets, d.n_experts, tiles);
   moe_status_t st = check_launch("prefill_tiles");
   if (st != MOE_OK) return st;

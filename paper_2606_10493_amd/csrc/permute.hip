@@ -14,7 +14,8 @@
 // valid rows (positions expert_offsets[E] .. T*k-1, in slot order), so the
 // outputs stay a bijection and every later index stays in bounds.
 //
-//   one chunk  (T <= 256): permute_small_kernel does count, scan and scatter.
+//   one chunk  (T <= 256): permute_small_kernel does count, scan and scatter
+//              (layer_prologue_kernel: the same, beside the activation quantization).
 //   several chunks: permute_count_kernel -> permute_scan_kernel -> permute_scatter_kernel.
 #include "common.h"
 
@@ -135,11 +136,9 @@ __device__ __forceinline__ void scatter_chunk(const unsigned long long* mask, co
 // One chunk (T <= 256): mask, scan and scatter in one workgroup.  Threads
 // take slots, not tokens, so that a few tokens with k slots each (decode)
 // spread over k * T threads instead of a serial loop in T threads.
-__global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
-                                                            int32_t* __restrict__ offsets,
-                                                            int32_t* __restrict__ sorted_src,
-                                                            int32_t* __restrict__ dest_row,
-                                                            int32_t* __restrict__ dev_status) {
+__device__ __forceinline__ void permute_one_chunk(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                  int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_src,
+                                                  int32_t* __restrict__ dest_row, int32_t* __restrict__ dev_status) {
   __shared__ unsigned long long mask[kMaxExperts * 4];
   __shared__ int start[kMaxExperts];
   __shared__ int16_t sid[kChunk * kMaxTopk];
@@ -203,6 +202,35 @@ __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __res
     }
   }
   report(dev_status, err);
+}
+
+__global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                            int32_t* __restrict__ offsets,
+                                                            int32_t* __restrict__ sorted_src,
+                                                            int32_t* __restrict__ dest_row,
+                                                            int32_t* __restrict__ dev_status) {
+  permute_one_chunk(ids, T, k, E, offsets, sorted_src, dest_row, dev_status);
+}
+
+// Layer prologue for one chunk of tokens (T <= 256), one launch instead of
+// two: workgroup 0 sorts the slots (as permute_small_kernel); workgroups 1..
+// quantize the bf16 activations, 16 groups of 128 columns each (as
+// moe_quant_act).
+__global__ __launch_bounds__(256) void layer_prologue_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                             int32_t* __restrict__ offsets,
+                                                             int32_t* __restrict__ sorted_src,
+                                                             int32_t* __restrict__ dest_row,
+                                                             int32_t* __restrict__ dev_status,
+                                                             const uint16_t* __restrict__ x, int64_t n_groups,
+                                                             int groups_per_row, uint8_t* __restrict__ qx,
+                                                             float* __restrict__ sx) {
+  if (blockIdx.x == 0) {
+    permute_one_chunk(ids, T, k, E, offsets, sorted_src, dest_row, dev_status);
+    return;
+  }
+  const int64_t g = (int64_t)(blockIdx.x - 1) * 16 + (threadIdx.x >> 4);
+  if (g >= n_groups) return;  // whole 16-lane groups leave together
+  quant_row_group<uint16_t>(x, g, threadIdx.x & 15, groups_per_row, qx, sx);
 }
 
 // counts: [n_chunks][E+1]; entry E is the chunk's number of invalid slots.
@@ -279,6 +307,20 @@ __global__ __launch_bounds__(256) void permute_scatter_kernel(const int32_t* __r
 int64_t n_chunks_of(int32_t T) { return ((int64_t)T + kChunk - 1) / kChunk; }
 
 }  // namespace
+
+// Quantize x [T, H] and sort the slots of T <= 256 tokens in one launch.
+// Arguments are checked by the caller.
+moe_status_t launch_layer_prologue(const uint16_t* x, int32_t T, int32_t H, const int32_t* topk_ids, int32_t k,
+                                   int32_t E, uint8_t* qx, float* sx, int32_t* offsets, int32_t* sorted_src,
+                                   int32_t* dest_row, int32_t* dev_status, hipStream_t stream) {
+  if (T > kChunk) return fail(MOE_ERR_INVALID_ARG, "layer prologue: T=%d > %d", T, kChunk);
+  const int gpr = H / kBlock;
+  const int64_t n_groups = (int64_t)T * gpr;
+  const int64_t blocks = 1 + (n_groups + 15) / 16;
+  MOE_LAUNCH("layer_prologue", layer_prologue_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, topk_ids, T, k, E,
+             offsets, sorted_src, dest_row, dev_status, x, n_groups, gpr, qx, sx);
+  return check_launch("layer prologue");
+}
 
 }  // namespace moe
 

@@ -14,32 +14,6 @@ namespace moe {
 
 namespace {
 
-template <typename InT>
-struct Loader8;
-
-template <>
-struct Loader8<uint16_t> {
-  static __device__ __forceinline__ void load(const uint16_t* p, float (&v)[8]) {
-    const uint4 raw = *reinterpret_cast<const uint4*>(p);
-    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[2 * i] = bf16_to_f32(w[i] & 0xffffu);
-      v[2 * i + 1] = bf16_to_f32(w[i] >> 16);
-    }
-  }
-};
-
-template <>
-struct Loader8<float> {
-  static __device__ __forceinline__ void load(const float* p, float (&v)[8]) {
-    const float4 a = *reinterpret_cast<const float4*>(p);
-    const float4 b = *reinterpret_cast<const float4*>(p + 4);
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-  }
-};
-
 __device__ __forceinline__ uint2 encode8(const float (&v)[8], float s) {
   uint32_t lo = 0, hi = 0;
 #pragma unroll
@@ -55,21 +29,8 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(const InT* __restrict__
                                                          int groups_per_row, uint8_t* __restrict__ q,
                                                          float* __restrict__ s) {
   const int64_t g = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
-  const int sub = threadIdx.x & 15;
   if (g >= n_groups) return;  // whole 16-lane groups leave together
-  const int64_t row = g / groups_per_row;
-  const int64_t col = (g - row * groups_per_row) * kBlock + sub * 8;
-  const int64_t idx = row * (int64_t)groups_per_row * kBlock + col;
-  float v[8];
-  Loader8<InT>::load(x + idx, v);
-  float amax = 0.0f;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
-#pragma unroll
-  for (int m = 8; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
-  const float sc = amax / kE4M3Max;
-  *reinterpret_cast<uint2*>(q + idx) = encode8(v, sc);
-  if (sub == 0) s[g] = sc;
+  quant_row_group<InT>(x, g, threadIdx.x & 15, groups_per_row, q, s);
 }
 
 // One 256-thread workgroup per 128x128 block.  Thread t covers columns
@@ -89,7 +50,7 @@ __global__ __launch_bounds__(256) void quant_weight_kernel(const float* __restri
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
     const int row = br * kBlock + (t >> 4) + 16 * r;
-    Loader8<float>::load(w + base + (int64_t)row * cols + c, v[r]);
+    load8_f32(w + base + (int64_t)row * cols + c, v[r]);
 #pragma unroll
     for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[r][i]));
   }
