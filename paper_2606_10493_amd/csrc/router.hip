@@ -10,15 +10,18 @@
 // experts are chosen, listed by decreasing key; equal values go to the lower
 // index.  Weights: s[id_j] / sum_j s[id_j] * scaling, summed in slot order.
 //
-// Two kernels:
-//   router_logits_kernel: 16 tokens x 256 experts per workgroup with the bf16
+// Kernels:
+//   router_logits_kernel (fewer than 256 tokens): 16 tokens x 256 experts per workgroup with the bf16
 //     MFMA 16x16x32 (A = token rows, B = router rows, both read straight
 //     from global memory as 16-byte pieces), over one of KS slices of K, so
 //     that a few tokens still spread over enough workgroups; fp32 partial
 //     logits [KS][T][E].
+//   router_logits_tiled_kernel (256 tokens or more): 128 x 256 tiles through
+//     LDS, also over K slices, the same partial layout.
 //   router_select_kernel: one wave per token sums the KS partials in slice
-//     order, applies the sigmoid and the bias, ranks groups and experts with
-//     wave shuffles and writes ids and weights.
+//     order, applies the sigmoid and the bias, keeps the best groups, finds
+//     the k-th largest key by a radix select over its bits and orders the k
+//     chosen experts; lanes 0 .. k-1 write ids and weights.
 #include "common.h"
 
 namespace moe {
@@ -27,8 +30,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kRouterMaxPerLane = 16;   // experts per lane in the selection (E <= 1024)
-constexpr int kRouterMaxGroups = 64;    // one group score per lane
+constexpr int kRouterMaxExperts = 1024; // one selection thread per expert
+constexpr int kRouterMaxGroups = 64;
 constexpr int kRouterMinChunk = 128;    // K elements per logits workgroup at least
 
 __global__ __launch_bounds__(256) void router_logits_kernel(const uint16_t* __restrict__ x, int T, int H,
@@ -70,144 +73,315 @@ __global__ __launch_bounds__(256) void router_logits_kernel(const uint16_t* __re
     }
 }
 
+// Many tokens: an LDS-tiled bf16 GEMM.  Workgroup = 128 tokens x 256
+// experts over one K slice, 512 threads; wave w computes tokens
+// 64 (w / 4) + [0, 64) against experts 64 (w % 4) + [0, 64) (16 MFMA
+// 16x16x32 per 32-K step).  The 32-K tiles of both operands go through two
+// LDS stages (each thread loads 16 bytes of x and 32 bytes of W_r per step);
+// a 64-byte LDS row holds one row's 32 K values, which a quarter wave reads
+// as 16 rows x 64 contiguous bytes.
+constexpr int kRtM = 128, kRtN = 256, kRtK = 32;
+
+__global__ __launch_bounds__(512) void router_logits_tiled_kernel(const uint16_t* __restrict__ x, int T, int H,
+                                                                  const uint16_t* __restrict__ w, int E, int kchunk,
+                                                                  float* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2][kRtM * kRtK];
+  __shared__ __attribute__((aligned(16))) uint16_t wsm[2][kRtN * kRtK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, kq = lane >> 4;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int t0 = blockIdx.x * kRtM, e0 = blockIdx.y * kRtN, ks = blockIdx.z;
+  const int64_t k0 = (int64_t)ks * kchunk;
+  // Loader: thread tid moves x row tid / 4 (16 bytes at K 8 (tid % 4)) and
+  // W_r rows tid / 4 and 128 + tid / 4; rows beyond T or E read a valid row.
+  const int lr = tid >> 2, lk = (tid & 3) * 8;
+  const uint16_t* xg = x + (int64_t)min(t0 + lr, T - 1) * H + k0 + lk;
+  const uint16_t* wg0 = w + (int64_t)min(e0 + lr, E - 1) * H + k0 + lk;
+  const uint16_t* wg1 = w + (int64_t)min(e0 + 128 + lr, E - 1) * H + k0 + lk;
+  v4f acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+  uint4 rx = *reinterpret_cast<const uint4*>(xg);
+  uint4 rw0 = *reinterpret_cast<const uint4*>(wg0);
+  uint4 rw1 = *reinterpret_cast<const uint4*>(wg1);
+  const int nsteps = kchunk / kRtK;
+  for (int st = 0; st < nsteps; ++st) {
+    const int b = st & 1;
+    *reinterpret_cast<uint4*>(&xs[b][lr * kRtK + lk]) = rx;
+    *reinterpret_cast<uint4*>(&wsm[b][lr * kRtK + lk]) = rw0;
+    *reinterpret_cast<uint4*>(&wsm[b][(128 + lr) * kRtK + lk]) = rw1;
+    __syncthreads();
+    if (st + 1 < nsteps) {  // the next step's loads fly during this step's MFMAs
+      const int64_t o = (int64_t)(st + 1) * kRtK;
+      rx = *reinterpret_cast<const uint4*>(xg + o);
+      rw0 = *reinterpret_cast<const uint4*>(wg0 + o);
+      rw1 = *reinterpret_cast<const uint4*>(wg1 + o);
+    }
+    bf16x8 a[4], bb[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&xs[b][(64 * wm + 16 * i + r) * kRtK + 8 * kq]));
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      bb[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&wsm[b][(64 * wn + 16 * j + r) * kRtK + 8 * kq]));
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bb[j], acc[i][j], 0, 0, 0);
+  }
+  // Lane l holds logits of tokens (64 wm + 16 i) + 4 kq + q for expert (64 wn + 16 j) + r.
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int t = t0 + 64 * wm + 16 * i + 4 * kq + q, e = e0 + 64 * wn + 16 * j + r;
+        if (t < T && e < E) part[((int64_t)ks * T + t) * E + e] = acc[i][j][q];
+      }
+}
+
 // (value, index) order of the selection: larger value first, then lower index.
 __device__ __forceinline__ bool beats(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
-// ids / wts rows have k_out = k (+1 with a shared expert) columns.  PER:
-// experts per lane (lane l holds experts l*PER .. l*PER + PER - 1).
-template <int PER>
+// Selection: one wave per token (four tokens per 256-thread workgroup),
+// lane l holding experts l, l + 64, ... (PER of them).  The KS partial
+// logits are summed in slice order, then:
+//   * group scores: for each group the two largest keys, by a wave
+//     reduction of (largest, second) pairs; lane g ranks group g against
+//     the others and the topk_group best are kept;
+//   * the k-th largest kept key (in the (value, index) order) by a radix
+//     select over the 32 bits of the keys mapped to ordered integers: each
+//     bit costs PER ballots, with no per-expert comparisons against all E;
+//   * the k chosen experts (keys above the k-th, and the lowest indices of
+//     those equal to it) are ordered among themselves through LDS.
+// ids / wts rows have k_out = k (+1 with a shared expert) columns.
+__device__ __forceinline__ uint32_t ordered_bits(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// WIDE (few tokens, many K slices): one token per workgroup; the four waves
+// each sum the slices q = w, w + 4, ... and wave 0 adds the four partial sums
+// (in wave order) before it selects, so the slices are read in one round
+// trip instead of several.
+template <int PER, bool WIDE>
 __global__ __launch_bounds__(256) void router_select_kernel(const float* __restrict__ part, int KS, int T, int E,
                                                             const float* __restrict__ bias, int k, int n_group,
                                                             int topk_group, float scaling, int shared,
                                                             int32_t* __restrict__ ids, float* __restrict__ wts) {
-  const int k_out = k + (shared >= 0 ? 1 : 0);
-  __shared__ float chosen[4][32];  // the chosen experts' scores of each wave's token
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;  // the whole wave
-  constexpr int per = PER;
+  __shared__ float sel_key[4][32], sel_s[4][32];
+  __shared__ int sel_e[4][32];
+  __shared__ float wide_sum[WIDE ? 3 : 1][WIDE ? 64 * PER : 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int slot = WIDE ? 0 : wave;
+  const int64_t t = WIDE ? (int64_t)blockIdx.x : (int64_t)blockIdx.x * 4 + wave;
+  if (t >= T) return;  // the whole wave (WIDE: the whole workgroup); no other barrier below
   const int epg = E / n_group;
-  // Logits: the KS slices summed in slice order; QB slices of all the lane's
-  // experts are loaded before any is added (a few tokens have many slices).
-  constexpr int QB = 128 / PER;
-  float lg[PER];
+  const int k_out = k + (shared >= 0 ? 1 : 0);
+
+  // Logits: the KS slices summed in slice order; each batch's loads go out
+  // together (slice index clamped, so every load is unconditional).
+  float s[PER], key[PER];
+  {
+    float lg[PER], bv[PER];
 #pragma unroll
-  for (int i = 0; i < PER; ++i) lg[i] = 0.0f;
-  for (int q0 = 0; q0 < KS; q0 += QB) {
-    float v[QB][PER];
+    for (int i = 0; i < PER; ++i) {
+      const int e = min(lane + 64 * i, E - 1);
+      bv[i] = bias ? bias[e] : 0.0f;
+      lg[i] = 0.0f;
+    }
+    constexpr int QB = (64 / PER) > 1 ? 64 / PER : 1;
+    const int q_first = WIDE ? wave : 0, q_step = WIDE ? 4 : 1;
+    for (int q0 = q_first; q0 < KS; q0 += QB * q_step) {
+      float v[QB][PER];
 #pragma unroll
-    for (int q = 0; q < QB; ++q)
+      for (int q = 0; q < QB; ++q)
+#pragma unroll
+        for (int i = 0; i < PER; ++i)
+          v[q][i] = part[((int64_t)min(q0 + q * q_step, KS - 1) * T + t) * E + min(lane + 64 * i, E - 1)];
+#pragma unroll
+      for (int q = 0; q < QB; ++q)
+#pragma unroll
+        for (int i = 0; i < PER; ++i)
+          if (q0 + q * q_step < KS) lg[i] += v[q][i];
+    }
+    if constexpr (WIDE) {
+      if (wave > 0) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) wide_sum[wave - 1][lane + 64 * i] = lg[i];
+      }
+      __syncthreads();
+      if (wave > 0) return;
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
-        const int e = lane * PER + i;
-        v[q][i] = (q0 + q < KS && e < E) ? part[((int64_t)(q0 + q) * T + t) * E + e] : 0.0f;
+        lg[i] += wide_sum[0][lane + 64 * i];
+        lg[i] += wide_sum[1][lane + 64 * i];
+        lg[i] += wide_sum[2][lane + 64 * i];
       }
+    }
 #pragma unroll
-    for (int q = 0; q < QB; ++q)
-#pragma unroll
-      for (int i = 0; i < PER; ++i)
-        if (q0 + q < KS) lg[i] += v[q][i];
-  }
-  float s[kRouterMaxPerLane], key[kRouterMaxPerLane];
-#pragma unroll
-  for (int i = 0; i < kRouterMaxPerLane; ++i) {
-    const int e = lane * per + i;
-    s[i] = 0.0f;
-    key[i] = -INFINITY;
-    if (i < per && e < E) {
+    for (int i = 0; i < PER; ++i) {
       s[i] = 1.0f / (1.0f + expf(-lg[i]));
-      key[i] = s[i] + (bias ? bias[e] : 0.0f);
+      key[i] = lane + 64 * i < E ? s[i] + bv[i] : -INFINITY;
     }
   }
-  // Group scores: the two largest keys of group g over the wave (values only,
-  // merged pairwise), kept by lane g.
-  float my_group = -INFINITY;
-  for (int g = 0; g < n_group; ++g) {
-    float b1 = -INFINITY, b2 = -INFINITY;
+
+  // Groups: score = sum of the two largest keys; lane g keeps group g's.
+  if (n_group > 1) {
+    float my_group = -INFINITY;
+    if (epg <= 64 && 64 % epg == 0) {
+      // Aligned groups (epg a power of two up to 64): register i holds groups
+      // i * 64 / epg + (lane / epg); all are reduced at once inside their
+      // epg-lane segments, then lane g fetches group g's score.
+      float b1[PER], b2[PER];
 #pragma unroll
-    for (int i = 0; i < kRouterMaxPerLane; ++i) {
-      const int e = lane * per + i;
-      if (i < per && e < E && e / epg == g) {
-        const float v = key[i];
-        if (v > b1) {
-          b2 = b1;
-          b1 = v;
-        } else if (v > b2) {
-          b2 = v;
+      for (int i = 0; i < PER; ++i) {
+        b1[i] = key[i];
+        b2[i] = -INFINITY;
+      }
+      for (int m = 1; m < epg; m <<= 1) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+          const float o1 = __shfl_xor(b1[i], m), o2 = __shfl_xor(b2[i], m);
+          const float n2 = fmaxf(fminf(b1[i], o1), fmaxf(b2[i], o2));
+          b1[i] = fmaxf(b1[i], o1);
+          b2[i] = n2;
         }
       }
-    }
+      const int gpr = 64 / epg;  // groups per register
 #pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      const float o1 = __shfl_xor(b1, m), o2 = __shfl_xor(b2, m);
-      const float n2 = fmaxf(fminf(b1, o1), fmaxf(b2, o2));
-      b1 = fmaxf(b1, o1);
-      b2 = n2;
-    }
-    const float score = n_group > 1 ? b1 + b2 : 0.0f;  // one group: all experts are kept anyway
-    if (lane == g) my_group = score;
-  }
-  int rank = 0;
-  for (int h = 0; h < n_group; ++h) {
-    const float gh = __shfl(my_group, h);
-    rank += beats(gh, h, my_group, lane) ? 1 : 0;
-  }
-  const int kept_group = (lane < n_group && rank < topk_group) ? 1 : 0;
+      for (int i = 0; i < PER; ++i) {
+        const float v = __shfl(b1[i] + b2[i], (lane % gpr) * epg);
+        if (lane / gpr == i) my_group = v;
+      }
+    } else {
+      for (int g = 0; g < n_group; ++g) {
+        float b1 = -INFINITY, b2 = -INFINITY;
 #pragma unroll
-  for (int i = 0; i < kRouterMaxPerLane; ++i) {
-    const int e = lane * per + i;
-    const int kept = __shfl(kept_group, (i < per && e < E) ? e / epg : 0);
-    if (!(i < per && e < E) || !kept) key[i] = -INFINITY;
-  }
-  // k rounds of a wave-wide arg-max over (key, index), carrying the score.
-  float total = 0.0f;
-  for (int j = 0; j < k; ++j) {
-    float bv = -INFINITY, bs = 0.0f;
-    int bi = 0x7fffffff;
+        for (int i = 0; i < PER; ++i) {
+          const int e = lane + 64 * i;
+          if (e < E && e / epg == g) {
+            const float v = key[i];
+            if (v > b1) {
+              b2 = b1;
+              b1 = v;
+            } else if (v > b2) {
+              b2 = v;
+            }
+          }
+        }
 #pragma unroll
-    for (int i = 0; i < kRouterMaxPerLane; ++i) {
-      const int e = lane * per + i;
-      if (i < per && e < E && beats(key[i], e, bv, bi)) {
-        bv = key[i];
-        bi = e;
-        bs = s[i];
+        for (int m = 32; m >= 1; m >>= 1) {
+          const float o1 = __shfl_xor(b1, m), o2 = __shfl_xor(b2, m);
+          const float n2 = fmaxf(fminf(b1, o1), fmaxf(b2, o2));
+          b1 = fmaxf(b1, o1);
+          b2 = n2;
+        }
+        if (lane == g) my_group = b1 + b2;
       }
     }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      const float ov = __shfl_xor(bv, m), os = __shfl_xor(bs, m);
-      const int oi = __shfl_xor(bi, m);
-      if (beats(ov, oi, bv, bi)) {
-        bv = ov;
-        bi = oi;
-        bs = os;
-      }
+    int rank = 0;
+    for (int h = 0; h < n_group; ++h) {
+      const float gh = __shfl(my_group, h);
+      rank += beats(gh, h, my_group, lane) ? 1 : 0;
     }
+    const int kept_group = (lane < n_group && rank < topk_group) ? 1 : 0;
 #pragma unroll
-    for (int i = 0; i < kRouterMaxPerLane; ++i)
-      if (lane * per + i == bi) key[i] = -INFINITY;
-    total += bs;
-    if (lane == 0) {
-      ids[(int64_t)t * k_out + j] = bi;
-      chosen[threadIdx.x >> 6][j] = bs;
+    for (int i = 0; i < PER; ++i) {
+      const int e = lane + 64 * i;
+      const int kept = __shfl(kept_group, e < E ? e / epg : 0);
+      if (!kept) key[i] = -INFINITY;
     }
   }
-  if (lane == 0) {
-    for (int j = 0; j < k; ++j) wts[(int64_t)t * k_out + j] = (chosen[threadIdx.x >> 6][j] / total) * scaling;
-    if (shared >= 0) {
-      ids[(int64_t)t * k_out + k] = shared;
-      wts[(int64_t)t * k_out + k] = 1.0f;
+
+  // Radix select of the k-th largest key: prefix of the ordered bits, and
+  // `need` = how many of the keys equal to it are chosen (lowest index first).
+  uint32_t u[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) u[i] = ordered_bits(key[i]);
+  uint32_t prefix = 0, mask = 0;
+  int need = k;
+  for (int b = 31; b >= 0; --b) {
+    const uint32_t bit = 1u << b;
+    int c1 = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) c1 += __popcll(__ballot((u[i] & mask) == prefix && (u[i] & bit)));
+    if (c1 >= need) prefix |= bit;
+    else need -= c1;
+    mask |= bit;
+  }
+  // Chosen: u > prefix, or u == prefix and among the first `need` such keys
+  // in expert order (e = lane + 64 i: register i, then lane).
+  const unsigned long long below = (1ull << lane) - 1ull;
+  int eq_before = 0, n_sel = 0;
+  bool chosen[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const unsigned long long eq = __ballot(u[i] == prefix);
+    const int my_eq = eq_before + __popcll(eq & below);
+    chosen[i] = u[i] > prefix || (u[i] == prefix && my_eq < need);
+    eq_before += __popcll(eq);
+  }
+  // Compact the k chosen (expert order) into LDS, then each takes its rank.
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const unsigned long long cb = __ballot(chosen[i]);
+    if (chosen[i]) {
+      const int at = n_sel + __popcll(cb & below);
+      sel_key[slot][at] = key[i];
+      sel_s[slot][at] = s[i];
+      sel_e[slot][at] = lane + 64 * i;
     }
+    n_sel += __popcll(cb);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  float cs = 0.0f;
+  int ce = 0, crank = 0;
+  if (lane < k) {
+    const float kv = sel_key[slot][lane];
+    ce = sel_e[slot][lane];
+    cs = sel_s[slot][lane];
+    for (int j = 0; j < k; ++j) crank += beats(sel_key[slot][j], sel_e[slot][j], kv, ce) ? 1 : 0;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if (lane < k) {
+    ids[t * k_out + crank] = ce;
+    sel_s[slot][crank] = cs;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if (lane < k) {
+    float total = 0.0f;
+    for (int j = 0; j < k; ++j) total += sel_s[slot][j];
+    wts[t * k_out + lane] = (sel_s[slot][lane] / total) * scaling;
+  }
+  if (shared >= 0 && lane == 0) {
+    ids[t * k_out + k] = shared;
+    wts[t * k_out + k] = 1.0f;
   }
 }
 
-// K slices of the logits: enough workgroups for a few tokens, each slice at
-// least kRouterMinChunk elements and a divisor of H / 32 slices of 32.
+// From this many tokens on the logits use the tiled kernel.
+constexpr int kRouterTiledMinTokens = 256;
+
+// K slices of the logits: enough workgroups to cover the chip (256 or
+// more), each slice a divisor of H / 32 slices of 32 and at least
+// kRouterMinChunk elements.
 int router_slices(int32_t T, int32_t H, int32_t E) {
-  const int64_t tiles = ((int64_t)T + 15) / 16 * (((int64_t)E + 255) / 256);
-  const int64_t want = tiles >= 256 ? 1 : 256 / tiles;
+  const bool tiled = T >= kRouterTiledMinTokens;
+  const int64_t tiles = tiled ? ((int64_t)T + kRtM - 1) / kRtM * (((int64_t)E + kRtN - 1) / kRtN)
+                              : ((int64_t)T + 15) / 16 * (((int64_t)E + 255) / 256);
+  const int64_t want = tiles >= 256 ? 1 : (256 + tiles - 1) / tiles;
   const int n32 = H / 32;
   int best = 1;
   for (int ks = 1; ks <= n32; ++ks)
@@ -230,9 +404,9 @@ extern "C" moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H,
                                    const float* bias, int32_t E, int32_t k, moe_router_cfg_t cfg,
                                    int32_t* topk_ids, float* topk_w, void* ws, size_t ws_bytes,
                                    hipStream_t stream) {
-  if (T < 0 || H <= 0 || H % 32 || E < 1 || E > 64 * kRouterMaxPerLane)
+  if (T < 0 || H <= 0 || H % 32 || E < 1 || E > kRouterMaxExperts)
     return fail(MOE_ERR_INVALID_ARG, "moe_router: T=%d H=%d E=%d (need H %% 32 == 0, 1 <= E <= %d)", T, H, E,
-                64 * kRouterMaxPerLane);
+                kRouterMaxExperts);
   if (cfg.n_group < 1 || cfg.n_group > kRouterMaxGroups || E % cfg.n_group || (cfg.n_group > 1 && E / cfg.n_group < 2) ||
       cfg.topk_group < 1 || cfg.topk_group > cfg.n_group || k < 1 || k > 32 ||
       k > cfg.topk_group * (E / cfg.n_group))
@@ -249,16 +423,30 @@ extern "C" moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H,
   if (!aligned(ws, 4)) return fail(MOE_ERR_INVALID_ARG, "moe_router: misaligned workspace");
   const int ks = router_slices(T, H, E);
   float* part = static_cast<float*>(ws);
-  const dim3 grid((unsigned)((T + 15) / 16), (unsigned)((E + 255) / 256), (unsigned)ks);
-  MOE_LAUNCH("router_logits", router_logits_kernel, grid, dim3(256), 0, stream, x_bf16, T, H, w_router_bf16, E, H / ks,
-             part);
+  if (T >= kRouterTiledMinTokens) {
+    const dim3 grid((unsigned)((T + kRtM - 1) / kRtM), (unsigned)((E + kRtN - 1) / kRtN), (unsigned)ks);
+    MOE_LAUNCH("router_logits", router_logits_tiled_kernel, grid, dim3(512), 0, stream, x_bf16, T, H, w_router_bf16,
+               E, H / ks, part);
+  } else {
+    const dim3 grid((unsigned)((T + 15) / 16), (unsigned)((E + 255) / 256), (unsigned)ks);
+    MOE_LAUNCH("router_logits", router_logits_kernel, grid, dim3(256), 0, stream, x_bf16, T, H, w_router_bf16, E,
+               H / ks, part);
+  }
   moe_status_t st = check_launch("moe_router");
   if (st != MOE_OK) return st;
+  // Few tokens with many K slices: one token per workgroup (WIDE).
+  const bool wide = ks >= 8 && T <= 64;
+  const dim3 sgrid((unsigned)(wide ? T : (T + 3) / 4)), sblock(256);
+#define MOE_ROUTER_SELECT(P)                                                                                       \
+  do {                                                                                                             \
+    if (wide)                                                                                                      \
+      MOE_LAUNCH("router_select", (router_select_kernel<P, true>), sgrid, sblock, 0, stream, part, ks, T, E, bias, \
+                 k, cfg.n_group, cfg.topk_group, cfg.routed_scaling, cfg.shared_expert, topk_ids, topk_w);         \
+    else                                                                                                           \
+      MOE_LAUNCH("router_select", (router_select_kernel<P, false>), sgrid, sblock, 0, stream, part, ks, T, E,      \
+                 bias, k, cfg.n_group, cfg.topk_group, cfg.routed_scaling, cfg.shared_expert, topk_ids, topk_w);   \
+  } while (0)
   const int per = (E + 63) / 64;
-  const dim3 sgrid((unsigned)((T + 3) / 4));
-#define MOE_ROUTER_SELECT(P)                                                                                  \
-  MOE_LAUNCH("router_select", router_select_kernel<P>, sgrid, dim3(256), 0, stream, part, ks, T, E, bias, k,  \
-             cfg.n_group, cfg.topk_group, cfg.routed_scaling, cfg.shared_expert, topk_ids, topk_w)
   if (per <= 1) MOE_ROUTER_SELECT(1);
   else if (per <= 2) MOE_ROUTER_SELECT(2);
   else if (per <= 4) MOE_ROUTER_SELECT(4);

@@ -106,6 +106,33 @@ def test_router_many_experts_wide_topk(moe):
     _check("E=1024 k=32", x, wr, bias, 32, 64, 16, 1.0, moe)
 
 
+@pytest.mark.parametrize("tokens", [255, 256, 300])
+def test_router_ragged_expert_tile_tiled_logits(moe, tokens):
+    """E = 320 (one full and one ragged 256-expert tile), tokens around the
+    switch to the LDS-tiled logits kernel and a ragged 128-token tail."""
+    w = synth.Workload("router_ragged", 1024, 256, 320, 6, tokens, "uniform")
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.02)
+    _check(f"E=320 T={tokens}", x, wr, bias, 6, 1, 1, 1.0, moe)
+
+
+def test_router_many_experts_many_tokens(moe):
+    w = synth.Workload("router_wide_tiled", 1024, 256, 1024, 32, 260, "uniform")
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.02)
+    _check("E=1024 k=32 T=260", x, wr, bias, 32, 64, 16, 1.0, moe)
+
+
+@pytest.mark.parametrize("experts,n_group,topk_group,k", [(256, 2, 1, 8), (384, 8, 3, 6)])
+def test_router_groups_not_aligned_to_lanes(moe, experts, n_group, topk_group, k):
+    """Groups of 128 and of 48 experts (not a power of two up to 64): the
+    group scores take the general per-group reduction."""
+    w = synth.Workload("router_groups", 1024, 256, experts, k, 70, "uniform")
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.02)
+    _check(f"E={experts} groups={n_group}", x, wr, bias, k, n_group, topk_group, 1.0, moe)
+
+
 def test_router_zero_tokens_and_bad_config(moe):
     w = synth.WORKLOADS["tiny"]
     wr, _ = synth.router_params(w)
