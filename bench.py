@@ -38,10 +38,10 @@ METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
 # profiles/*_hbm_traffic.md.  Valid only while the kernel's source file is the
 # one measured (sha256 prefix).
 TRAFFIC = {
-    ("decode1", "ffn_decode_gateup"): {"bytes": 235601715, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
-                                       "sha256_prefix": "39c437a5dfceacb3"},
-    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9573711565, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
-                                          "sha256_prefix": "79d78fd7c93d1996"},
+    ("decode1", "ffn_decode_gateup"): {"bytes": 235600896, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
+                                       "sha256_prefix": "63155ff48297212f"},
+    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9601313075, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
+                                          "sha256_prefix": "cbe0dfe0cfd1897f"},
 }
 
 
