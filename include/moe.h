@@ -236,7 +236,7 @@ moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const flo
  * bit-identical results (the FP8 routed-expert FFN of System Design, run
  * from device memory), in fewer launches:
  *   T <= 256: quantization and the slot sort run as one launch;
- *   DECODE regime with T * k <= 32 and I <= 2048: the down projection and
+ *   DECODE regime with T * k <= 16 and I <= 2048: the down projection and
  *   the combine run as one launch (a workgroup computes 32 output columns
  *   for every active expert and combines them per token in LDS).
  * x_bf16: device [T, H] bf16 bits; topk_ids: device int32 [T, k];

@@ -29,7 +29,7 @@ namespace moe {
 
 namespace {
 
-constexpr int kDcMaxRows = 32;                // R = T * k
+constexpr int kDcMaxRows = 16;                // R = T * k (beyond, 224 workgroups stream too few bytes per CU)
 constexpr int kDcMaxTokens = 16;              // rows of one expert: one 16-row MFMA operand
 constexpr int kDcMaxK = 2048;                 // I
 constexpr int kDcThreads = 1024;
@@ -48,8 +48,8 @@ struct DownCombineArgs {
 };
 
 // NT: 16-column operands per workgroup; HQ: h row blocks per 16-lane group
-// (R * K / 128 <= 64 HQ), all loaded before the weight window; W: items in
-// the weight window.
+// loaded before the weight window (the rest, if R * K / 128 > 64 HQ, are
+// loaded after it); W: items in the weight window.
 template <int NT, int HQ, int W>
 __global__ __launch_bounds__(kDcThreads) void ffn_decode_down_combine_kernel(DownCombineArgs p) {
   constexpr int kCols = 16 * NT;
@@ -67,8 +67,8 @@ __global__ __launch_bounds__(kDcThreads) void ffn_decode_down_combine_kernel(Dow
   const int R = p.tokens * p.topk;
   const int n0 = blockIdx.x * kCols;
 
-  // This thread's h values (row blocks g = tid/16, tid/16 + 64, ...) go out
-  // first; they are quantized once the weight loads are in flight.
+  // This thread's first HQ h row blocks (g = tid/16, tid/16 + 64, ...) go
+  // out first; they are quantized once the weight loads are in flight.
   constexpr int kHq = HQ;
   float hv[kHq][8];
 #pragma unroll
@@ -145,25 +145,31 @@ __global__ __launch_bounds__(kDcThreads) void ffn_decode_down_combine_kernel(Dow
   for (int u = 0; u < W; ++u) load_item(min(u, max(n_items - 1, 0)), wbuf[u]);
 
   // h quantized per 128 into LDS (16 lanes per row block).
+  auto quant_block = [&](int g, const float (&v)[8]) {
+    const int row = g / nb, b = g - row * nb, q16 = tid & 15;
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
+#pragma unroll
+    for (int m = 8; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
+    const float sc = amax / kE4M3Max;
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lo |= quantize_e4m3(v[i], sc) << (8 * i);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) hi |= quantize_e4m3(v[4 + i], sc) << (8 * i);
+    *reinterpret_cast<uint2*>(qh + row * p.K + b * kBlock + q16 * 8) = make_uint2(lo, hi);
+    if (q16 == 0) sh[row * nb + b] = sc;
+  };
 #pragma unroll
   for (int q = 0; q < kHq; ++q) {
     const int g = (tid >> 4) + q * (kDcThreads / 16);
-    if (g < R * nb) {  // whole 16-lane groups
-      const int row = g / nb, b = g - row * nb, q16 = tid & 15;
-      float amax = 0.0f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(hv[q][i]));
-#pragma unroll
-      for (int m = 8; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
-      const float sc = amax / kE4M3Max;
-      uint32_t lo = 0, hi = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) lo |= quantize_e4m3(hv[q][i], sc) << (8 * i);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) hi |= quantize_e4m3(hv[q][4 + i], sc) << (8 * i);
-      *reinterpret_cast<uint2*>(qh + row * p.K + b * kBlock + q16 * 8) = make_uint2(lo, hi);
-      if (q16 == 0) sh[row * nb + b] = sc;
-    }
+    if (g < R * nb) quant_block(g, hv[q]);  // whole 16-lane groups
+  }
+  for (int g = (tid >> 4) + kHq * (kDcThreads / 16); g < R * nb; g += kDcThreads / 16) {
+    float v[8];
+    load8_f32(p.h + (int64_t)(g / nb) * p.K + (g - (g / nb) * nb) * kBlock + (tid & 15) * 8, v);
+    quant_block(g, v);
   }
   // Partials start at zero: a wave without K blocks (K < 512) adds +0.0, as
   // the decode down kernel's does.
@@ -251,14 +257,10 @@ moe_status_t run_ffn_decode_down_combine(const moe_dims_t& d, int32_t T, const f
   a.h = h; a.offsets = offsets; a.E = d.n_experts;
   a.w = w_down; a.s = s_down; a.N = d.hidden; a.K = d.inter;
   a.dest_row = dest_row; a.topk_w = topk_w; a.topk = d.topk; a.tokens = T; a.out = out;
-  const int groups = T * d.topk * (d.inter / kBlock);  // h row blocks
-  const dim3 grid((unsigned)(d.hidden / 32)), block(kDcThreads);
-  if (groups <= 128)
-    MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<2, 2, 4>), grid, block, 0, stream, a);
-  else if (groups <= 256)
-    MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<2, 4, 3>), grid, block, 0, stream, a);
-  else
-    MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<2, 8, 1>), grid, block, 0, stream, a);
+  // Two h row blocks per lane group ahead of the weight window (they fit in
+  // registers beside it); any others are loaded after it.
+  MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<2, 2, 4>), dim3((unsigned)(d.hidden / 32)),
+             dim3(kDcThreads), 0, stream, a);
   return check_launch("ffn_decode_down_combine");
 }
 

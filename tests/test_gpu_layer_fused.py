@@ -2,7 +2,7 @@
 
 moe_ffn_layer runs the arithmetic of moe_quant_act -> moe_permute ->
 moe_expert_ffn -> moe_combine in fewer launches (quantization and the slot
-sort in one launch for T <= 256; in the decode regime with T * k <= 32 the
+sort in one launch for T <= 256; in the decode regime with T * k <= 16 the
 down projection and the combine in one launch, each workgroup combining its
 output columns of every active expert in LDS).  Bar: its output equals the four-call path's bit for bit,
 and the oracle's within 2e-2 (max|out - ref| / max|ref|).
@@ -44,7 +44,8 @@ CASES = [
     (256, 128, 8, 2, 1, "uniform", "decode"),
     (1024, 512, 16, 4, 4, "uniform", "decode"),     # h quantized in the down kernel
     (1024, 512, 16, 4, 5, "zipf", "decode"),        # separate h quantization
-    (768, 384, 32, 8, 4, "zipf", "decode"),         # T * k = 32, three K blocks over four waves
+    (768, 384, 32, 8, 2, "zipf", "decode"),         # T * k = 16, three K blocks over four waves
+    (768, 384, 32, 8, 4, "zipf", "decode"),         # T * k = 32: separate down and combine
     (768, 384, 32, 8, 17, "uniform", "decode"),     # two token operands, separate down and combine
     (768, 384, 32, 8, 33, "zipf", "decode"),        # four token operands
     (768, 384, 32, 8, 64, "zipf", "decode"),        # decode limit
