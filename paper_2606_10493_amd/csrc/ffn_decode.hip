@@ -69,7 +69,6 @@ struct DecodeArgs {
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int64_t kGridCap = 2048;  // workgroups per launch (more items loop)
 constexpr int kQhRows = 4;    // QH: rows of h quantized in the down kernel's prologue
 constexpr int kQhMaxK = 2048; // QH: 16 lane groups x 128 columns
 
@@ -439,7 +438,7 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
 
 template <int MT, int NT, bool GATEUP, bool QH, int U, bool A16 = false>
 moe_status_t launch_decode(const DecodeArgs& a, int64_t max_items, hipStream_t stream) {
-  const int64_t grid = max_items < kGridCap ? max_items : kGridCap;
+  const int64_t grid = max_items < 2048 ? max_items : 2048;
   if (grid <= 0) return MOE_OK;
   const char* name = A16 ? (GATEUP ? "ffn_decode_w8a16_gateup" : "ffn_decode_w8a16_down")
                          : (GATEUP ? "ffn_decode_gateup" : "ffn_decode_down");
