@@ -158,7 +158,9 @@ def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache
     kern = {}
     for kname, kms in prof:
         kern.setdefault(kname, []).append(kms)
-    kern_us = {kname: 1000.0 * sum(v) / len(v) for kname, v in kern.items()}
+    # Per step: a kernel launched more than once per step (decode launches per
+    # expert row-count class) is summed over the step's launches.
+    kern_us = {kname: 1000.0 * sum(v) / steps for kname, v in kern.items()}
     out = buf.out.cpu().numpy()
     if not np.all(np.isfinite((out.view(np.uint16).astype(np.uint32) << 16).view(np.float32))):
         raise RuntimeError("non-finite output")

@@ -64,6 +64,7 @@ struct DecodeArgs {
   float* out;                 // fp32 [rows, N]
   uint16_t* out16;            // A16 GATEUP: bf16 h [rows, N] (out unused)
   const float* hf;            // QH: fp32 h rows [rows, K] quantized in the prologue
+  int m_lo, m_hi;             // the launch covers the experts with m_lo <= rows <= m_hi
 };
 
 namespace {
@@ -72,15 +73,16 @@ constexpr int kWaves = 4;
 constexpr int kQhRows = 4;    // QH: rows of h quantized in the down kernel's prologue
 constexpr int kQhMaxK = 2048; // QH: 16 lane groups x 128 columns
 
-// The a-th non-empty expert (or -1), the number of non-empty experts and the
-// expert's row range, found by one wave with ballots.  The offsets of 256
+// The a-th expert whose row count lies in [m_lo, m_hi] (or -1), the number
+// of such experts and the expert's row range, found by one wave with ballots.  The offsets of 256
 // experts are loaded in one round trip (4 per lane + the end value), so the
 // lookup costs one L2 latency before the weight stream can start.
 struct ExpertRef {
   int e, n_active, p0, m;
 };
 
-__device__ __forceinline__ ExpertRef find_expert(const int32_t* __restrict__ offsets, int E, int64_t a) {
+__device__ __forceinline__ ExpertRef find_expert(const int32_t* __restrict__ offsets, int E, int64_t a, int m_lo,
+                                                 int m_hi) {
   const int lane = threadIdx.x & 63;
   ExpertRef ref{-1, 0, 0, 0};
   for (int c0 = 0; c0 < E; c0 += 256) {
@@ -97,7 +99,7 @@ __device__ __forceinline__ ExpertRef find_expert(const int32_t* __restrict__ off
       const int nxt_first = c < 3 ? __shfl(o[c + 1], 0) : o[4];
       const int up = __shfl_down(o[c], 1);
       const int nxt = lane < 63 ? up : nxt_first;
-      const bool on = x < E && nxt > o[c];
+      const bool on = x < E && nxt - o[c] >= m_lo && nxt - o[c] <= m_hi;
       const unsigned long long bal = __ballot(on);
       const int cnt = __popcll(bal);
       if (ref.e < 0 && a < ref.n_active + cnt) {
@@ -157,11 +159,11 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   const uint8_t* wfirst_mat = up_wave ? p.w1 : p.w0;
   const float* sfirst_mat = up_wave ? p.s1 : p.s0;
 
-  ExpertRef ref = find_expert(p.offsets, p.E, blockIdx.x / tiles);
+  ExpertRef ref = find_expert(p.offsets, p.E, blockIdx.x / tiles, p.m_lo, p.m_hi);
   const int64_t items = (int64_t)ref.n_active * tiles;
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
-    if (item != blockIdx.x) ref = find_expert(p.offsets, p.E, item / tiles);
+    if (item != blockIdx.x) ref = find_expert(p.offsets, p.E, item / tiles, p.m_lo, p.m_hi);
     const int e = ref.e;
     const int n0 = (int)(item % tiles) * 16 * NT;
     const int p0 = ref.p0;
@@ -446,6 +448,31 @@ moe_status_t launch_decode(const DecodeArgs& a, int64_t max_items, hipStream_t s
   return check_launch(name);
 }
 
+// One operation (gate/up or down) over the active experts, one launch per
+// row-count class: experts with up to 16 rows take the one-operand kernel
+// (every expert when T <= 16), 17-32 rows two operands, more rows four, so
+// that the many experts with few rows of a mixed batch run at the register
+// budget (and occupancy) of the one-operand kernel.  Each launch covers
+// only its experts; an expert has at most T rows.
+template <int NT, bool GATEUP, bool QH, int U1, int U24, bool A16 = false>
+moe_status_t launch_by_rows(DecodeArgs a, int32_t T, int64_t R, int tiles_per_expert, hipStream_t stream) {
+  auto items = [&](int lo) {  // experts with at least lo rows, at most E
+    const int64_t n = R / lo;
+    return (n < a.E ? n : (int64_t)a.E) * tiles_per_expert;
+  };
+  a.m_lo = 1;
+  a.m_hi = 16;
+  moe_status_t st = launch_decode<1, NT, GATEUP, QH, U1, A16>(a, items(1), stream);
+  if (st != MOE_OK || T <= 16) return st;
+  a.m_lo = 17;
+  a.m_hi = 32;
+  st = launch_decode<2, NT, GATEUP, false, U24, A16>(a, items(17), stream);
+  if (st != MOE_OK || T <= 32) return st;
+  a.m_lo = 33;
+  a.m_hi = 0x7fffffff;
+  return launch_decode<4, NT, GATEUP, false, U24, A16>(a, items(33), stream);
+}
+
 }  // namespace
 
 // Shapes the decode kernels take: a wave's weight scales sit one per lane,
@@ -463,7 +490,6 @@ moe_status_t run_ffn_decode_gateup(const moe_dims_t& d, int32_t T, const uint8_t
                                    const float* s_gate, const uint8_t* w_up, const float* s_up, float* h,
                                    hipStream_t stream) {
   const int64_t R = (int64_t)T * d.topk;
-  const int64_t max_active = R < d.n_experts ? R : d.n_experts;
   moe_status_t st0 = decode_shape_check(d);
   if (st0 != MOE_OK) return st0;
   DecodeArgs g{};
@@ -471,10 +497,7 @@ moe_status_t run_ffn_decode_gateup(const moe_dims_t& d, int32_t T, const uint8_t
   g.offsets = offsets; g.E = d.n_experts;
   g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
   g.N = d.inter; g.K = d.hidden; g.out = h;
-  const int64_t gu_items = max_active * (d.inter / 16);
-  if (T <= 16) return launch_decode<1, 1, true, false, 3>(g, gu_items, stream);
-  if (T <= 32) return launch_decode<2, 1, true, false, 2>(g, gu_items, stream);
-  return launch_decode<4, 1, true, false, 2>(g, gu_items, stream);
+  return launch_by_rows<1, true, false, 3, 2>(g, T, R, d.inter / 16, stream);
 }
 
 // Decode-regime FFN: gate/up -> h (fp32) -> quantize h -> down.
@@ -496,12 +519,14 @@ moe_status_t run_ffn_decode(const moe_dims_t& d, int32_t T, const uint8_t* qx, c
   const int64_t dn_items = max_active * (d.hidden / 32);
   // Up to kQhRows tokens (so at most kQhRows rows per expert) the down kernel
   // quantizes h itself; above that a separate launch writes qh, sh first.
-  if (T <= kQhRows && d.inter <= kQhMaxK) return launch_decode<1, 2, false, true, 4>(dn, dn_items, stream);
+  if (T <= kQhRows && d.inter <= kQhMaxK) {
+    dn.m_lo = 1;
+    dn.m_hi = 0x7fffffff;
+    return launch_decode<1, 2, false, true, 4>(dn, dn_items, stream);
+  }
   st = moe_quant_rows_f32(h, (int32_t)R, d.inter, qh, sh, stream);
   if (st != MOE_OK) return st;
-  if (T <= 16) return launch_decode<1, 2, false, false, 4>(dn, dn_items, stream);
-  if (T <= 32) return launch_decode<2, 2, false, false, 2>(dn, dn_items, stream);
-  return launch_decode<4, 2, false, false, 2>(dn, dn_items, stream);
+  return launch_by_rows<2, false, false, 4, 2>(dn, T, R, d.hidden / 32, stream);
 }
 
 // W8A16 decode FFN: bf16 activations, gate/up -> h (bf16) -> down.
@@ -510,7 +535,6 @@ moe_status_t run_ffn_decode_w8a16(const moe_dims_t& d, int32_t T, const uint16_t
                                   const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
                                   const float* s_down, float* y_rows, uint16_t* h16, hipStream_t stream) {
   const int64_t R = (int64_t)T * d.topk;
-  const int64_t max_active = R < d.n_experts ? R : d.n_experts;
   moe_status_t st0 = decode_shape_check(d);
   if (st0 != MOE_OK) return st0;
   DecodeArgs g{};
@@ -518,21 +542,14 @@ moe_status_t run_ffn_decode_w8a16(const moe_dims_t& d, int32_t T, const uint16_t
   g.offsets = offsets; g.E = d.n_experts;
   g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
   g.N = d.inter; g.K = d.hidden; g.out16 = h16;
-  const int64_t gu_items = max_active * (d.inter / 16);
-  moe_status_t st;
-  if (T <= 16) st = launch_decode<1, 1, true, false, 3, true>(g, gu_items, stream);
-  else if (T <= 32) st = launch_decode<2, 1, true, false, 2, true>(g, gu_items, stream);
-  else st = launch_decode<4, 1, true, false, 2, true>(g, gu_items, stream);
+  moe_status_t st = launch_by_rows<1, true, false, 3, 2, true>(g, T, R, d.inter / 16, stream);
   if (st != MOE_OK) return st;
   DecodeArgs dn{};
   dn.a16 = h16; dn.sorted_src = nullptr; dn.topk = d.topk; dn.a_rows = (int)R;
   dn.offsets = offsets; dn.E = d.n_experts;
   dn.w0 = w_down; dn.s0 = s_down;
   dn.N = d.hidden; dn.K = d.inter; dn.out = y_rows;
-  const int64_t dn_items = max_active * (d.hidden / 32);
-  if (T <= 16) return launch_decode<1, 2, false, false, 4, true>(dn, dn_items, stream);
-  if (T <= 32) return launch_decode<2, 2, false, false, 2, true>(dn, dn_items, stream);
-  return launch_decode<4, 2, false, false, 2, true>(dn, dn_items, stream);
+  return launch_by_rows<2, false, false, 4, 2, true>(dn, T, R, d.hidden / 32, stream);
 }
 
 }  // namespace moe
