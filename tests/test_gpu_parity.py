@@ -294,6 +294,41 @@ def test_prefill_tail_tiles_of_every_operand_count(moe):
         assert rel_err(y[o0:o1], inter["y"][o0:o1]) <= TOL, e
 
 
+@pytest.mark.parametrize("w8a16", [False, True])
+def test_decode_row_count_classes(moe, w8a16):
+    """Decode launches one kernel per expert row-count class (1-16, 17-32,
+    33+ rows).  Experts with exactly 1, 16, 17, 32, 33 and 64 rows (and one
+    empty expert) must each be computed once, by the right class."""
+    counts = [64, 33, 32, 17, 16, 1, 0, 29]  # 192 slots = 64 tokens x 3
+    k, t = 3, 64
+    w = synth.Workload("classes", 512, 256, len(counts), k, t, "uniform", 0.0, "sigmoid", seed=7)
+    x = synth.activations(w)
+    _, wts = synth.routing(w)
+    slots = np.repeat(np.arange(len(counts), dtype=np.int32), counts)
+    ids = np.ascontiguousarray(slots.reshape(k, t).T)  # slot t + j*T -> token t, choice j
+    assert all(len(set(r)) == k for r in ids.tolist())
+    wg, wu, wd = synth.weights_host(w)
+    ow = oracle.prepare_weights(wg, wu, wd)
+    dweights = quantize_weights_gpu(moe, wg, wu, wd)
+    buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, moe.MOE_REGIME_DECODE, w8a16=w8a16)
+    moe.run_layer(buf, bf16_dev(x), to_dev(ids), to_dev(wts), dweights)
+    torch.cuda.synchronize()
+    assert int(buf.dev_status.item()) == 0
+    if w8a16:
+        ref, inter = oracle.moe_layer_w8a16(x, ids, wts, ow), None
+    else:
+        ref, inter = oracle.moe_layer(x, ids, wts, ow, want_intermediates=True)
+        assert np.diff(inter["offsets"]).tolist() == counts
+        y = buf.y_rows.cpu().numpy().astype(np.float64)
+        for e in range(len(counts)):  # every expert's rows on their own
+            o0, o1 = inter["offsets"][e], inter["offsets"][e + 1]
+            if o1 > o0:
+                assert rel_err(y[o0:o1], inter["y"][o0:o1]) <= TOL, e
+    err = rel_err(bits_to_f32(buf.out), oracle.bf16_to_f32(ref))
+    log(f"  row classes (w8a16={w8a16}): out rel err {err:.3e}")
+    assert err <= TOL
+
+
 @pytest.mark.parametrize("case", SMALL_CASES[:3], ids=lambda c: "x".join(map(str, c[:5])))
 def test_decode_and_prefill_kernels_agree(moe, case):
     w, x, ids, wts, (wg, wu, wd) = _small_layer(case, seed=3)
