@@ -143,3 +143,33 @@ def test_fused_layer_deepseek_decode_equals_four_calls(moe, deepseek_layer, name
     b = _run(moe, w, x, ids, wts, deepseek_layer, moe.MOE_REGIME_AUTO, fused=False)
     assert int(a.dev_status.item()) == 0
     assert np.array_equal(a.out.cpu().numpy(), b.out.cpu().numpy())
+
+
+@pytest.mark.parametrize("h,i,e,k,t,regime", [
+    (256, 128, 1, 1, 3, "decode"),        # a single expert
+    (256, 128, 1, 1, 300, "prefill"),
+    (256, 128, 1024, 32, 2, "decode"),    # E = 1024, k = 32: the widest sort
+    (256, 128, 1024, 32, 40, "prefill"),
+    (384, 128, 8, 2, 9, "decode"),        # H a multiple of 128 but not of 256 (decode only)
+], ids=lambda v: str(v))
+def test_fused_layer_edge_shapes(moe, h, i, e, k, t, regime):
+    rg = moe.MOE_REGIME_DECODE if regime == "decode" else moe.MOE_REGIME_PREFILL
+    w, x, ids, wts = _layer_inputs(h, i, e, k, t, "uniform", seed=11)
+    wg, wu, wd = synth.weights_host(w)
+    dweights = quantize_weights_gpu(moe, wg, wu, wd)
+    a = _run(moe, w, x, ids, wts, dweights, rg, fused=True)
+    b = _run(moe, w, x, ids, wts, dweights, rg, fused=False)
+    assert int(a.dev_status.item()) == 0
+    assert np.array_equal(a.out.cpu().numpy(), b.out.cpu().numpy())
+    ref = oracle.moe_layer(x, ids, wts, oracle.prepare_weights(wg, wu, wd))
+    assert rel_err(bits_to_f32(a.out), oracle.bf16_to_f32(ref)) <= TOL
+
+
+def test_fused_layer_prefill_rejects_h_not_multiple_of_256(moe):
+    w, x, ids, wts = _layer_inputs(384, 128, 8, 2, 9, "uniform")
+    wg, wu, wd = synth.weights_host(w)
+    dweights = quantize_weights_gpu(moe, wg, wu, wd)
+    buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, moe.MOE_REGIME_PREFILL, fused=True)
+    with pytest.raises(moe.MoEError):
+        moe.run_layer(buf, bf16_dev(x), to_dev(ids), to_dev(wts), dweights)
+    torch.cuda.synchronize()
