@@ -204,12 +204,68 @@ __device__ __forceinline__ void permute_one_chunk(const int32_t* __restrict__ id
   report(dev_status, err);
 }
 
+// At most kTinySlots slots (decode batches): the same results as
+// permute_one_chunk with two barriers.  Slot f's stable position among the
+// valid slots is the number of valid slots g with (id[g], g) < (id[f], f);
+// an invalid slot goes after all valid ones, in slot order; offsets[e] is
+// the number of valid slots with id < e.  Every count runs over at most 64
+// slots staged in LDS.
+constexpr int kTinySlots = 64;
+
+__device__ __forceinline__ void permute_tiny(const int32_t* __restrict__ ids, int T, int k, int E,
+                                             int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_src,
+                                             int32_t* __restrict__ dest_row, int32_t* __restrict__ dev_status) {
+  __shared__ int sid[kTinySlots];
+  __shared__ int valid[kTinySlots];
+  const int n = T * k, tid = threadIdx.x;
+  if (tid < n) {
+    const int32_t id = ids[tid];
+    sid[tid] = (id >= 0 && id < E) ? id : -1;
+  }
+  __syncthreads();
+  uint32_t err = 0;
+  if (tid < n) {
+    const int t = tid / k, j = tid - t * k;
+    const int me = sid[tid];
+    if (me < 0) {
+      err = MOE_DEV_BAD_EXPERT_ID;
+    } else {
+      for (int i = 0; i < j; ++i)
+        if (sid[t * k + i] == me) err = MOE_DEV_DUP_EXPERT_ID;
+    }
+    valid[tid] = err == 0;
+  }
+  __syncthreads();
+  int n_valid = 0;
+  for (int g = 0; g < n; ++g) n_valid += valid[g];
+  if (tid < n) {
+    const int me = sid[tid];
+    int pos = 0;
+    if (valid[tid]) {
+      for (int g = 0; g < n; ++g) pos += (valid[g] && (sid[g] < me || (sid[g] == me && g < tid))) ? 1 : 0;
+    } else {
+      pos = n_valid;
+      for (int g = 0; g < tid; ++g) pos += valid[g] ? 0 : 1;
+    }
+    dest_row[tid] = pos;
+    sorted_src[pos] = tid;
+  }
+  for (int e = tid; e < E; e += blockDim.x) {
+    int c = 0;
+    for (int g = 0; g < n; ++g) c += (valid[g] && sid[g] < e) ? 1 : 0;
+    offsets[e] = c;
+  }
+  if (tid == 0) offsets[E] = n_valid;
+  report(dev_status, err);
+}
+
 __global__ __launch_bounds__(256) void permute_small_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
                                                             int32_t* __restrict__ offsets,
                                                             int32_t* __restrict__ sorted_src,
                                                             int32_t* __restrict__ dest_row,
                                                             int32_t* __restrict__ dev_status) {
-  permute_one_chunk(ids, T, k, E, offsets, sorted_src, dest_row, dev_status);
+  if (T * k <= kTinySlots) permute_tiny(ids, T, k, E, offsets, sorted_src, dest_row, dev_status);
+  else permute_one_chunk(ids, T, k, E, offsets, sorted_src, dest_row, dev_status);
 }
 
 // Layer prologue for one chunk of tokens (T <= 256), one launch instead of
@@ -225,7 +281,8 @@ __global__ __launch_bounds__(256) void layer_prologue_kernel(const int32_t* __re
                                                              int groups_per_row, uint8_t* __restrict__ qx,
                                                              float* __restrict__ sx) {
   if (blockIdx.x == 0) {
-    permute_one_chunk(ids, T, k, E, offsets, sorted_src, dest_row, dev_status);
+    if (T * k <= kTinySlots) permute_tiny(ids, T, k, E, offsets, sorted_src, dest_row, dev_status);
+    else permute_one_chunk(ids, T, k, E, offsets, sorted_src, dest_row, dev_status);
     return;
   }
   const int64_t g = (int64_t)(blockIdx.x - 1) * 16 + (threadIdx.x >> 4);

@@ -171,7 +171,19 @@ def test_permute_wide_topk_and_many_experts(moe):
     assert st == 0 and np.array_equal(off, r_off) and np.array_equal(src, r_src) and np.array_equal(dst, r_dst)
 
 
-@pytest.mark.parametrize("t", [5, 700])
+@pytest.mark.parametrize("t,k,e", [(8, 8, 256), (64, 1, 16), (65, 1, 16), (2, 32, 1024), (3, 32, 1024)],
+                         ids=lambda v: str(v))
+def test_permute_small_batch_boundaries(moe, t, k, e):
+    """Around 64 slots, where the one-workgroup sort switches between its
+    pairwise-count form (up to 64 slots) and its token-mask form."""
+    rng = np.random.default_rng(t * 100 + k)
+    ids = np.stack([rng.choice(e, k, replace=False) for _ in range(t)]).astype(np.int32)
+    off, src, dst, st = _run_permute(moe, ids, e)
+    r_off, r_src, r_dst = oracle.permute(ids, e)
+    assert st == 0 and np.array_equal(off, r_off) and np.array_equal(src, r_src) and np.array_equal(dst, r_dst)
+
+
+@pytest.mark.parametrize("t", [5, 21, 22, 80, 700])
 def test_permute_reports_bad_ids_and_stays_a_bijection(moe, t):
     rng = np.random.default_rng(5)
     ids = np.stack([rng.choice(8, 3, replace=False) for _ in range(t)]).astype(np.int32)
@@ -188,6 +200,10 @@ def test_permute_reports_bad_ids_and_stays_a_bijection(moe, t):
     valid[1 * 3 + 2] = False
     valid[3 * 3 + 1] = False
     assert np.all(src[off[-1]:] == np.flatnonzero(~valid))
+    flat = ids.reshape(-1)
+    good = np.flatnonzero(valid)
+    assert np.array_equal(src[:off[-1]], good[np.argsort(flat[good], kind="stable")])
+    assert np.array_equal(off[:-1], np.searchsorted(np.sort(flat[good]), np.arange(8)))
 
 
 # --------------------------------------------------------------- combine
