@@ -40,8 +40,8 @@ METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
 TRAFFIC = {
     ("decode1", "ffn_decode_gateup"): {"bytes": 235600691, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
                                        "sha256_prefix": "ac6a38abd53a3d3b"},
-    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9601313075, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
-                                          "sha256_prefix": "cbe0dfe0cfd1897f"},
+    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 10126903910, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
+                                          "sha256_prefix": "b4d463edabdef11f"},
 }
 
 

@@ -145,7 +145,11 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   for (int x = tid; x < p.E; x += kThreads) {
     const int s0 = p.mtile_start[x], s1 = p.mtile_start[x + 1];
     const int o0 = p.offsets[x], o1 = p.offsets[x + 1];
-    if (s0 <= eblk && eblk < s1) {
+    // o0 <= o1 holds for consistent offsets.  Testing it (with non-short-
+    // circuit ANDs) makes all four loads precede the branch: one round trip
+    // instead of the offsets being fetched only inside it.
+    const bool owner = (s0 <= eblk) & (eblk < s1) & (o0 <= o1);
+    if (owner) {
       const int64_t local = item - (int64_t)s0 * p.n_tiles;
       const int mcount = s1 - s0;
       const int ntx = (int)(local / mcount);
@@ -179,41 +183,27 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   float* sa_lds = reinterpret_cast<float*>(smem + kStages * kHalf);  // [nb][kSaStride]
   float* sw_lds = sa_lds + nb * kSaStride;                       // [2][nb]
 
-  for (int i = tid; i < kBM; i += kThreads) {
+  // The set-up before the first MFMA is three round trips: (1) the owner
+  // lookup above; (2) the tile's A row indices (threads 0-127) and the weight
+  // scales (the other threads) in parallel; (3) the first two weight blocks,
+  // the first two K blocks of expert rows and the row scales together (at
+  // the start of k_loop).  Each load loop is written so that a thread issues
+  // all its loads before it waits for any.
+  if (tid < kBM) {
     int row = -1;
-    if (i < mc) {
-      const int src = p.sorted_src ? p.sorted_src[m0 + i] / p.topk : m0 + i;
+    if (tid < mc) {
+      const int src = p.sorted_src ? p.sorted_src[m0 + tid] / p.topk : m0 + tid;
       row = (src >= 0 && src < p.a_rows) ? src : -1;
     }
-    arow[i] = row;
-  }
-  // Weight scales of the tile's two 128-row blocks: GATEUP gate and up block
-  // nt; DOWN blocks 2nt and 2nt + 1 (waves 0-3 and 4-7).
-  for (int i = tid; i < 2 * nb; i += kThreads) {
-    const int h = i / nb, b = i - h * nb;
-    const int64_t wrow = (int64_t)e * (p.N / kBlock) + (GATEUP ? nt : 2 * nt + h);
-    sw_lds[i] = ((GATEUP && h) ? p.s1 : p.s0)[wrow * nb + b];
-  }
-  __syncthreads();
-  for (int i = tid; i < kBM * nb; i += kThreads) {
-    const int m = i / nb, b = i - m * nb;
-    sa_lds[b * kSaStride + m] = arow[m] >= 0 ? p.sa[(int64_t)arow[m] * nb + b] : 0.0f;
-  }
-
-  // Expert rows: 1024 16-byte chunks per K block, 2 per thread; chunk c
-  // covers row c/8, bytes 16*(c%8).  Rows beyond the expert (or with a bad
-  // index) load row 0 instead: their codes are finite and their scale in
-  // sa_lds is 0, so their products promote to exactly 0, and only rows
-  // below mc are written.
-  const uint8_t* a_src[2];
-  int a_dst[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int c = tid + i * kThreads;
-    const int row = c >> 3, col = (c & 7) * 16;
-    const int ar = arow[row];
-    a_src[i] = p.a + (int64_t)(ar >= 0 ? ar : 0) * p.K + col;
-    a_dst[i] = swz(row, c & 7);
+    arow[tid] = row;
+  } else {
+    // Weight scales of the tile's two 128-row blocks: GATEUP gate and up
+    // block nt; DOWN blocks 2nt and 2nt + 1 (waves 0-3 and 4-7).
+    for (int i = tid - kBM; i < 2 * nb; i += kThreads - kBM) {
+      const int h = i / nb, b = i - h * nb;
+      const int64_t wrow = (int64_t)e * (p.N / kBlock) + (GATEUP ? nt : 2 * nt + h);
+      sw_lds[i] = ((GATEUP && h) ? p.s1 : p.s0)[wrow * nb + b];
+    }
   }
 
   // This wave's 32-row weight operand: rows 0-15 and 16-31 are two packed
@@ -227,6 +217,100 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     const uint8_t* wm = (GATEUP && r32 >= 16) ? p.w1 : p.w0;
     wsrc = wm + ebase + grp * nb * kTileBytes + packed_lane_offset(0, 2 * g2, r32 & 15);
   }
+  v8i wr[kRing][2];  // [slot][K half]
+#define MOE_PF_WLOAD(SLOT, BLK)                                                            \
+  do {                                                                                     \
+    const uint8_t* w_ = wsrc + (int64_t)(BLK) * kTileBytes;                                \
+    wr[SLOT][0] = join_v8i(*reinterpret_cast<const uint4*>(w_),                            \
+                           *reinterpret_cast<const uint4*>(w_ + 512));                     \
+    wr[SLOT][1] = join_v8i(*reinterpret_cast<const uint4*>(w_ + 1024),                     \
+                           *reinterpret_cast<const uint4*>(w_ + 1536));                    \
+  } while (0)
+  __syncthreads();
+
+  // Row scales, [K block][row]: element i = m * nb + b of the tile's
+  // [row][K block] table goes to sa_lds[b][m] (consecutive threads take
+  // consecutive elements, so a wave's loads stay contiguous in memory).
+  constexpr int kScalesPerThread = 16;  // covers K <= 8192 in one batch
+  const int a_last = arow[mc - 1] >= 0 ? arow[mc - 1] : 0;  // the tile's last row (row 0 if its index is bad)
+  // A slot past the table, or on a row without a valid index, holds 0; its
+  // load still runs (so that no branch splits the batch) and reads an entry
+  // of the tile's own rows instead (a slot past the table: the first row's
+  // entry 0; a row without a valid index: the last row's entry).  One
+  // stand-in address for all tiles, such as row 0, would be read by every
+  // workgroup at once, and one L2 channel would serve them all.
+  struct ScaleSlot {
+    int m, b, at;
+  };
+  auto row_scale_slot = [&](int i) {
+    const bool in = i < kBM * nb;
+    ScaleSlot r;
+    r.m = in ? i / nb : 0;
+    r.b = in ? i - r.m * nb : 0;
+    r.at = in ? r.b * kSaStride + r.m : -1;
+    return r;
+  };
+  auto row_scale_value = [&](const ScaleSlot& sl, int ar) {
+    const float v = p.sa[(int64_t)(ar >= 0 ? ar : a_last) * nb + sl.b];
+    return (sl.at >= 0 && ar >= 0) ? v : 0.0f;
+  };
+  // N slots per thread: element i = u * kThreads + tid, whose (m, b)
+  // advance by (kThreads / nb, kThreads % nb) per u with a carry instead of
+  // a division per element.  `between` runs after the loads are issued and
+  // before their values are stored.  Elements beyond 16 slots per thread
+  // (K > 8192) follow one at a time.
+  auto fill_row_scales = [&](auto n_tag, auto&& between) {
+    constexpr int N = decltype(n_tag)::value;
+    ScaleSlot ss[N];
+    int sar[N];
+    float sv[N];
+    const int dq = kThreads / nb, dr = kThreads - dq * nb;
+    int m = tid / nb, b = tid - m * nb;
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+      const bool in = m < kBM;
+      ss[u].m = in ? m : 0;
+      ss[u].b = in ? b : 0;
+      ss[u].at = in ? b * kSaStride + m : -1;
+      sar[u] = arow[ss[u].m];
+      b += dr;
+      m += dq;
+      if (b >= nb) {
+        b -= nb;
+        ++m;
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // all row indices read before the first scale load
+#pragma unroll
+    for (int u = 0; u < N; ++u) sv[u] = row_scale_value(ss[u], sar[u]);
+    between();
+#pragma unroll
+    for (int u = 0; u < N; ++u)
+      if (ss[u].at >= 0) sa_lds[ss[u].at] = sv[u];
+    for (int i = N * kThreads + tid; i < kBM * nb; i += kThreads) {
+      const ScaleSlot sl = row_scale_slot(i);
+      sa_lds[sl.at] = row_scale_value(sl, arow[sl.m]);
+    }
+  };
+
+  // Expert rows: 1024 16-byte chunks per K block, 2 per thread; chunk c
+  // covers row c/8, bytes 16*(c%8).  Rows beyond the expert (or with a bad
+  // index) load the tile's last row instead (row 0 if that one is bad too):
+  // their codes are finite and their scale in sa_lds is 0, so their
+  // products promote to exactly 0, and only rows below mc are written.  The
+  // stand-in is a row the tile reads anyway, not one address that every
+  // tail tile of the launch would read at once.
+  const uint8_t* a_src[2];
+  int a_dst[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int c = tid + i * kThreads;
+    const int row = c >> 3, col = (c & 7) * 16;
+    const int ar = arow[row];
+    a_src[i] = p.a + (int64_t)(ar >= 0 ? ar : a_last) * p.K + col;
+    a_dst[i] = swz(row, c & 7);
+  }
+
   const float* swf0 = sw_lds + (GATEUP ? 0 : (wave >> 2)) * nb;  // scale of result rows 0-15
   const float* swf1 = sw_lds + (GATEUP ? 1 : (wave >> 2)) * nb;  // scale of result rows 16-31
   // LDS offsets of this lane's B operand pieces in expert row r32: K chunks
@@ -244,7 +328,6 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[j][i] = 0.0f;
 
-  v8i wr[kRing][2];  // [slot][K half]
   u32x4 ra[2];       // this thread's two 16-byte chunks of one K block of expert rows (ext vectors stay in VGPRs)
   v8i bx[4][2];      // B operands of the step: [expert-row operand][K half]
   float sa[4], sw0 = 0.0f, sw1 = 0.0f;
@@ -260,14 +343,6 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   auto k_loop = [&](auto nq_tag) {
     constexpr int NQ = decltype(nq_tag)::value;
     constexpr int NA = NQ > 2 ? 2 : 1;  // 16-byte expert-row chunks per thread (chunk 1 holds rows 64-127)
-#define MOE_PF_WLOAD(SLOT, BLK)                                                            \
-  do {                                                                                     \
-    const uint8_t* w_ = wsrc + (int64_t)(BLK) * kTileBytes;                                \
-    wr[SLOT][0] = join_v8i(*reinterpret_cast<const uint4*>(w_),                            \
-                           *reinterpret_cast<const uint4*>(w_ + 512));                     \
-    wr[SLOT][1] = join_v8i(*reinterpret_cast<const uint4*>(w_ + 1024),                     \
-                           *reinterpret_cast<const uint4*>(w_ + 1536));                    \
-  } while (0)
   // Expert rows of K block BLK (clamped to the last block, a harmless
   // reload) into registers, and from there into its LDS stage BLK % 3.
 #define MOE_PF_ALOAD(BLK)                                                                  \
@@ -358,11 +433,28 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     __syncthreads();                                                                       \
   } while (0)
 
-    MOE_PF_ALOAD(0);
+    // The first two weight blocks, blocks 0 and 1 of the expert rows and the
+    // row scales in one round trip; block 1 stays in ra for the first memory
+    // phase.
+    // Row scales in batches sized to the table (4, 8 or 16 slots per
+    // thread; every load instruction costs address-unit time, and the down
+    // projection's table fills 4 slots); between a batch's loads and its LDS
+    // stores go the loads of the first two K blocks of expert rows and of
+    // the first two weight blocks, so the stores wait for the scales only.
+    u32x4 ra0[NA];
+    auto issue_blocks = [&]() {
 #pragma unroll
-    for (int s = 0; s < kRing - 1; ++s) MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
-    MOE_PF_ASTORE(0);
-    MOE_PF_ALOAD(1);
+      for (int i = 0; i < NA; ++i) ra0[i] = *reinterpret_cast<const u32x4*>(a_src[i]);
+      MOE_PF_ALOAD(1);
+#pragma unroll
+      for (int s = 0; s < kRing - 1; ++s) MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
+    };
+    const int n_slots = (kBM * nb + kThreads - 1) / kThreads;
+    if (n_slots <= 4) fill_row_scales(std::integral_constant<int, 4>{}, issue_blocks);
+    else if (n_slots <= 8) fill_row_scales(std::integral_constant<int, 8>{}, issue_blocks);
+    else fill_row_scales(std::integral_constant<int, kScalesPerThread>{}, issue_blocks);
+#pragma unroll
+    for (int i = 0; i < NA; ++i) *reinterpret_cast<u32x4*>(smem + a_dst[i]) = ra0[i];
     __syncthreads();
     if (wave >= 4) __syncthreads();  // the lagging half starts one phase later (wave-uniform branch)
 
