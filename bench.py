@@ -38,10 +38,10 @@ METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
 # profiles/*_hbm_traffic.md.  Valid only while the kernel's source file is the
 # one measured (sha256 prefix).
 TRAFFIC = {
-    ("decode1", "ffn_decode_gateup"): {"bytes": 235600691, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
-                                       "sha256_prefix": "ac6a38abd53a3d3b"},
-    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 10126903910, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
-                                          "sha256_prefix": "b4d463edabdef11f"},
+    ("decode1", "ffn_decode_gateup"): {"bytes": 235600711, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
+                                       "sha256_prefix": "1099a418eefb5545"},
+    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 10420016070, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
+                                          "sha256_prefix": "2378356045ea209e"},
 }
 
 

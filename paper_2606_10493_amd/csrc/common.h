@@ -16,34 +16,31 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
 // fp32 -> e4m3 code (OCP E4M3: bias 7, no infinities, max 448), round to
-// nearest with ties to the even code, |v| >= 448 saturates to 448, the sign
-// of zero is kept.  Written from the IEEE-754 binary32 layout:
-//   * |v| < 2^-6 (e4m3 subnormals, spacing 2^-9): code = rne(|v| * 2^9),
-//     the product is exact and 8 is the smallest normal (code 0x08);
-//   * otherwise re-bias the exponent (127 -> 7) and round the 23-bit
-//     mantissa to 3 bits by adding 0x7FFFF plus the kept LSB before dropping
-//     20 bits; a mantissa carry moves into the exponent field by itself.
-// Both candidates are computed and the right one selected (no branches:
-// this runs per element in the GEMM epilogues); the subnormal candidate is
-// formed from min(|v|, 1) so that its conversion stays in range.
+// nearest with ties to the even code, |v| >= 448 saturates to 448 (NaN too),
+// the sign of zero is kept; values below 2^-6 go to the e4m3 subnormals
+// (spacing 2^-9).
+//
+// gfx950's fp32 -> fp8 conversion rounds to nearest even and produces the
+// e4m3 subnormals; it is given the value clamped to +-448 (fminf also maps
+// NaN to 448), so it never sees an out-of-range input.  The result equals
+// the code defined above for every one of the 2^32 fp32 bit patterns
+// (compared on gfx950 against a bit-level software encoder of the same
+// rule); the library's tests compare it with the oracle's nearest-value
+// search on every value of several bands and at every rounding midpoint.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint32_t encode_e4m3(float v) {
-  const uint32_t u = __float_as_uint(v);
-  const uint32_t sign = (u >> 24) & 0x80u;
-  const uint32_t a = u & 0x7fffffffu;
-  const float fa = __uint_as_float(a);
-  const uint32_t sub = (uint32_t)__builtin_rintf(fminf(fa, 1.0f) * 512.0f);
-  const uint32_t nrm = ((a + 0x7ffffu + ((a >> 20) & 1u)) >> 20) - (120u << 3);
-  const uint32_t code = (fa < kE4M3Max) ? (a < 0x3c800000u ? sub : nrm) : 0x7eu;  // 2^-6; NaN saturates
-  return code | sign;
-}
+__device__ __forceinline__ float e4m3_clamp(float v) { return __builtin_copysignf(fminf(fabsf(v), kE4M3Max), v); }
 
-// Quantize one value given the block scale s (s == 0: all-zero block, keep
-// the sign only).  x / s is the correctly rounded fp32 quotient (the library
-// is built with correctly rounded fp32 division).
-__device__ __forceinline__ uint32_t quantize_e4m3(float x, float s) {
-  const uint32_t code = encode_e4m3(x / s);
-  return s > 0.0f ? code : ((__float_as_uint(x) >> 24) & 0x80u);
+// Four values of one scale block quantized with its scale s into one word
+// (byte i = value i): the code of x / s (the correctly rounded fp32 quotient;
+// the library is built with correctly rounded fp32 division).  s == 0 only
+// when every |x| of the block is below 448 * 2^-150 (amax / 448 rounds to
+// 0): then x itself is encoded, which keeps only its sign.
+__device__ __forceinline__ uint32_t quantize4_e4m3(float a, float b, float c, float d, float s) {
+  const bool z = !(s > 0.0f);
+  const float qa = z ? a : a / s, qb = z ? b : b / s, qc = z ? c : c / s, qd = z ? d : d / s;
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(qa), e4m3_clamp(qb), 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(qc), e4m3_clamp(qd), w, true);
+  return (uint32_t)w;
 }
 
 // fp32 -> bf16 bits, round to nearest even (finite inputs).
@@ -104,8 +101,20 @@ __device__ __forceinline__ v8i load_v8i_packed(const uint8_t* p) {
   return join_v8i(*reinterpret_cast<const uint4*>(p), *reinterpret_cast<const uint4*>(p + 1024));
 }
 
+// SiLU(g) * u = g * sigmoid(g) * u.  silu_mul: expf and a correctly rounded
+// division (the decode kernels, bound by weight streaming).  silu_mul_fast:
+// the hardware base-2 exponential of -g * log2(e) and the hardware
+// reciprocal (each about 1 ulp; about 4 ulp in all), for the prefill GEMM
+// epilogue, where no matrix instruction overlaps the epilogue's vector
+// work.  exp2 -> +inf for very negative g gives 0 (the limit), exp2 -> 0
+// for very positive g gives g * u.
 __device__ __forceinline__ float silu_mul(float g, float u) {
   return (g * (1.0f / (1.0f + expf(-g)))) * u;
+}
+
+__device__ __forceinline__ float silu_mul_fast(float g, float u) {
+  const float e = __builtin_amdgcn_exp2f(g * -1.44269504088896341f);
+  return (g * __builtin_amdgcn_rcpf(1.0f + e)) * u;
 }
 
 // Eight consecutive values of a row as fp32 (one 16-byte load of bf16, two of fp32).
@@ -144,11 +153,8 @@ __device__ __forceinline__ void quant_row_group(const InT* __restrict__ x, int64
 #pragma unroll
   for (int m = 8; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
   const float sc = amax / kE4M3Max;
-  uint32_t lo = 0, hi = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) lo |= quantize_e4m3(v[i], sc) << (8 * i);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) hi |= quantize_e4m3(v[4 + i], sc) << (8 * i);
+  const uint32_t lo = quantize4_e4m3(v[0], v[1], v[2], v[3], sc);
+  const uint32_t hi = quantize4_e4m3(v[4], v[5], v[6], v[7], sc);
   *reinterpret_cast<uint2*>(q + idx) = make_uint2(lo, hi);
   if (sub == 0) s[g] = sc;
 }

@@ -267,11 +267,8 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
 #pragma unroll
             for (int sh = 8; sh >= 1; sh >>= 1) amax = fmaxf(amax, __shfl_xor(amax, sh, 16));
             const float sc = amax / kE4M3Max;
-            uint32_t lo = 0, hi = 0;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) lo |= quantize_e4m3(hv[q][i], sc) << (8 * i);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) hi |= quantize_e4m3(hv[q][4 + i], sc) << (8 * i);
+            const uint32_t lo = quantize4_e4m3(hv[q][0], hv[q][1], hv[q][2], hv[q][3], sc);
+            const uint32_t hi = quantize4_e4m3(hv[q][4], hv[q][5], hv[q][6], hv[q][7], sc);
             *reinterpret_cast<uint2*>(qh_lds + q * kQhMaxK + qcol) = make_uint2(lo, hi);
             if (qsub == 0) sh_lds[q * (kQhMaxK / kBlock) + qgrp] = sc;
           }

@@ -153,11 +153,8 @@ __global__ __launch_bounds__(kDcThreads) void ffn_decode_down_combine_kernel(Dow
 #pragma unroll
     for (int m = 8; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
     const float sc = amax / kE4M3Max;
-    uint32_t lo = 0, hi = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) lo |= quantize_e4m3(v[i], sc) << (8 * i);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) hi |= quantize_e4m3(v[4 + i], sc) << (8 * i);
+    const uint32_t lo = quantize4_e4m3(v[0], v[1], v[2], v[3], sc);
+    const uint32_t hi = quantize4_e4m3(v[4], v[5], v[6], v[7], sc);
     *reinterpret_cast<uint2*>(qh + row * p.K + b * kBlock + q16 * 8) = make_uint2(lo, hi);
     if (q16 == 0) sh[row * nb + b] = sc;
   };

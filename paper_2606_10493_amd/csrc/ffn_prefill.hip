@@ -510,7 +510,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     float mx = 0.0f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      hv[j][i] = silu_mul(acc[j][i], acc[j][i + 8]);
+      hv[j][i] = silu_mul_fast(acc[j][i], acc[j][i + 8]);
       mx = fmaxf(mx, fabsf(hv[j][i]));
     }
     mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -527,9 +527,8 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     const float s = amax / kE4M3Max;
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
-      uint32_t packed = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) packed |= quantize_e4m3(hv[j][4 * half + q], s) << (8 * q);
+      const float* hq = hv[j] + 4 * half;
+      const uint32_t packed = quantize4_e4m3(hq[0], hq[1], hq[2], hq[3], s);
       *reinterpret_cast<uint32_t*>(qtile + swz(t, wave) + 8 * half + 4 * g2) = packed;
     }
     if (wave == 0 && g2 == 0 && t < mc) p.sh[(int64_t)(m0 + t) * (p.N / kBlock) + nt] = s;

@@ -15,12 +15,7 @@ namespace moe {
 namespace {
 
 __device__ __forceinline__ uint2 encode8(const float (&v)[8], float s) {
-  uint32_t lo = 0, hi = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) lo |= quantize_e4m3(v[i], s) << (8 * i);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) hi |= quantize_e4m3(v[4 + i], s) << (8 * i);
-  return make_uint2(lo, hi);
+  return make_uint2(quantize4_e4m3(v[0], v[1], v[2], v[3], s), quantize4_e4m3(v[4], v[5], v[6], v[7], s));
 }
 
 // grid: ceil(rows * cols/128 / 16) blocks of 256 threads; 16 groups per block.

@@ -82,6 +82,39 @@ def test_quant_rows_f32_neighbours_of_ties_bit_exact(moe):
     assert np.array_equal(q.cpu().numpy(), q_ref)
 
 
+def _band(lo, hi):
+    """Every fp32 value in [lo, hi)."""
+    a, b = np.float32(lo).view(np.uint32), np.float32(hi).view(np.uint32)
+    return np.arange(a, b, dtype=np.uint32).view(np.float32)
+
+
+def test_quant_rows_f32_every_value_of_three_bands_bit_exact(moe):
+    """Every fp32 value of [2^-8, 2^-5) (across the e4m3 subnormal/normal
+    boundary at 2^-6), of [1, 2) and of [256, 448], and the negatives of
+    every 16th of them, quantized with scale 1 (each row holds 448): the
+    library's codes against the oracle's nearest-value search, value by value
+    (40M values)."""
+    vals = np.concatenate([_band(2.0 ** -8, 2.0 ** -5), _band(1.0, 2.0), _band(256.0, 448.0), np.float32([448.0])])
+    vals = np.concatenate([vals, -vals[::16]])
+    n = (len(vals) + 126) // 127
+    x = np.zeros((n, 128), np.float32)
+    x[:, 0] = 448.0
+    flat = np.zeros(n * 127, np.float32)
+    flat[: len(vals)] = vals
+    x[:, 1:] = flat.reshape(n, 127)
+    log(f"quant_rows_f32 on {len(vals)} band values")
+    q_ref, s_ref = oracle.quantize_rows(x)
+    assert np.all(s_ref == 1.0)
+    q = torch.empty(x.shape, dtype=torch.uint8, device="cuda")
+    s = torch.empty((n, 1), dtype=torch.float32, device="cuda")
+    moe.moe_quant_rows_f32(to_dev(x), q, s)
+    torch.cuda.synchronize()
+    assert np.array_equal(s.cpu().numpy(), s_ref)
+    qc = q.cpu().numpy()
+    bad = np.flatnonzero(qc.reshape(-1) != q_ref.reshape(-1))
+    assert bad.size == 0, (bad.size, x.reshape(-1)[bad[:8]], qc.reshape(-1)[bad[:8]], q_ref.reshape(-1)[bad[:8]])
+
+
 @pytest.mark.parametrize("rows,cols", [(1, 128), (37, 1024), (4096, 7168)])
 def test_quant_act_random_bit_exact(moe, rows, cols):
     rng = np.random.default_rng(rows)
