@@ -330,7 +330,8 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 
   u32x4 ra[2];       // this thread's two 16-byte chunks of one K block of expert rows (ext vectors stay in VGPRs)
   v8i bx[4][2];      // B operands of the step: [expert-row operand][K half]
-  float sa[4], sw0 = 0.0f, sw1 = 0.0f;
+  v16f dp[2] = {v16f{}, v16f{}};  // operands 2 and 3 of the last step, promoted in the next memory phase
+  float sa[4] = {0.0f, 0.0f, 0.0f, 0.0f}, sw0 = 0.0f, sw1 = 0.0f;  // zero: the first memory phase promotes dp (zero) with them
 
   // The K loop is instantiated for NQ = 1..4 expert-row operands: a tile
   // whose rows fill only NQ of the four 32-row operands (the last tile of
@@ -386,6 +387,8 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 #define MOE_PF_MEM(U, J)                                                                   \
   do {                                                                                     \
     const int j_ = (J);                                                                    \
+    if (NQ > 2) MOE_PF_PROMOTE(2, dp[0]);                                                  \
+    if (NQ > 3) MOE_PF_PROMOTE(3, dp[1]);                                                  \
     MOE_PF_ASTORE(j_ + 1);                                                                 \
     MOE_PF_ALOAD(j_ + 2);                                                                  \
     MOE_PF_WLOAD(((U) + kRing - 1) % kRing, j_ + kRing - 1 < nb ? j_ + kRing - 1 : nb - 1); \
@@ -421,8 +424,8 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     if (NQ > 3) d[3] = mfma_f8_32x32x64(wr[U][1], bx[3][1], d[3]);                         \
     if (NQ > 1) MOE_PF_PROMOTE(1, d[1]);                                                   \
     __builtin_amdgcn_sched_barrier(0);                                                     \
-    if (NQ > 2) MOE_PF_PROMOTE(2, d[2]);                                                   \
-    if (NQ > 3) MOE_PF_PROMOTE(3, d[3]);                                                   \
+    if (NQ > 2) dp[0] = d[2];                                                              \
+    if (NQ > 3) dp[1] = d[3];                                                              \
     __builtin_amdgcn_sched_barrier(0);                                                     \
   } while (0)
 #define MOE_PF_STEP(U, J)                                                                  \
@@ -468,6 +471,8 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     }
     if (j0 < nb) MOE_PF_STEP(0, j0);
     if (j0 + 1 < nb) MOE_PF_STEP(1, j0 + 1);
+    if (NQ > 2) MOE_PF_PROMOTE(2, dp[0]);
+    if (NQ > 3) MOE_PF_PROMOTE(3, dp[1]);
     if (wave < 4) __syncthreads();   // pairs with the lagging half's last barrier
 #undef MOE_PF_WLOAD
 #undef MOE_PF_ALOAD
