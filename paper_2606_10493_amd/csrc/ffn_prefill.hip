@@ -75,6 +75,8 @@ struct PrefillArgs {
   int a_rows;
   const int32_t* offsets;     // [E+1]
   const int32_t* mtile_start; // [E+1] exclusive scan of ceil(M_e/128)
+  const int4* desc;           // [max_mtiles] m-tile block descriptors (prefill_tiles_kernel)
+  int64_t max_mtiles;         // bound on the m-tiles (sizes desc)
   int E;
   const uint8_t* w0;          // GATEUP: W_gate [E, N, K]; DOWN: W_down [E, N, K]; packed tiles
   const float* s0;
@@ -87,16 +89,26 @@ struct PrefillArgs {
   float* sh;                  // GATEUP output [rows, N/128]
 };
 
+// mtile_start = exclusive scan of the experts' m-tile counts, and for every
+// m-tile index b in [mtile_start[e], mtile_start[e+1]) the descriptor
+// desc[b] = (e, mtile_start[e], offsets[e], offsets[e+1]), from which a GEMM
+// workgroup derives its tile with one uniform load (no search over experts).
 __global__ __launch_bounds__(1024) void prefill_tiles_kernel(const int32_t* __restrict__ offsets, int E,
-                                                             int32_t* __restrict__ mtile_start) {
+                                                             int32_t* __restrict__ mtile_start,
+                                                             int4* __restrict__ desc, int64_t max_mtiles) {
   __shared__ int wave_tot[16];
   const int e = threadIdx.x;
-  const int c = (e < E) ? (offsets[e + 1] - offsets[e] + kBM - 1) / kBM : 0;
+  const int o0 = e < E ? offsets[e] : 0, o1 = e < E ? offsets[e + 1] : 0;
+  const int c = (e < E && o1 > o0) ? (o1 - o0 + kBM - 1) / kBM : 0;
   int total;
   const int excl = block_exclusive_scan(c, wave_tot, &total);
   if (e < E) mtile_start[e] = excl;
   if (e == 0) mtile_start[E] = total;
+  for (int b = excl; b < excl + c && b < max_mtiles; ++b) desc[b] = make_int4(e, excl, o0, o1);
 }
+
+// The tiles workspace: mtile_start [E+1] (padded to 16 bytes), then desc [max_mtiles].
+size_t tiles_desc_offset(int64_t n_experts) { return ((size_t)(n_experts + 1) * sizeof(int32_t) + 15) & ~(size_t)15; }
 
 // LDS byte offset of 16-byte chunk c (0..7) of row `row` in a 128-byte-row
 // tile.  gfx950's LDS serves 256 bytes per clock (64 four-byte banks), so
@@ -111,12 +123,41 @@ __device__ __forceinline__ v16f mfma_f8_32x32x64(const v8i& a, const v8i& b, con
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
 }
 
+// The tile of work item `item`: expert e owns items [mtile_start[e],
+// mtile_start[e+1]) * n_tiles in n-tile-major order, item = mtile_start[e] *
+// n_tiles + nt * mcount_e + mt.  The m-tiles that read the same weight slice
+// (same nt) are neighbours, so they run together on one XCD and the slice
+// comes from HBM once (m-tile major order fetched the weights once per
+// m-tile).  The expert's ceil(M/32) row groups are dealt evenly over its
+// mcount tiles (tile mt gets q/mcount groups, one more for mt < q % mcount):
+// the same MFMA work as full tiles plus a tail, but tiles of similar size,
+// which advance through their shared weight slice at similar speed, so the
+// slice is fetched from HBM once and read by the others from L2 (a 1-32-row
+// tail tile ran about 3.6 times faster than the full tiles and fetched the
+// slice ahead of them; gate/up read 1.7 times its algorithmic bytes).
+struct Tile {
+  int e, m0, mc, nt;  // expert, first sorted row, rows, n-tile
+};
+
+__device__ __forceinline__ Tile tile_of(const PrefillArgs& p, int item) {
+  const int4 d = p.desc[item / p.n_tiles];
+  const int e = d.x, s0 = d.y, o0 = d.z, o1 = d.w;
+  const int mcount = (o1 - o0 + kBM - 1) / kBM;
+  const int local = item - s0 * p.n_tiles;
+  const int ntx = local / mcount;
+  const int mt = local - ntx * mcount;
+  const int q = (o1 - o0 + 31) >> 5;
+  const int base = q / mcount, extra = q - base * mcount;
+  const int first = o0 + 32 * (mt * base + min(mt, extra));
+  const int groups = base + (mt < extra ? 1 : 0);
+  return Tile{e, first, min(32 * groups, o1 - first), ntx};
+}
+
 template <bool GATEUP>
 __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ int arow[kBM];
   __shared__ float rowmax[8][kBM];
-  __shared__ int tile_info[4];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -125,86 +166,22 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 
   // XCD-major work item over the real items (the grid is an upper bound):
   // XCD x takes items [x*per, (x+1)*per) in order.
-  const int64_t real = (int64_t)p.mtile_start[p.E] * p.n_tiles;
-  const int64_t per = (real + kXcd - 1) / kXcd;
-  const int64_t slot = blockIdx.x / kXcd;
+  int total = p.mtile_start[p.E];
+  if (total > p.max_mtiles) total = (int)p.max_mtiles;  // inconsistent offsets: only described m-tiles run
+  const int real = total * p.n_tiles;  // < 2^31 (the grid bound is checked on the host)
+  const int per = (real + kXcd - 1) / kXcd;
+  const int slot = blockIdx.x / kXcd;
   if (slot >= per) return;
-  const int64_t item = (int64_t)(blockIdx.x % kXcd) * per + slot;
+  const int item = (int)(blockIdx.x % kXcd) * per + slot;
   if (item >= real) return;
-  // Expert e owns items [mtile_start[e], mtile_start[e+1]) * n_tiles, in
-  // n-tile-major order: item = mtile_start[e] * n_tiles + nt * mcount_e + mt.
-  // The m-tiles that read the same weight slice (same nt) are neighbours, so
-  // they run together on one XCD and the slice comes from HBM once (m-tile
-  // major order fetched the weights once per m-tile).  The owner e is the
-  // one with mtile_start[e] <= item / n_tiles < mtile_start[e+1] (empty
-  // experts own nothing), found by all threads in one round of loads; the
-  // owner also publishes the tile's row range and n-tile.
-  const int64_t eblk = item / p.n_tiles;
-  if (tid == 0) tile_info[0] = -1;
-  __syncthreads();
-  for (int x = tid; x < p.E; x += kThreads) {
-    const int s0 = p.mtile_start[x], s1 = p.mtile_start[x + 1];
-    const int o0 = p.offsets[x], o1 = p.offsets[x + 1];
-    // o0 <= o1 holds for consistent offsets.  Testing it (with non-short-
-    // circuit ANDs) makes all four loads precede the branch: one round trip
-    // instead of the offsets being fetched only inside it.
-    const bool owner = (s0 <= eblk) & (eblk < s1) & (o0 <= o1);
-    if (owner) {
-      const int64_t local = item - (int64_t)s0 * p.n_tiles;
-      const int mcount = s1 - s0;
-      const int ntx = (int)(local / mcount);
-      const int mt = (int)(local - (int64_t)ntx * mcount);
-      // The expert's ceil(M/32) row groups are dealt evenly over its
-      // mcount tiles (tile mt gets q/mcount groups, one more for mt <
-      // q % mcount): the same MFMA work as full tiles plus a tail, but
-      // tiles of similar size, which advance through their shared weight
-      // slice at similar speed, so the slice is fetched from HBM once and
-      // read by the others from L2 (a 1-32-row tail tile ran about 3.6
-      // times faster than the full tiles and fetched the slice ahead of
-      // them; gate/up read 1.7 times its algorithmic bytes).
-      const int q = (o1 - o0 + 31) >> 5;
-      const int base = q / mcount, extra = q - base * mcount;
-      const int first = o0 + 32 * (mt * base + min(mt, extra));
-      const int groups = base + (mt < extra ? 1 : 0);
-      tile_info[0] = x;
-      tile_info[1] = first;
-      tile_info[2] = min(32 * groups, o1 - first);
-      tile_info[3] = ntx;
-    }
-  }
-  __syncthreads();
-  const int e = tile_info[0];
-  if (e < 0) return;            // no owner: inconsistent offsets, nothing to compute
-  const int m0 = tile_info[1];  // first sorted row of the tile
-  const int mc = tile_info[2];  // rows in the tile
-  const int nt = tile_info[3];  // n-tile
+  const Tile tile = tile_of(p, item);  // one uniform load, no search and no barrier
+  const int m0 = tile.m0;  // first sorted row of the tile
+  const int mc = tile.mc;  // rows in the tile
+  const int nt = tile.nt;  // n-tile
   const int nb = p.K / kBlock;
 
   float* sa_lds = reinterpret_cast<float*>(smem + kStages * kHalf);  // [nb][kSaStride]
   float* sw_lds = sa_lds + nb * kSaStride;                       // [2][nb]
-
-  // The set-up before the first MFMA is three round trips: (1) the owner
-  // lookup above; (2) the tile's A row indices (threads 0-127) and the weight
-  // scales (the other threads) in parallel; (3) the first two weight blocks,
-  // the first two K blocks of expert rows and the row scales together (at
-  // the start of k_loop).  Each load loop is written so that a thread issues
-  // all its loads before it waits for any.
-  if (tid < kBM) {
-    int row = -1;
-    if (tid < mc) {
-      const int src = p.sorted_src ? p.sorted_src[m0 + tid] / p.topk : m0 + tid;
-      row = (src >= 0 && src < p.a_rows) ? src : -1;
-    }
-    arow[tid] = row;
-  } else {
-    // Weight scales of the tile's two 128-row blocks: GATEUP gate and up
-    // block nt; DOWN blocks 2nt and 2nt + 1 (waves 0-3 and 4-7).
-    for (int i = tid - kBM; i < 2 * nb; i += kThreads - kBM) {
-      const int h = i / nb, b = i - h * nb;
-      const int64_t wrow = (int64_t)e * (p.N / kBlock) + (GATEUP ? nt : 2 * nt + h);
-      sw_lds[i] = ((GATEUP && h) ? p.s1 : p.s0)[wrow * nb + b];
-    }
-  }
 
   // This wave's 32-row weight operand: rows 0-15 and 16-31 are two packed
   // 16-row groups (GATEUP: the gate and the up group nt*8 + w; DOWN: groups
@@ -212,7 +189,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   // [0, 32) of each block, i.e. kq = 2 g2 and 2 g2 + 1 of the packed tile.
   const uint8_t* wsrc;
   {
-    const int64_t ebase = (int64_t)e * p.N * p.K;
+    const int64_t ebase = (int64_t)tile.e * p.N * p.K;
     const int64_t grp = GATEUP ? (int64_t)nt * (kBlock / 16) + wave : (int64_t)nt * (kBN / 16) + 2 * wave + (r32 >> 4);
     const uint8_t* wm = (GATEUP && r32 >= 16) ? p.w1 : p.w0;
     wsrc = wm + ebase + grp * nb * kTileBytes + packed_lane_offset(0, 2 * g2, r32 & 15);
@@ -226,100 +203,36 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     wr[SLOT][1] = join_v8i(*reinterpret_cast<const uint4*>(w_ + 1024),                     \
                            *reinterpret_cast<const uint4*>(w_ + 1536));                    \
   } while (0)
-  __syncthreads();
 
-  // Row scales, [K block][row]: element i = m * nb + b of the tile's
-  // [row][K block] table goes to sa_lds[b][m] (consecutive threads take
-  // consecutive elements, so a wave's loads stay contiguous in memory).
-  constexpr int kScalesPerThread = 16;  // covers K <= 8192 in one batch
-  const int a_last = arow[mc - 1] >= 0 ? arow[mc - 1] : 0;  // the tile's last row (row 0 if its index is bad)
-  // A slot past the table, or on a row without a valid index, holds 0; its
-  // load still runs (so that no branch splits the batch) and reads an entry
-  // of the tile's own rows instead (a slot past the table: the first row's
-  // entry 0; a row without a valid index: the last row's entry).  One
-  // stand-in address for all tiles, such as row 0, would be read by every
-  // workgroup at once, and one L2 channel would serve them all.
-  struct ScaleSlot {
-    int m, b, at;
-  };
-  auto row_scale_slot = [&](int i) {
-    const bool in = i < kBM * nb;
-    ScaleSlot r;
-    r.m = in ? i / nb : 0;
-    r.b = in ? i - r.m * nb : 0;
-    r.at = in ? r.b * kSaStride + r.m : -1;
-    return r;
-  };
-  auto row_scale_value = [&](const ScaleSlot& sl, int ar) {
-    const float v = p.sa[(int64_t)(ar >= 0 ? ar : a_last) * nb + sl.b];
-    return (sl.at >= 0 && ar >= 0) ? v : 0.0f;
-  };
-  // N slots per thread: element i = u * kThreads + tid, whose (m, b)
-  // advance by (kThreads / nb, kThreads % nb) per u with a carry instead of
-  // a division per element.  `between` runs after the loads are issued and
-  // before their values are stored.  Elements beyond 16 slots per thread
-  // (K > 8192) follow one at a time.
-  auto fill_row_scales = [&](auto n_tag, auto&& between) {
-    constexpr int N = decltype(n_tag)::value;
-    ScaleSlot ss[N];
-    int sar[N];
-    float sv[N];
-    const int dq = kThreads / nb, dr = kThreads - dq * nb;
-    int m = tid / nb, b = tid - m * nb;
+  // The set-up before the first MFMA is two round trips after the tile
+  // lookup: (1) the row indices and weight scales, with the first two
+  // weight blocks issued behind them; (2) the row scales and the first two K
+  // blocks of expert rows (the weights are in flight since round trip 1).
+  // Each load loop is written so that a thread issues all its loads before
+  // it waits for any.  Weight scales of the tile's two 128-row blocks:
+  // GATEUP gate and up block nt; DOWN blocks 2nt and 2nt + 1 (waves 0-3 and
+  // 4-7).
+  auto issue_indices_and_weights = [&]() {
+    // One unconditional 4-byte load per thread from a per-thread address
+    // (threads 0-127: the row's sorted_src entry, clamped to the tile; the
+    // others: their weight-scale entry, clamped to the table), so that no
+    // branch makes the weight loads below wait for it.
+    const int ti = tid < kBM ? min(tid, mc - 1) : min(tid - kBM, 2 * nb - 1);
+    const int h = ti / nb, b = ti - h * nb;
+    const int64_t wrow = (int64_t)tile.e * (p.N / kBlock) + (GATEUP ? nt : 2 * nt + h);
+    const float* sw_src = ((GATEUP && h) ? p.s1 : p.s0) + wrow * nb + b;
+    const uint32_t* src = (tid < kBM && p.sorted_src) ? reinterpret_cast<const uint32_t*>(p.sorted_src + m0 + ti)
+                                                      : reinterpret_cast<const uint32_t*>(sw_src);
+    const uint32_t raw = *src;
 #pragma unroll
-    for (int u = 0; u < N; ++u) {
-      const bool in = m < kBM;
-      ss[u].m = in ? m : 0;
-      ss[u].b = in ? b : 0;
-      ss[u].at = in ? b * kSaStride + m : -1;
-      sar[u] = arow[ss[u].m];
-      b += dr;
-      m += dq;
-      if (b >= nb) {
-        b -= nb;
-        ++m;
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);  // all row indices read before the first scale load
-#pragma unroll
-    for (int u = 0; u < N; ++u) sv[u] = row_scale_value(ss[u], sar[u]);
-    between();
-#pragma unroll
-    for (int u = 0; u < N; ++u)
-      if (ss[u].at >= 0) sa_lds[ss[u].at] = sv[u];
-    for (int i = N * kThreads + tid; i < kBM * nb; i += kThreads) {
-      const ScaleSlot sl = row_scale_slot(i);
-      sa_lds[sl.at] = row_scale_value(sl, arow[sl.m]);
+    for (int s = 0; s < kRing - 1; ++s) MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
+    if (tid < kBM) {
+      const int srow = p.sorted_src ? (int)raw / p.topk : m0 + tid;
+      arow[tid] = (tid < mc && srow >= 0 && srow < p.a_rows) ? srow : -1;
+    } else if (tid - kBM < 2 * nb) {
+      sw_lds[tid - kBM] = __uint_as_float(raw);
     }
   };
-
-  // Expert rows: 1024 16-byte chunks per K block, 2 per thread; chunk c
-  // covers row c/8, bytes 16*(c%8).  Rows beyond the expert (or with a bad
-  // index) load the tile's last row instead (row 0 if that one is bad too):
-  // their codes are finite and their scale in sa_lds is 0, so their
-  // products promote to exactly 0, and only rows below mc are written.  The
-  // stand-in is a row the tile reads anyway, not one address that every
-  // tail tile of the launch would read at once.
-  const uint8_t* a_src[2];
-  int a_dst[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int c = tid + i * kThreads;
-    const int row = c >> 3, col = (c & 7) * 16;
-    const int ar = arow[row];
-    a_src[i] = p.a + (int64_t)(ar >= 0 ? ar : a_last) * p.K + col;
-    a_dst[i] = swz(row, c & 7);
-  }
-
-  const float* swf0 = sw_lds + (GATEUP ? 0 : (wave >> 2)) * nb;  // scale of result rows 0-15
-  const float* swf1 = sw_lds + (GATEUP ? 1 : (wave >> 2)) * nb;  // scale of result rows 16-31
-  // LDS offsets of this lane's B operand pieces in expert row r32: K chunks
-  // 4h + 2 g2 + part; rows 32j + r32 share (row / 2) % 8, hence one offset.
-  int bo[2][2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h)
-#pragma unroll
-    for (int part = 0; part < 2; ++part) bo[h][part] = swz(r32, 4 * h + 2 * g2 + part);
 
   // acc[j][i]: weight row 8*(i/4) + 4*g2 + i%4 of the operand, expert row 32j + r32.
   v16f acc[4];
@@ -344,6 +257,104 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   auto k_loop = [&](auto nq_tag) {
     constexpr int NQ = decltype(nq_tag)::value;
     constexpr int NA = NQ > 2 ? 2 : 1;  // 16-byte expert-row chunks per thread (chunk 1 holds rows 64-127)
+    // Round trip 1: the tile's A row indices (threads 0-127) and the weight
+    // scales (the other threads), with the first two weight blocks issued
+    // behind them (the row indices are waited for, the weights are not).
+    issue_indices_and_weights();
+    __syncthreads();
+    // Row scales, [K block][row]: element i = m * nb + b of the tile's
+    // [row][K block] table goes to sa_lds[b][m] (consecutive threads take
+    // consecutive elements, so a wave's loads stay contiguous in memory).
+    constexpr int kScalesPerThread = 16;  // covers K <= 8192 in one batch
+    const int a_last = arow[mc - 1] >= 0 ? arow[mc - 1] : 0;  // the tile's last row (row 0 if its index is bad)
+    // A slot past the table, or on a row without a valid index, holds 0; its
+    // load still runs (so that no branch splits the batch) and reads an entry
+    // of the tile's own rows instead (a slot past the table: the first row's
+    // entry 0; a row without a valid index: the last row's entry).  One
+    // stand-in address for all tiles, such as row 0, would be read by every
+    // workgroup at once, and one L2 channel would serve them all.
+    struct ScaleSlot {
+      int m, b, at;
+    };
+    auto row_scale_slot = [&](int i) {
+      const bool in = i < kBM * nb;
+      ScaleSlot r;
+      r.m = in ? i / nb : 0;
+      r.b = in ? i - r.m * nb : 0;
+      r.at = in ? r.b * kSaStride + r.m : -1;
+      return r;
+    };
+    auto row_scale_value = [&](const ScaleSlot& sl, int ar) {
+      const float v = p.sa[(int64_t)(ar >= 0 ? ar : a_last) * nb + sl.b];
+      return (sl.at >= 0 && ar >= 0) ? v : 0.0f;
+    };
+    // N slots per thread: element i = u * kThreads + tid, whose (m, b)
+    // advance by (kThreads / nb, kThreads % nb) per u with a carry instead of
+    // a division per element.  `between` runs after the loads are issued and
+    // before their values are stored.  Elements beyond 16 slots per thread
+    // (K > 8192) follow one at a time.
+    auto fill_row_scales = [&](auto n_tag, auto&& between) {
+      constexpr int N = decltype(n_tag)::value;
+      ScaleSlot ss[N];
+      int sar[N];
+      float sv[N];
+      const int dq = kThreads / nb, dr = kThreads - dq * nb;
+      int m = tid / nb, b = tid - m * nb;
+  #pragma unroll
+      for (int u = 0; u < N; ++u) {
+        const bool in = m < kBM;
+        ss[u].m = in ? m : 0;
+        ss[u].b = in ? b : 0;
+        ss[u].at = in ? b * kSaStride + m : -1;
+        sar[u] = arow[ss[u].m];
+        b += dr;
+        m += dq;
+        if (b >= nb) {
+          b -= nb;
+          ++m;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);  // all row indices read before the first scale load
+  #pragma unroll
+      for (int u = 0; u < N; ++u) sv[u] = row_scale_value(ss[u], sar[u]);
+      between();
+  #pragma unroll
+      for (int u = 0; u < N; ++u)
+        if (ss[u].at >= 0) sa_lds[ss[u].at] = sv[u];
+      for (int i = N * kThreads + tid; i < kBM * nb; i += kThreads) {
+        const ScaleSlot sl = row_scale_slot(i);
+        sa_lds[sl.at] = row_scale_value(sl, arow[sl.m]);
+      }
+    };
+
+    // Expert rows: 1024 16-byte chunks per K block, 2 per thread; chunk c
+    // covers row c/8, bytes 16*(c%8).  Rows beyond the expert (or with a bad
+    // index) load the tile's last row instead (row 0 if that one is bad too):
+    // their codes are finite and their scale in sa_lds is 0, so their
+    // products promote to exactly 0, and only rows below mc are written.  The
+    // stand-in is a row the tile reads anyway, not one address that every
+    // tail tile of the launch would read at once.
+    const uint8_t* a_src[2];
+    int a_dst[2];
+  #pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + i * kThreads;
+      const int row = c >> 3, col = (c & 7) * 16;
+      const int ar = arow[row];
+      a_src[i] = p.a + (int64_t)(ar >= 0 ? ar : a_last) * p.K + col;
+      a_dst[i] = swz(row, c & 7);
+    }
+
+    const float* swf0 = sw_lds + (GATEUP ? 0 : (wave >> 2)) * nb;  // scale of result rows 0-15
+    const float* swf1 = sw_lds + (GATEUP ? 1 : (wave >> 2)) * nb;  // scale of result rows 16-31
+    // LDS offsets of this lane's B operand pieces in expert row r32: K chunks
+    // 4h + 2 g2 + part; rows 32j + r32 share (row / 2) % 8, hence one offset.
+    int bo[2][2];
+  #pragma unroll
+    for (int h = 0; h < 2; ++h)
+  #pragma unroll
+      for (int part = 0; part < 2; ++part) bo[h][part] = swz(r32, 4 * h + 2 * g2 + part);
+
   // Expert rows of K block BLK (clamped to the last block, a harmless
   // reload) into registers, and from there into its LDS stage BLK % 3.
 #define MOE_PF_ALOAD(BLK)                                                                  \
@@ -436,21 +447,19 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     __syncthreads();                                                                       \
   } while (0)
 
-    // The first two weight blocks, blocks 0 and 1 of the expert rows and the
-    // row scales in one round trip; block 1 stays in ra for the first memory
-    // phase.
+    // Blocks 0 and 1 of the expert rows and the row scales in one round
+    // trip (the first two weight blocks were issued before the previous
+    // item's epilogue); block 1 stays in ra for the first memory phase.
     // Row scales in batches sized to the table (4, 8 or 16 slots per
     // thread; every load instruction costs address-unit time, and the down
     // projection's table fills 4 slots); between a batch's loads and its LDS
-    // stores go the loads of the first two K blocks of expert rows and of
-    // the first two weight blocks, so the stores wait for the scales only.
+    // stores go the loads of the first two K blocks of expert rows, so the
+    // stores wait for the scales only.
     u32x4 ra0[NA];
     auto issue_blocks = [&]() {
 #pragma unroll
       for (int i = 0; i < NA; ++i) ra0[i] = *reinterpret_cast<const u32x4*>(a_src[i]);
       MOE_PF_ALOAD(1);
-#pragma unroll
-      for (int s = 0; s < kRing - 1; ++s) MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
     };
     const int n_slots = (kBM * nb + kThreads - 1) / kThreads;
     if (n_slots <= 4) fill_row_scales(std::integral_constant<int, 4>{}, issue_blocks);
@@ -474,7 +483,6 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     if (NQ > 2) MOE_PF_PROMOTE(2, dp[0]);
     if (NQ > 3) MOE_PF_PROMOTE(3, dp[1]);
     if (wave < 4) __syncthreads();   // pairs with the lagging half's last barrier
-#undef MOE_PF_WLOAD
 #undef MOE_PF_ALOAD
 #undef MOE_PF_ASTORE
 #undef MOE_PF_PROMOTE
@@ -490,6 +498,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     default: k_loop(std::integral_constant<int, 4>{}); break;
   }
 
+
   if (!GATEUP) {
     // y[m0 + t][nt*256 + 32w + 8*(i/4) + 4*g2 + i%4] for expert row t = 32j + r32.
 #pragma unroll
@@ -502,8 +511,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
           *reinterpret_cast<v4f*>(dst + q * 8) = v4f{acc[j][4 * q], acc[j][4 * q + 1], acc[j][4 * q + 2], acc[j][4 * q + 3]};
       }
     }
-    return;
-  }
+  } else {
 
   // GATEUP epilogue: h = SiLU(G) * U for channels 16w + 8*(i/4) + 4*g2 + i%4
   // (i < 8; the up value is acc[j][i + 8]) of rows t = 32j + r32; per-row
@@ -548,6 +556,8 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
       *reinterpret_cast<uint4*>(p.qh + (int64_t)(m0 + row) * p.N + nt * kBlock + col) =
           *reinterpret_cast<const uint4*>(qtile + swz(row, c & 7));
   }
+  }  // GATEUP epilogue
+#undef MOE_PF_WLOAD
 }
 
 template <bool GATEUP>
@@ -575,14 +585,24 @@ moe_status_t prefill_shape_check(const moe_dims_t& d) {
     return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: one expert matrix (%d x %d) exceeds 2 GiB", d.inter,
                 d.hidden);
   const int kmax = d.hidden > d.inter ? d.hidden : d.inter;
+  // The [2][K/128] weight-scale table is loaded one entry per thread, by the threads after the first 128.
+  if (2 * (kmax / kBlock) > kThreads - kBM)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: K=%d exceeds %d", kmax, (kThreads - kBM) / 2 * kBlock);
   const size_t lds = (size_t)kStages * kHalf + sizeof(float) * ((size_t)kSaStride + 2) * (kmax / kBlock);
   if (lds > 150 * 1024) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: K=%d needs %zu bytes of LDS", kmax, lds);
   return MOE_OK;
 }
 
+// Bound on the 128-row m-tiles of R routed rows over E experts.
+int64_t prefill_max_mtiles(int64_t R, int64_t E) { return (R + kBM - 1) / kBM + (R < E ? R : E); }
+
+// mtile_start [E+1] and the m-tile descriptors [max_mtiles].
+size_t prefill_tiles_bytes(int64_t n_experts, int64_t max_mtiles) {
+  return tiles_desc_offset(n_experts) + (size_t)max_mtiles * sizeof(int4);
+}
+
 size_t prefill_tile_workspace(const moe_dims_t& d, int32_t T) {
-  (void)T;
-  return sizeof(int32_t) * (size_t)(d.n_experts + 1);
+  return prefill_tiles_bytes(d.n_experts, prefill_max_mtiles((int64_t)T * d.topk, d.n_experts));
 }
 
 // Gate/up then down over the expert-sorted rows described by offsets[0..E].
@@ -595,13 +615,15 @@ moe_status_t run_ffn_prefill_view(const moe_dims_t& d, int64_t max_mtiles, int32
                                   int32_t* tiles, hipStream_t stream) {
   moe_status_t st0 = prefill_shape_check(d);
   if (st0 != MOE_OK) return st0;
-  MOE_LAUNCH("prefill_tiles", prefill_tiles_kernel, dim3(1), dim3(1024), 0, stream, offsets, d.n_experts, tiles);
+  int4* desc = reinterpret_cast<int4*>(reinterpret_cast<uint8_t*>(tiles) + tiles_desc_offset(d.n_experts));
+  MOE_LAUNCH("prefill_tiles", prefill_tiles_kernel, dim3(1), dim3(1024), 0, stream, offsets, d.n_experts, tiles, desc,
+             max_mtiles);
   moe_status_t st = check_launch("prefill_tiles");
   if (st != MOE_OK) return st;
 
   PrefillArgs g{};
   g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = a_rows;
-  g.offsets = offsets; g.mtile_start = tiles; g.E = d.n_experts;
+  g.offsets = offsets; g.mtile_start = tiles; g.desc = desc; g.max_mtiles = max_mtiles; g.E = d.n_experts;
   g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
   g.N = d.inter; g.K = d.hidden; g.n_tiles = d.inter / kBlock;
   g.qh = qh; g.sh = sh; g.y = nullptr;
@@ -610,7 +632,7 @@ moe_status_t run_ffn_prefill_view(const moe_dims_t& d, int64_t max_mtiles, int32
 
   PrefillArgs dn{};
   dn.a = qh; dn.sa = sh; dn.sorted_src = nullptr; dn.topk = d.topk; dn.a_rows = (int)((int64_t)a_rows * d.topk);
-  dn.offsets = offsets; dn.mtile_start = tiles; dn.E = d.n_experts;
+  dn.offsets = offsets; dn.mtile_start = tiles; dn.desc = desc; dn.max_mtiles = max_mtiles; dn.E = d.n_experts;
   dn.w0 = w_down; dn.s0 = s_down; dn.w1 = nullptr; dn.s1 = nullptr;
   dn.N = d.hidden; dn.K = d.inter; dn.n_tiles = d.hidden / kBN;
   dn.y = y_rows; dn.qh = nullptr; dn.sh = nullptr;
@@ -622,8 +644,7 @@ moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, 
                              const float* s_gate, const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
                              const float* s_down, float* y_rows, uint8_t* qh, float* sh, int32_t* tiles,
                              hipStream_t stream) {
-  const int64_t R = (int64_t)T * d.topk;
-  const int64_t max_mtiles = (R + kBM - 1) / kBM + (R < d.n_experts ? R : d.n_experts);
+  const int64_t max_mtiles = prefill_max_mtiles((int64_t)T * d.topk, d.n_experts);
   return run_ffn_prefill_view(d, max_mtiles, T, qx, sx, offsets, sorted_src, w_gate, s_gate, w_up, s_up, w_down,
                               s_down, y_rows, qh, sh, tiles, stream);
 }

@@ -41,6 +41,7 @@ moe_status_t run_ffn_prefill_view(const moe_dims_t& d, int64_t max_mtiles, int32
                                   const uint8_t* w_gate, const float* s_gate, const uint8_t* w_up, const float* s_up,
                                   const uint8_t* w_down, const float* s_down, float* y_rows, uint8_t* qh, float* sh,
                                   int32_t* tiles, hipStream_t stream);
+size_t prefill_tiles_bytes(int64_t n_experts, int64_t max_mtiles);
 
 namespace {
 
@@ -71,7 +72,7 @@ StreamLayout layout(const moe_dims_t& d, int32_t T, int32_t chunk_tokens) {
   L.perm_ws = take(moe_permute_workspace(chunk_tokens, d.topk, d.n_experts));
   L.qh = take((size_t)ck * I);
   L.sh = take((size_t)ck * (I / kBlock) * sizeof(float));
-  L.tiles = take((size_t)(E + 1) * sizeof(int32_t));
+  L.tiles = take(prefill_tiles_bytes(E, (ck + 127) / 128 + E));  // views of G <= E experts, chunk rows
   L.y = take((size_t)T * k * H * sizeof(float));
   L.total = off;
   return L;
