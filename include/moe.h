@@ -183,6 +183,9 @@ moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t 
  * y_rows: device fp32 [T*k, H] in expert-sorted order.
  * ws: device workspace of moe_expert_ffn_workspace(dims, T, regime) bytes.
  * regime: see moe_regime_t; DECODE requires T <= MOE_DECODE_MAX_TOKENS.
+ * The PREFILL regime requires H % 256 == 0, max(H, I) <= 24576 and
+ * I * H < 2^31; other shapes return MOE_ERR_UNSUPPORTED_SHAPE before anything
+ * is enqueued.
  */
 size_t moe_expert_ffn_workspace(moe_dims_t dims, int32_t T, moe_regime_t regime);
 moe_status_t moe_expert_ffn(moe_dims_t dims, int32_t T, moe_regime_t regime,

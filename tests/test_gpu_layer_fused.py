@@ -151,6 +151,7 @@ def test_fused_layer_deepseek_decode_equals_four_calls(moe, deepseek_layer, name
     (256, 128, 1024, 32, 2, "decode"),    # E = 1024, k = 32: the widest sort
     (256, 128, 1024, 32, 40, "prefill"),
     (384, 128, 8, 2, 9, "decode"),        # H a multiple of 128 but not of 256 (decode only)
+    (8448, 256, 4, 2, 40, "prefill"),     # K = 8448 > 8192: row scales beyond one 16-load batch
 ], ids=lambda v: str(v))
 def test_fused_layer_edge_shapes(moe, h, i, e, k, t, regime):
     rg = moe.MOE_REGIME_DECODE if regime == "decode" else moe.MOE_REGIME_PREFILL
@@ -167,6 +168,20 @@ def test_fused_layer_edge_shapes(moe, h, i, e, k, t, regime):
 
 def test_fused_layer_prefill_rejects_h_not_multiple_of_256(moe):
     w, x, ids, wts = _layer_inputs(384, 128, 8, 2, 9, "uniform")
+    wg, wu, wd = synth.weights_host(w)
+    dweights = quantize_weights_gpu(moe, wg, wu, wd)
+    buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, moe.MOE_REGIME_PREFILL, fused=True)
+    with pytest.raises(moe.MoEError):
+        moe.run_layer(buf, bf16_dev(x), to_dev(ids), to_dev(wts), dweights)
+    torch.cuda.synchronize()
+
+
+
+def test_fused_layer_prefill_rejects_k_beyond_its_limit(moe):
+    """K <= 24576 in the prefill regime (the [2][K/128] weight-scale table is
+    loaded one entry per thread); H = 24832 is rejected before anything runs
+    (the decode regime stops at H = 16384)."""
+    w, x, ids, wts = _layer_inputs(24832, 128, 2, 1, 4, "uniform")
     wg, wu, wd = synth.weights_host(w)
     dweights = quantize_weights_gpu(moe, wg, wu, wd)
     buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, moe.MOE_REGIME_PREFILL, fused=True)
