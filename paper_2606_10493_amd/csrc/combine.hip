@@ -13,13 +13,49 @@
 namespace moe {
 namespace {
 
+// Slots in batches of 8: the batch's row indices and weights are loaded
+// first, then its 8 rows (16 loads in flight per thread), then the products
+// are added in slot order.  A slot past k reloads slot k-1 and is not
+// added.  Same arithmetic and order as combine8, so the same bits.
+__device__ __forceinline__ uint4 combine8_batched(const float* __restrict__ y, const int32_t* __restrict__ dest,
+                                                  const float* __restrict__ w, int k, int H, int64_t t, int n) {
+#pragma clang fp contract(off)
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
+  for (int j0 = 0; j0 < k; j0 += 8) {
+    int64_t p[8];
+    float wj[8], v[8][8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = min(j0 + u, k - 1);
+      p[u] = dest[t * k + j];
+      wj[u] = w[t * k + j];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) load8_f32(y + p[u] * H + n, v[u]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (j0 + u < k) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = acc[i] + wj[u] * v[u][i];
+      }
+  }
+  uint4 o;
+  o.x = (uint32_t)f32_to_bf16_rne(acc[0]) | ((uint32_t)f32_to_bf16_rne(acc[1]) << 16);
+  o.y = (uint32_t)f32_to_bf16_rne(acc[2]) | ((uint32_t)f32_to_bf16_rne(acc[3]) << 16);
+  o.z = (uint32_t)f32_to_bf16_rne(acc[4]) | ((uint32_t)f32_to_bf16_rne(acc[5]) << 16);
+  o.w = (uint32_t)f32_to_bf16_rne(acc[6]) | ((uint32_t)f32_to_bf16_rne(acc[7]) << 16);
+  return o;
+}
+
 __global__ __launch_bounds__(128) void combine_kernel(const float* __restrict__ y, const int32_t* __restrict__ dest,
                                                       const float* __restrict__ w, int k, int H, int blocks_per_tok,
                                                       uint16_t* __restrict__ out) {
   const int64_t t = blockIdx.x / blocks_per_tok;
   const int n = ((int)(blockIdx.x - t * blocks_per_tok) * 128 + (int)threadIdx.x) * 8;
   if (n >= H) return;
-  *reinterpret_cast<uint4*>(out + t * H + n) = combine8(y, dest, w, k, H, t, n);
+  *reinterpret_cast<uint4*>(out + t * H + n) = combine8_batched(y, dest, w, k, H, t, n);
 }
 
 }  // namespace
