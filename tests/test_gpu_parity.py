@@ -240,7 +240,7 @@ def test_permute_reports_bad_ids_and_stays_a_bijection(moe, t):
 
 
 # --------------------------------------------------------------- combine
-@pytest.mark.parametrize("t,k,h", [(1, 8, 7168), (37, 2, 256), (300, 8, 1024)])
+@pytest.mark.parametrize("t,k,h", [(1, 8, 7168), (37, 2, 256), (300, 8, 1024), (5, 9, 512), (3, 17, 256), (4, 32, 128)])
 def test_combine_bit_exact(moe, t, k, h):
     rng = np.random.default_rng(t)
     y = rng.standard_normal((t * k, h)).astype(np.float32)
