@@ -187,12 +187,6 @@ __device__ __forceinline__ uint4 combine8_of(RowOf row_of, const int32_t* __rest
   return o;
 }
 
-// The same for outputs n .. n+7 of fp32 expert rows y [rows, H] in memory.
-__device__ __forceinline__ uint4 combine8(const float* __restrict__ y, const int32_t* __restrict__ dest,
-                                          const float* __restrict__ w, int k, int H, int64_t t, int n) {
-  return combine8_of([&](int64_t p) { return y + p * H + n; }, dest, w, k, t);
-}
-
 // Exclusive prefix sum of v over the whole workgroup (blockDim.x a multiple
 // of 64, at most 1024): shuffle scan inside each wave, wave totals through
 // LDS (wave_tot holds blockDim.x/64 ints).  Returns the exclusive prefix and
