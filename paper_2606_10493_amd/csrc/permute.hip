@@ -205,57 +205,80 @@ __device__ __forceinline__ void permute_one_chunk(const int32_t* __restrict__ id
 }
 
 // At most kTinySlots slots (decode batches): the same results as
-// permute_one_chunk with two barriers.  Slot f's stable position among the
-// valid slots is the number of valid slots g with (id[g], g) < (id[f], f);
-// an invalid slot goes after all valid ones, in slot order; offsets[e] is
-// the number of valid slots with id < e.  Every count runs over at most 64
-// slots staged in LDS.
+// permute_one_chunk with two barriers and no loop whose trip count depends
+// on the slot count.  Each slot gets a key: its id if valid, INT_MAX if not
+// (or past the slots).  Slot f's stable position among the valid slots is the
+// number of keys g with (key[g], g) < (key[f], f); an invalid slot goes after
+// all valid ones, in slot order (a ballot prefix count); offsets[e] is the
+// number of keys below e.  The counts read the 64 keys as 16 broadcast int4
+// LDS loads, issued together.
 constexpr int kTinySlots = 64;
 
 __device__ __forceinline__ void permute_tiny(const int32_t* __restrict__ ids, int T, int k, int E,
                                              int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_src,
                                              int32_t* __restrict__ dest_row, int32_t* __restrict__ dev_status) {
   __shared__ int sid[kTinySlots];
-  __shared__ int valid[kTinySlots];
+  __shared__ __attribute__((aligned(16))) int key[kTinySlots];
   const int n = T * k, tid = threadIdx.x;
-  if (tid < n) {
-    const int32_t id = ids[tid];
-    sid[tid] = (id >= 0 && id < E) ? id : -1;
+  if (tid < kTinySlots) {
+    int id = -1;
+    if (tid < n) {
+      const int32_t v = ids[tid];
+      id = (v >= 0 && v < E) ? v : -1;
+    }
+    sid[tid] = id;
   }
   __syncthreads();
   uint32_t err = 0;
+  bool valid = false;
+  int me = INT_MAX;
   if (tid < n) {
     const int t = tid / k, j = tid - t * k;
-    const int me = sid[tid];
-    if (me < 0) {
+    const int id = sid[tid];
+    if (id < 0) {
       err = MOE_DEV_BAD_EXPERT_ID;
     } else {
       for (int i = 0; i < j; ++i)
-        if (sid[t * k + i] == me) err = MOE_DEV_DUP_EXPERT_ID;
+        if (sid[t * k + i] == id) err = MOE_DEV_DUP_EXPERT_ID;
     }
-    valid[tid] = err == 0;
+    valid = err == 0;
+    me = valid ? id : INT_MAX;
   }
+  if (tid < kTinySlots) key[tid] = me;
+  // Slots live in wave 0 (n <= 64): its ballots count valid and invalid slots.
+  const unsigned long long vmask = __ballot(tid < n && valid);
+  const unsigned long long bmask = __ballot(tid < n && !valid);
   __syncthreads();
-  int n_valid = 0;
-  for (int g = 0; g < n; ++g) n_valid += valid[g];
+  const int4* k4 = reinterpret_cast<const int4*>(key);
   if (tid < n) {
-    const int me = sid[tid];
-    int pos = 0;
-    if (valid[tid]) {
-      for (int g = 0; g < n; ++g) pos += (valid[g] && (sid[g] < me || (sid[g] == me && g < tid))) ? 1 : 0;
+    int pos;
+    if (valid) {
+      pos = 0;
+#pragma unroll
+      for (int q = 0; q < kTinySlots / 4; ++q) {
+        const int4 v = k4[q];
+        const int g = 4 * q;
+        pos += (v.x < me || (v.x == me && g < tid)) ? 1 : 0;
+        pos += (v.y < me || (v.y == me && g + 1 < tid)) ? 1 : 0;
+        pos += (v.z < me || (v.z == me && g + 2 < tid)) ? 1 : 0;
+        pos += (v.w < me || (v.w == me && g + 3 < tid)) ? 1 : 0;
+      }
     } else {
-      pos = n_valid;
-      for (int g = 0; g < tid; ++g) pos += valid[g] ? 0 : 1;
+      pos = __popcll(vmask) + __popcll(bmask & ((1ull << tid) - 1ull));
     }
     dest_row[tid] = pos;
     sorted_src[pos] = tid;
   }
   for (int e = tid; e < E; e += blockDim.x) {
     int c = 0;
-    for (int g = 0; g < n; ++g) c += (valid[g] && sid[g] < e) ? 1 : 0;
+#pragma unroll
+    for (int q = 0; q < kTinySlots / 4; ++q) {
+      const int4 v = k4[q];
+      c += (v.x < e ? 1 : 0) + (v.y < e ? 1 : 0) + (v.z < e ? 1 : 0) + (v.w < e ? 1 : 0);
+    }
     offsets[e] = c;
   }
-  if (tid == 0) offsets[E] = n_valid;
+  if (tid == 0) offsets[E] = __popcll(vmask);
   report(dev_status, err);
 }
 
