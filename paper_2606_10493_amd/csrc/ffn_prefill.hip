@@ -38,7 +38,8 @@
 // writes fp32 in 16-byte pieces.
 //
 // Work items are (expert m-tile, n-tile) pairs; m-tiles of all experts are
-// numbered by an exclusive scan of ceil(M_e / 128) (prefill_tiles_kernel),
+// numbered by an exclusive scan of ceil(M_e / 128) and described one by one
+// (prefill_tiles_kernel), so a workgroup finds its tile with one load,
 // an expert's 32-row groups are dealt evenly over its m-tiles, and its
 // items are ordered n-tile major, so the m-tiles sharing a weight slice are
 // neighbours of similar size.  Work items are assigned XCD-major: the
