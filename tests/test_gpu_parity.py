@@ -115,6 +115,30 @@ def test_quant_rows_f32_every_value_of_three_bands_bit_exact(moe):
     assert bad.size == 0, (bad.size, x.reshape(-1)[bad[:8]], qc.reshape(-1)[bad[:8]], q_ref.reshape(-1)[bad[:8]])
 
 
+def test_quant_rows_f32_tiny_scales_bit_exact(moe):
+    """Blocks whose scale amax / 448 lies on either side of 2^-90, where the
+    quantizer switches from the reciprocal-and-correction quotient to the
+    division, down to subnormal inputs, and an all-zero block: codes and
+    scales against the oracle, bit for bit."""
+    rng = np.random.default_rng(9)
+    amaxes = [448 * 2.0 ** e for e in (-80, -89, -90, -91, -95, -110, -125)] + [1e-38, 3e-42, 0.0]
+    rows = []
+    for a in amaxes:
+        for _ in range(4):
+            v = (rng.uniform(-1.0, 1.0, 128) * a).astype(np.float32)
+            if a > 0:
+                v[rng.integers(0, 128)] = np.float32(a)
+            rows.append(v)
+    x = np.stack(rows).astype(np.float32)
+    q_ref, s_ref = oracle.quantize_rows(x)
+    q = torch.empty(x.shape, dtype=torch.uint8, device="cuda")
+    s = torch.empty((x.shape[0], 1), dtype=torch.float32, device="cuda")
+    moe.moe_quant_rows_f32(to_dev(x), q, s)
+    torch.cuda.synchronize()
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(q.cpu().numpy(), q_ref)
+
+
 @pytest.mark.parametrize("rows,cols", [(1, 128), (37, 1024), (4096, 7168)])
 def test_quant_act_random_bit_exact(moe, rows, cols):
     rng = np.random.default_rng(rows)
