@@ -40,8 +40,8 @@ METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
 TRAFFIC = {
     ("decode1", "ffn_decode_gateup"): {"bytes": 235600711, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
                                        "sha256_prefix": "1099a418eefb5545"},
-    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9794541638, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
-                                          "sha256_prefix": "0c65a5339a7de533"},
+    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9590282477, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
+                                          "sha256_prefix": "05820e98354c819e"},
 }
 
 
