@@ -340,13 +340,18 @@ __global__ __launch_bounds__(1024) void permute_scan_kernel(const int32_t* __res
   __shared__ int wave_tot[16];
   const int e = threadIdx.x;
   int tot = 0;
-  if (e < E)
+  // Unrolled by 8 so that eight independent loads go out before the first
+  // wait (a plain loop waited for every chunk's count in turn).
+  if (e < E) {
+#pragma unroll 8
     for (int c = 0; c < n_chunks; ++c) tot += counts[(int64_t)c * (E + 1) + e];
+  }
   int total_valid;
   const int excl = block_exclusive_scan(tot, wave_tot, &total_valid);
   if (e < E) {
     int run = excl;
     offsets[e] = run;
+#pragma unroll 8
     for (int c = 0; c < n_chunks; ++c) {
       const int64_t i = (int64_t)c * (E + 1) + e;
       base[i] = run;
