@@ -336,7 +336,9 @@ moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H, const uint
  * ws: device, moe_ffn_streamed_workspace(dims, T, chunk_tokens) bytes, 256-byte
  * aligned (it holds the fp32 expert rows of all T*k slots).  compute and copy
  * should be distinct streams for the copies to overlap the kernels.
- * Requires H % 256 == 0.
+ * Shapes: the PREFILL limits of moe_expert_ffn (H % 256 == 0,
+ * max(H, I) <= 24576, I * H < 2^31); others return
+ * MOE_ERR_UNSUPPORTED_SHAPE before anything is enqueued.
  */
 typedef struct moe_stream_ctx* moe_stream_ctx_t;
 moe_status_t moe_stream_ctx_create(int32_t ring_slots, moe_stream_ctx_t* out);

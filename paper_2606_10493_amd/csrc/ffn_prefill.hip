@@ -217,9 +217,13 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     // One unconditional 4-byte load per thread from a per-thread address
     // (threads 0-127: the row's sorted_src entry, clamped to the tile; the
     // others: their weight-scale entry, clamped to the table), so that no
-    // branch makes the weight loads below wait for it.
-    const int ti = tid < kBM ? min(tid, mc - 1) : min(tid - kBM, 2 * nb - 1);
-    const int h = ti / nb, b = ti - h * nb;
+    // branch makes the weight loads below wait for it.  Without sorted_src
+    // (DOWN) threads 0-127 read the tile's first weight-scale entry, whose
+    // value they ignore: the weight-scale index tw stays in [0, 2 nb) for
+    // every thread, so the address is inside the expert's scale rows.
+    const int ti = min(tid, mc - 1);
+    const int tw = tid < kBM ? 0 : min(tid - kBM, 2 * nb - 1);
+    const int h = tw / nb, b = tw - h * nb;
     const int64_t wrow = (int64_t)tile.e * (p.N / kBlock) + (GATEUP ? nt : 2 * nt + h);
     const float* sw_src = ((GATEUP && h) ? p.s1 : p.s0) + wrow * nb + b;
     const uint32_t* src = (tid < kBM && p.sorted_src) ? reinterpret_cast<const uint32_t*>(p.sorted_src + m0 + ti)

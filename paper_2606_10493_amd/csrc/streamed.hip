@@ -42,6 +42,7 @@ moe_status_t run_ffn_prefill_view(const moe_dims_t& d, int64_t max_mtiles, int32
                                   const uint8_t* w_down, const float* s_down, float* y_rows, uint8_t* qh, float* sh,
                                   int32_t* tiles, hipStream_t stream);
 size_t prefill_tiles_bytes(int64_t n_experts, int64_t max_mtiles);
+moe_status_t prefill_shape_check(const moe_dims_t& d);
 
 namespace {
 
@@ -143,6 +144,9 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
   if (d.hidden % 256 || d.inter % kBlock)
     return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_ffn_streamed: H must be a multiple of 256 and I of 128");
   if (!ctx) return fail(MOE_ERR_INVALID_ARG, "moe_ffn_streamed: null stream context");
+  // The prefill kernels' limits (K, LDS, expert matrix size), before anything is enqueued.
+  moe_status_t st0 = prefill_shape_check(d);
+  if (st0 != MOE_OK) return st0;
   if (T == 0) return MOE_OK;
   if ((int64_t)T * d.topk > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_ffn_streamed: T*k overflows");
   if (!x_bf16 || !topk_ids || !topk_w || !host_w_gate || !host_s_gate || !host_w_up || !host_s_up || !host_w_down ||
