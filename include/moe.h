@@ -263,6 +263,30 @@ moe_status_t moe_ffn_layer(moe_dims_t dims, int32_t T, moe_regime_t regime, cons
                            void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * moe_ffn_layer for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same call without the workspace arguments.  The layer's intermediate
+ * tensors live in a device array of MOE_NOALLOC_SCRATCH_BYTES bytes inside
+ * the library, one per GPU, held until the process ends; its device address
+ * is looked up on the first call on each device.  The call allocates and
+ * frees nothing and its results are bit-identical to moe_ffn_layer's.
+ * A call whose moe_ffn_layer_workspace(dims, T, regime) exceeds
+ * MOE_NOALLOC_SCRATCH_BYTES returns MOE_ERR_WORKSPACE before anything is
+ * enqueued (DeepSeek-V3 shapes fit up to 64 decode tokens, or 128 prefill
+ * tokens).  Other arguments, errors and T == 0 as in moe_ffn_layer.
+ * All calls on one GPU share its scratch array, which keeps the last call's
+ * contents (nothing in it needs clearing): calls that may overlap on one GPU
+ * (different streams, or host threads without ordering) race.
+ */
+#define MOE_NOALLOC_SCRATCH_BYTES (32u << 20)
+moe_status_t moe_ffn_layer_noalloc(moe_dims_t dims, int32_t T, moe_regime_t regime, const uint16_t* x_bf16,
+                                   const int32_t* topk_ids, const float* topk_w,
+                                   const uint8_t* w_gate, const float* s_gate,
+                                   const uint8_t* w_up, const float* s_up,
+                                   const uint8_t* w_down, const float* s_down,
+                                   uint16_t* out_bf16, int32_t* dev_status, hipStream_t stream);
+
+/*
  * Router (gate): the step before moe_permute.  The paper's Background on
  * Mixture-of-Experts names top-k and grouped top-k gating and SmallEP runs
  * the gate locally before sorting tokens; it fixes no formula, so the rule

@@ -14,7 +14,8 @@ import os
 from ._lib import (  # noqa: F401
     LIB_PATH, MoEError, lib, MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED_SHAPE,
     MOE_ERR_WORKSPACE, MOE_ERR_HIP, MOE_REGIME_AUTO, MOE_REGIME_DECODE, MOE_REGIME_PREFILL,
-    MOE_DEV_BAD_EXPERT_ID, MOE_DEV_DUP_EXPERT_ID, MOE_DECODE_MAX_TOKENS, MoeDims, MoeRouterCfg,
+    MOE_DEV_BAD_EXPERT_ID, MOE_DEV_DUP_EXPERT_ID, MOE_DECODE_MAX_TOKENS, MOE_NOALLOC_SCRATCH_BYTES, MoeDims,
+    MoeRouterCfg,
     EXPORTED_SYMBOLS,
 )
 from ._lib import check as _check
@@ -172,6 +173,19 @@ def moe_ffn_layer(dims: MoeDims, T: int, regime: int, x_bf16, topk_ids, topk_w, 
     _check(lib.moe_ffn_layer(dims, T, regime, _ptr(x_bf16), _ptr(topk_ids), _ptr(topk_w), _ptr(w_gate),
                              _ptr(s_gate), _ptr(w_up), _ptr(s_up), _ptr(w_down), _ptr(s_down), _ptr(out_bf16),
                              _ptr(dev_status), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def moe_ffn_layer_noalloc(dims: MoeDims, T: int, regime: int, x_bf16, topk_ids, topk_w, w_gate, s_gate, w_up, s_up,
+                          w_down, s_down, out_bf16, dev_status=None, stream=None):
+    """moe_ffn_layer with the library's per-GPU scratch array instead of a workspace (see include/moe.h)."""
+    for t, nb, n in ((x_bf16, 2, "x_bf16"), (topk_ids, 4, "topk_ids"), (topk_w, 4, "topk_w"),
+                     (w_gate, 1, "w_gate"), (s_gate, 4, "s_gate"), (w_up, 1, "w_up"), (s_up, 4, "s_up"),
+                     (w_down, 1, "w_down"), (s_down, 4, "s_down"), (out_bf16, 2, "out_bf16"),
+                     (dev_status, 4, "dev_status")):
+        _need(t, nb, n)
+    _check(lib.moe_ffn_layer_noalloc(dims, T, regime, _ptr(x_bf16), _ptr(topk_ids), _ptr(topk_w), _ptr(w_gate),
+                                     _ptr(s_gate), _ptr(w_up), _ptr(s_up), _ptr(w_down), _ptr(s_down),
+                                     _ptr(out_bf16), _ptr(dev_status), _stream(stream)))
 
 
 class StreamContext:

@@ -17,6 +17,8 @@ MOE_REGIME_DECODE = 1
 MOE_REGIME_PREFILL = 2
 MOE_DECODE_MAX_TOKENS = 64
 
+MOE_NOALLOC_SCRATCH_BYTES = 32 << 20
+
 MOE_DEV_BAD_EXPERT_ID = 1
 MOE_DEV_DUP_EXPERT_ID = 2
 
@@ -67,6 +69,7 @@ _SIGS = {
     "moe_combine": (_ST, [_P, _P, _P, _I, _I, _I, _P, _P]),
     "moe_ffn_layer_workspace": (_S, [MoeDims, _I, _ST]),
     "moe_ffn_layer": (_ST, [MoeDims, _I, _ST, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "moe_ffn_layer_noalloc": (_ST, [MoeDims, _I, _ST, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "moe_expert_ffn_w8a16_workspace": (_S, [MoeDims, _I]),
     "moe_expert_ffn_w8a16": (_ST, [MoeDims, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "moe_router_workspace": (_S, [_I, _I, _I]),
