@@ -1,15 +1,21 @@
 #!/usr/bin/env python3
-"""Benchmark of one routed-expert FP8 MoE layer (DeepSeek-V3 shape) on one MI355X.
+"""Benchmark of the routed-expert FP8 MoE layer (DeepSeek-V3 shape) on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload decode1]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload prefill32k_streamed] [--also LIST]
 
 A step is one pass of the whole path over one batch already resident in
-HBM: quantize -> permute -> expert FFN -> combine, as one moe_ffn_layer call
-(--unfused: the four calls moe_quant_act, moe_permute, moe_expert_ffn,
-moe_combine).  The
-default workload is DeepSeek-V3-shaped decode with one token (hidden 7168,
-expert intermediate 2048, 256 experts, top-8, FP8 e4m3 weights with
-128x128 fp32 block scales, synthetic data).  Decode steps rotate over
+HBM: quantize -> permute -> expert FFN -> combine.  The default workload is
+the largest single-GPU configuration: a 32768-token prefill of one
+DeepSeek-V3-shaped routed-expert layer (hidden 7168, expert intermediate
+2048, 256 experts, top-8, Zipf(0.8) routing, FP8 e4m3 weights with 128x128
+fp32 block scales, synthetic data) in 4096-token chunks, with the layer's
+11.27 GB of expert weights in pinned host memory streamed into a device
+ring on a copy stream while the expert kernels run (moe_ffn_streamed).
+The resident workloads (8192-token prefill chunk, batched decode at 64
+tokens, decode at 4 and 1 tokens, ...) are timed in the same run as one
+moe_ffn_layer call per step (--unfused: the four calls moe_quant_act,
+moe_permute, moe_expert_ffn, moe_combine) and reported under "also", each
+with the roofline of its own dominant kernel.  Decode steps rotate over
 several independently drawn weight layers so that repeated steps cannot be
 served from the 256 MB Infinity Cache.
 
@@ -32,16 +38,16 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 FP8_PEAK_TFLOPS = 5000.0     # MI355X dense FP8 MFMA
 METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
+DEFAULT_WORKLOAD = "prefill32k_streamed"
+DEFAULT_ALSO = "prefill8k,decode64_zipf,decode4,decode1,decode1_w8a16,router"
 
 # HBM bytes per launch of a kernel, from rocprofv3 FETCH_SIZE and WRITE_SIZE
 # runs scaled by a plain 1 GiB copy (FETCH x2.000, WRITE x1.000), recorded in
-# profiles/*_hbm_traffic.md.  Valid only while the kernel's source file is the
-# one measured (sha256 prefix).
+# the *_hbm_traffic summaries under profiles/.  Valid only while the kernel's
+# source file is the one measured (sha256 prefix).
 TRAFFIC = {
     ("decode1", "ffn_decode_gateup"): {"bytes": 235600711, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
                                        "sha256_prefix": "1099a418eefb5545"},
-    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9590282477, "source": "paper_2606_10493_amd/csrc/ffn_prefill.hip",
-                                          "sha256_prefix": "05820e98354c819e"},
 }
 
 
@@ -59,16 +65,16 @@ def measured_traffic(workload, kernel):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="decode1")
-    ap.add_argument("--layers", type=int, default=0, help="weight layers to rotate over (0: auto)")
-    ap.add_argument("--also", default="decode4,decode1_w8a16,router",
-                    help="comma list of extra workloads (summary only); NAME_w8a16 runs the W8A16 decode FFN, "
-                         "router times the gate on the main workload's tokens")
+    ap.add_argument("--steps", type=int, default=0, help="timed steps (0: 10 for streamed, 50 for resident)")
+    ap.add_argument("--warmup", type=int, default=0, help="warm-up steps (0: 2 for streamed, 10 for resident)")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--layers", type=int, default=0, help="decode: weight layers to rotate over (0: 4)")
+    ap.add_argument("--also", default=DEFAULT_ALSO,
+                    help="comma list of extra resident workloads (each with its own roofline); NAME_w8a16 runs "
+                         "the W8A16 decode FFN, router times the gate on the main workload's tokens")
     ap.add_argument("--unfused", action="store_true",
-                    help="run the layer as four library calls (quantize, permute, expert FFN, combine) instead "
-                         "of one moe_ffn_layer call")
+                    help="run resident layers as four library calls (quantize, permute, expert FFN, combine) "
+                         "instead of one moe_ffn_layer call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -78,6 +84,23 @@ def parse():
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+class LayerCache:
+    """Device weight layers (packed e4m3 + scales) by layer index.  Weights depend
+    only on (seed, layer, expert, matrix), so every DeepSeek-V3-shaped workload
+    shares them."""
+
+    def __init__(self, moe, torch, synth):
+        self.moe, self.torch, self.synth = moe, torch, synth
+        self.layers = {}
+
+    def get(self, w, layer):
+        key = (w.hidden, w.inter, w.n_experts, w.seed, layer)
+        if key not in self.layers:
+            log(f"drawing and quantizing weight layer {layer} on the GPU")
+            self.layers[key] = make_layer(self.moe, self.torch, self.synth, w, layer)
+        return self.layers[key]
 
 
 def make_layer(moe, torch, synth, w, layer):
@@ -117,20 +140,32 @@ def algorithmic(w, ids):
     }
 
 
-def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache, w8a16=False, fused=True):
+def profile_steps(moe, torch, step, n_steps, per_step):
+    """Kernel durations of n_steps steps from the library's launch events:
+    {name: (launches, total ms)}."""
+    moe.moe_profile_begin(per_step * n_steps)
+    for i in range(n_steps):
+        step(i)
+    prof = moe.moe_profile_end()
+    torch.cuda.synchronize()
+    kern = {}
+    for kname, kms in prof:
+        n, tot = kern.get(kname, (0, 0.0))
+        kern[kname] = (n + 1, tot + kms)
+    return kern
+
+
+def time_resident(moe, torch, synth, cache, name, steps, warmup, layers_n, w8a16=False, fused=True):
     import numpy as np
     w = synth.WORKLOADS[name]
     if w.chunk_tokens:
-        raise SystemExit(f"{name}: the streamed workload is not benchmarked by this script yet")
+        raise SystemExit(f"{name}: a streamed workload, not a resident one")
     x = synth.activations(w)
     ids, wts = synth.routing(w)
     dx = torch.from_numpy(x.view(np.int16)).cuda()
     dids = torch.from_numpy(ids).cuda()
     dw = torch.from_numpy(wts).cuda()
-    while len(layers_cache) < layers_n:
-        log(f"drawing and quantizing weight layer {len(layers_cache)} on the GPU")
-        layers_cache.append(make_layer(moe, torch, synth, w, len(layers_cache)))
-    layers = layers_cache[:layers_n]
+    layers = [cache.get(w, l) for l in range(layers_n)]
     buf = moe.MoELayerBuffers(w.hidden, w.inter, w.n_experts, w.topk, w.tokens, with_status=False, w8a16=w8a16,
                               fused=fused and not w8a16)
     stream = torch.cuda.current_stream()
@@ -148,23 +183,68 @@ def time_workload(moe, torch, synth, name, steps, warmup, layers_n, layers_cache
     ev1.record(stream)
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / steps
-
     # Per-kernel durations: the same steps again with the library's launch events.
-    moe.moe_profile_begin(16 * steps)
-    for i in range(steps):
-        step(i)
-    prof = moe.moe_profile_end()
-    torch.cuda.synchronize()
-    kern = {}
-    for kname, kms in prof:
-        kern.setdefault(kname, []).append(kms)
-    # Per step: a kernel launched more than once per step (decode launches per
-    # expert row-count class) is summed over the step's launches.
-    kern_us = {kname: 1000.0 * sum(v) / steps for kname, v in kern.items()}
+    kern = profile_steps(moe, torch, step, steps, 16)
     out = buf.out.cpu().numpy()
     if not np.all(np.isfinite((out.view(np.uint16).astype(np.uint32) << 16).view(np.float32))):
         raise RuntimeError("non-finite output")
-    return w, ids, wts, x, ms, kern_us
+    return w, ids, wts, x, ms, kern
+
+
+def decode_roofline(alg, kern, steps, workload):
+    """Decode gate/up GEMV against HBM (per step: the launches of its row-count classes)."""
+    dom = "ffn_decode_gateup"
+    n, tot_ms = kern[dom]
+    us = 1000.0 * tot_ms / steps
+    achieved = alg["gateup_bytes"] / (us * 1e-6) / 1e9
+    return {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(workload, dom),
+            "per_launch": {"algorithmic_bytes_per_step": alg["gateup_bytes"], "launches_per_step": n // steps,
+                           "us_per_step": round(us, 2)}}
+
+
+def prefill_roofline(flops_total, kern, dom, workload, launches_note=""):
+    """A prefill GEMM kernel against dense FP8 MFMA: algorithmic FLOPs per launch
+    over its mean launch duration."""
+    n, tot_ms = kern[dom]
+    avg_us = 1000.0 * tot_ms / n
+    per_launch = flops_total / n
+    achieved = per_launch / (avg_us * 1e-6) / 1e12
+    return {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": FP8_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4), "traffic": measured_traffic(workload, dom),
+            "per_launch": {"launches": n, "algorithmic_flops": round(per_launch), "avg_us": round(avg_us, 2),
+                           **({"note": launches_note} if launches_note else {})}}
+
+
+def resident_summary(moe, torch, synth, cache, extra, steps, warmup, layers_n, fused):
+    base_name, w8a16 = (extra[:-len("_w8a16")], True) if extra.endswith("_w8a16") else (extra, False)
+    w0 = synth.WORKLOADS[base_name]
+    decode = w0.tokens <= moe.MOE_DECODE_MAX_TOKENS
+    n_layers = layers_n if decode else 1
+    w, ids, _, _, ms, kern = time_resident(moe, torch, synth, cache, base_name, steps, warmup, n_layers,
+                                           w8a16=w8a16, fused=fused)
+    alg = algorithmic(w, ids)
+    kern_us = {k: round(1000.0 * tot / steps, 2) for k, (n, tot) in kern.items()}
+    res = {"tokens_per_s": round(w.tokens / (ms / 1000.0), 1), "ms_per_step": round(ms, 4),
+           "tokens": w.tokens, "routing": w.routing + (f"({w.zipf_s})" if w.routing == "zipf" else ""),
+           "active_experts": alg["active_experts"],
+           "layer_weight_GBps": round(alg["layer_weight_bytes"] / (ms * 1e-3) / 1e9, 1),
+           "weight_layers_rotated": n_layers, "kernel_us_per_step": kern_us}
+    if w8a16:
+        dom = "ffn_decode_w8a16_gateup"
+        n, tot = kern[dom]
+        us = 1000.0 * tot / steps
+        ach = alg["gateup_bytes"] / (us * 1e-6) / 1e9   # same weight bytes; activations counted as in W8A8
+        res["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                           "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+    elif decode:
+        res["roofline"] = decode_roofline(alg, kern, steps, base_name)
+        res["layer_frac_hbm"] = round(alg["layer_weight_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+    else:
+        res["roofline"] = prefill_roofline(alg["gateup_flops"] * steps, kern, "ffn_prefill_gateup", base_name)
+        res["roofline_down"] = prefill_roofline(alg["down_flops"] * steps, kern, "ffn_prefill_down", base_name)
+        res["layer_TFLOPs"] = round((alg["gateup_flops"] + alg["down_flops"]) / (ms * 1e-3) / 1e12, 1)
+    return res
 
 
 def time_router(moe, torch, synth, w, steps, warmup):
@@ -182,24 +262,17 @@ def time_router(moe, torch, synth, w, steps, warmup):
                      device="cuda")
     groups = 8 if w.n_experts % 8 == 0 and w.n_experts >= 16 else 1
 
-    def call():
+    def call(_i=0):
         moe.moe_router(dx, dwr, db, ids, wts, groups, min(4, groups), 1.0, ws)
 
     for _ in range(warmup):
         call()
     torch.cuda.synchronize()
-    moe.moe_profile_begin(4 * steps)
-    for _ in range(steps):
-        call()
-    prof = moe.moe_profile_end()
-    torch.cuda.synchronize()
-    kern = {}
-    for kname, kms in prof:
-        kern.setdefault(kname, []).append(kms)
-    return {kk: round(1000.0 * sum(v) / len(v), 2) for kk, v in kern.items()}
+    kern = profile_steps(moe, torch, call, steps, 4)
+    return {kk: round(1000.0 * tot / n, 2) for kk, (n, tot) in kern.items()}
 
 
-def time_streamed(moe, torch, synth, name, steps, warmup):
+def time_streamed(moe, torch, synth, cache, name, steps, warmup):
     """Stream-loaded layers: weights in pinned host memory, streamed through a
     ring of expert slots (all experts of a layer by default).  With several
     layers (stream-loading across a stack, each layer with its own weights and
@@ -212,14 +285,16 @@ def time_streamed(moe, torch, synth, name, steps, warmup):
     routes = [synth.routing(w, layer=l) for l in range(n_layers)]
     host_layers = []
     for l in range(n_layers):
-        log(f"drawing and quantizing weight layer {l} on the GPU, then pinning a host copy")
-        dev_layer = make_layer(moe, torch, synth, w, l)
+        dev_layer = cache.get(w, l)
+        log(f"pinning a host copy of weight layer {l}")
         host = []
         for t in dev_layer:
             h = torch.empty(t.shape, dtype=t.dtype, pin_memory=True)
             h.copy_(t)
             host.append(h)
         host_layers.append(tuple(host))
+        if l > 0:   # layer 0 stays resident for the resident workloads of the same run
+            del cache.layers[(w.hidden, w.inter, w.n_experts, w.seed, l)]
         del dev_layer
         torch.cuda.empty_cache()
     dims = moe.MoeDims(w.hidden, w.inter, w.n_experts, w.topk)
@@ -237,7 +312,7 @@ def time_streamed(moe, torch, synth, name, steps, warmup):
     compute = torch.cuda.current_stream()
     copy = torch.cuda.Stream()
 
-    def step():
+    def step(_i=0):
         inp = dx
         for l in range(n_layers):
             moe.moe_ffn_streamed(dims, w.chunk_tokens, inp, dids[l], dws[l], host_layers[l], ring, ring_s, ctx,
@@ -276,24 +351,20 @@ def time_streamed(moe, torch, synth, name, steps, warmup):
                                                                non_blocking=True)
         compute.wait_stream(copy)
 
-    copy_ms = timed(copies, 1)
-    # Kernel durations of one step with the library's launch events.
-    moe.moe_profile_begin(20000 * n_layers)
-    step()
-    prof = moe.moe_profile_end()
-    torch.cuda.synchronize()
-    kern = {}
-    for kname, kms in prof:
-        kern.setdefault(kname, []).append(kms)
-    kern_total_ms = {k: sum(v) for k, v in kern.items()}
+    copy_ms = [timed(copies, 1) for _ in range(3)]
+    # Kernel durations of the timed number of steps with the library's launch events.
+    kern = profile_steps(moe, torch, step, steps, 4000 * n_layers)
     ctx.close()
     h2d_bytes = sum(t.numel() * t.element_size() for host in host_layers for t in host)
     ids_all = np.concatenate([ids for ids, _ in routes])
-    return w, ids_all, routes[0][1], x, ms, copy_ms, h2d_bytes, kern_total_ms
+    out0 = outs[(n_layers - 1) % 2].cpu().numpy()
+    if not np.all(np.isfinite((out0.view(np.uint16).astype(np.uint32) << 16).view(np.float32))):
+        raise RuntimeError("non-finite output")
+    return w, ids_all, routes[0][1], x, ms, copy_ms, h2d_bytes, kern
 
 
-def cpu_baseline(torch, synth, w, x, ids, wts, budget_s):
-    """The oracle as it stands, on a bounded sample of the workload."""
+def cpu_baseline(torch, synth, w, x, ids, wts, budget_s, tokens):
+    """The oracle as it stands, on a bounded sample of the workload (the given tokens)."""
     import numpy as np
     import oracle
     try:
@@ -302,10 +373,6 @@ def cpu_baseline(torch, synth, w, x, ids, wts, budget_s):
     except Exception:  # pragma: no cover
         blas_threads = os.cpu_count() or 1
     k = w.topk
-    if w.tokens <= 64:
-        tokens = list(range(w.tokens))
-    else:
-        tokens = list(range(16))
     experts = sorted(set(ids[tokens].reshape(-1).tolist()))
     ow = {}
     for e in experts:   # weight preparation (not timed): re-drawn fp32, quantized by the oracle
@@ -332,9 +399,10 @@ def cpu_baseline(torch, synth, w, x, ids, wts, budget_s):
         if el >= budget_s:
             break
     return {"value": done / el, "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
-            "sample": f"{len(tokens)} token(s) of the workload ({len(experts)} experts), full layer path "
-                      f"(quantize, permute, expert FFN, combine) repeated {done // len(tokens)} times "
-                      f"in {el:.1f} s; weight quantization excluded"}
+            "host_cpu_count": os.cpu_count(), "blas_threads": int(blas_threads),
+            "sample": f"token(s) {tokens[0]}..{tokens[-1]} of the {w.tokens}-token workload ({len(experts)} experts): "
+                      f"the full layer path (quantize, permute, expert FFN, combine) repeated "
+                      f"{done // len(tokens)} times in {el:.1f} s; weight quantization excluded"}
 
 
 def main():
@@ -344,7 +412,7 @@ def main():
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
               "the multi-GPU expert-parallel path is not built", file=sys.stderr)
         sys.exit(2)
-    import numpy as np
+    import numpy as np  # noqa: F401
     import torch
 
     import paper_2606_10493_amd as moe
@@ -362,107 +430,101 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 5}))
         return
+    cache = LayerCache(moe, torch, synth)
     w0 = synth.WORKLOADS[args.workload]
+    layers_n = args.layers or 4
     if w0.chunk_tokens:
-        return main_streamed(args, moe, torch, synth)
-    decode = w0.tokens <= moe.MOE_DECODE_MAX_TOKENS
-    layers_n = args.layers or (4 if decode else 1)
-    cache = []
-    w, ids, wts, x, ms, kern_us = time_workload(moe, torch, synth, args.workload, args.steps, args.warmup,
-                                                layers_n, cache, fused=not args.unfused)
-    alg = algorithmic(w, ids)
-    tok_s = w.tokens / (ms / 1000.0)
-    if decode:
-        dom = "ffn_decode_gateup"
-        us = kern_us[dom]
-        achieved = alg["gateup_bytes"] / (us * 1e-6) / 1e9
-        roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": measured_traffic(args.workload, dom),
-                "per_launch": {"algorithmic_bytes": alg["gateup_bytes"], "avg_us": round(us, 2)}}
+        steps, warmup = args.steps or 10, args.warmup or 2
+        res, w, x, ids, wts = main_streamed(args, moe, torch, synth, cache, steps, warmup)
     else:
-        dom = "ffn_prefill_gateup"
-        us = kern_us[dom]
-        achieved = alg["gateup_flops"] / (us * 1e-6) / 1e12
-        roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": FP8_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
-                "traffic": measured_traffic(args.workload, dom),
-                "per_launch": {"algorithmic_flops": alg["gateup_flops"], "avg_us": round(us, 2)}}
-    layer_gbs = alg["layer_weight_bytes"] / (ms * 1e-3) / 1e9
-    layer_tflops = (alg["gateup_flops"] + alg["down_flops"]) / (ms * 1e-3) / 1e12
+        steps, warmup = args.steps or 50, args.warmup or 10
+        res, w, x, ids, wts = main_resident(args, moe, torch, synth, cache, steps, warmup, layers_n)
     also = {}
+    r_steps, r_warm = args.steps or 50, args.warmup or 10
     for extra in [a for a in args.also.split(",") if a and a != args.workload]:
+        log(f"also: {extra}")
         if extra == "router":
-            also["router"] = {"tokens": w.tokens, "kernel_us": time_router(moe, torch, synth, w, args.steps,
-                                                                          args.warmup)}
+            also["router"] = {"tokens": w.tokens, "kernel_us": time_router(moe, torch, synth, w, r_steps, r_warm)}
             continue
-        base_name, w8a16 = (extra[:-len("_w8a16")], True) if extra.endswith("_w8a16") else (extra, False)
-        try:
-            we, ide, _, _, mse, kue = time_workload(moe, torch, synth, base_name, args.steps, args.warmup,
-                                                    layers_n, cache, w8a16=w8a16, fused=not args.unfused)
-        except SystemExit as exc:
-            also[extra] = {"skipped": str(exc)}
+        base = extra[:-len("_w8a16")] if extra.endswith("_w8a16") else extra
+        if synth.WORKLOADS[base].chunk_tokens:
+            also[extra] = {"skipped": "streamed workloads run as the main --workload"}
             continue
-        ae = algorithmic(we, ide)
-        also[extra] = {"tokens_per_s": round(we.tokens / (mse / 1000.0), 1), "ms_per_step": round(mse, 4),
-                       "layer_weight_GBps": round(ae["layer_weight_bytes"] / (mse * 1e-3) / 1e9, 1),
-                       "active_experts": ae["active_experts"],
-                       "kernel_us": {kk: round(v, 2) for kk, v in kue.items()}}
+        also[extra] = resident_summary(moe, torch, synth, cache, extra, r_steps, r_warm, layers_n,
+                                       fused=not args.unfused)
+    res["also"] = also
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        cpu = cpu_baseline(torch, synth, w, x, ids, wts, args.cpu_seconds)
+        sample = list(range(w.tokens)) if w.tokens <= 4 else [0]
+        cpu = cpu_baseline(torch, synth, w, x, ids, wts, args.cpu_seconds, sample)
+    res["cpu_baseline"] = cpu
+    print(json.dumps(res), flush=True)
+
+
+def main_resident(args, moe, torch, synth, cache, steps, warmup, layers_n):
+    w0 = synth.WORKLOADS[args.workload]
+    decode = w0.tokens <= moe.MOE_DECODE_MAX_TOKENS
+    n_layers = layers_n if decode else 1
+    w, ids, wts, x, ms, kern = time_resident(moe, torch, synth, cache, args.workload, steps, warmup, n_layers,
+                                             fused=not args.unfused)
+    alg = algorithmic(w, ids)
+    if decode:
+        roof = decode_roofline(alg, kern, steps, args.workload)
+    else:
+        roof = prefill_roofline(alg["gateup_flops"] * steps, kern, "ffn_prefill_gateup", args.workload)
+    layer_gbs = alg["layer_weight_bytes"] / (ms * 1e-3) / 1e9
+    layer_tflops = (alg["gateup_flops"] + alg["down_flops"]) / (ms * 1e-3) / 1e12
     res = {
-        "metric": METRIC, "value": round(tok_s, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "metric": METRIC, "value": round(w.tokens / (ms / 1000.0), 2), "unit": "tokens/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
         "config": {"workload": args.workload, "hidden": w.hidden, "inter": w.inter, "n_experts": w.n_experts,
                    "topk": w.topk, "tokens": w.tokens, "routing": w.routing,
-                   "weight_layers_rotated": layers_n, "active_experts": alg["active_experts"],
+                   "weight_layers_rotated": n_layers, "active_experts": alg["active_experts"],
                    "entry": "four calls" if args.unfused else "moe_ffn_layer"},
         "layer": {"weight_GBps": round(layer_gbs, 1), "frac_hbm": round(layer_gbs / HBM_PEAK_GBS, 4),
                   "TFLOPs": round(layer_tflops, 2)},
         "roofline": roof,
-        "kernel_us": {kk: round(v, 2) for kk, v in kern_us.items()},
-        "cpu_baseline": cpu,
-        "also": also,
+        "kernel_us_per_step": {k: round(1000.0 * tot / steps, 2) for k, (n, tot) in kern.items()},
     }
-    print(json.dumps(res), flush=True)
+    return res, w, x, ids, wts
 
 
-def main_streamed(args, moe, torch, synth):
-    w, ids, wts, x, ms, copy_ms, h2d_bytes, kern_ms = time_streamed(moe, torch, synth, args.workload, args.steps,
-                                                                     args.warmup)
+def main_streamed(args, moe, torch, synth, cache, steps, warmup):
+    w, ids, wts, x, ms, copy_ms, h2d_bytes, kern = time_streamed(moe, torch, synth, cache, args.workload, steps,
+                                                                 warmup)
     n_layers = max(1, w.layers)
     alg = algorithmic(w.with_tokens(w.tokens * n_layers), ids)
-    gu_ms = kern_ms.get("ffn_prefill_gateup", 0.0)
-    dn_ms = kern_ms.get("ffn_prefill_down", 0.0)
-    gemm_tflops = (alg["gateup_flops"] + alg["down_flops"]) / ((gu_ms + dn_ms) * 1e-3) / 1e12
-    h2d_gbs = h2d_bytes / (copy_ms * 1e-3) / 1e9
-    cpu = None
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle on a bounded sample")
-        cpu = cpu_baseline(torch, synth, w, x, ids, wts, args.cpu_seconds)
+    gu_n, gu_ms = kern.get("ffn_prefill_gateup", (0, 0.0))
+    dn_n, dn_ms = kern.get("ffn_prefill_down", (0, 0.0))
+    copy_best = min(copy_ms)
+    h2d_gbs = h2d_bytes / (copy_best * 1e-3) / 1e9
+    note = "launches per step: one per expert group (over all 4096-token chunks)"
+    roof = prefill_roofline(alg["gateup_flops"] * steps, kern, "ffn_prefill_gateup", args.workload, note)
+    roof_dn = prefill_roofline(alg["down_flops"] * steps, kern, "ffn_prefill_down", args.workload, note)
     res = {
         "metric": METRIC, "value": round(w.tokens / (ms / 1000.0), 1), "unit": "tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": True,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
         "config": {"workload": args.workload, "hidden": w.hidden, "inter": w.inter, "n_experts": w.n_experts,
                    "topk": w.topk, "tokens": w.tokens, "chunk_tokens": w.chunk_tokens, "routing": w.routing,
-                   "zipf_s": w.zipf_s, "layers": n_layers, "ring_slots": w.ring_slots or w.n_experts},
-        "streaming": {"h2d_bytes": h2d_bytes, "copy_only_ms": round(copy_ms, 3),
+                   "zipf_s": w.zipf_s, "layers": n_layers, "ring_slots": w.ring_slots or w.n_experts,
+                   "entry": "moe_ffn_streamed"},
+        "streaming": {"h2d_bytes": h2d_bytes, "copy_only_ms": [round(c, 3) for c in copy_ms],
                       "h2d_GBps_copy_only": round(h2d_gbs, 2),
                       "h2d_GBps_in_layer": round(h2d_bytes / (ms * 1e-3) / 1e9, 2),
+                      "frac_of_copy_only": round(copy_best / ms, 4),
                       "layer_tokens_per_s": round(n_layers * w.tokens / (ms / 1000.0), 1),
-                      "exposed_compute_ms": round(ms - copy_ms, 3),
-                      "gemm_kernel_ms": round(gu_ms + dn_ms, 3)},
-        "roofline": {"kernel": "ffn_prefill_gateup + ffn_prefill_down (per expert and chunk)", "bound": "mfma",
-                     "achieved": round(gemm_tflops, 1), "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4), "traffic": None},
-        "kernel_ms_per_step": {k: round(v, 3) for k, v in kern_ms.items()},
-        "cpu_baseline": cpu,
+                      "exposed_compute_ms": round(ms - copy_best, 3),
+                      "gemm_kernel_ms_per_step": round((gu_ms + dn_ms) / steps, 3),
+                      "gemm_TFLOPs": round((alg["gateup_flops"] + alg["down_flops"]) /
+                                           ((gu_ms + dn_ms) / steps * 1e-3) / 1e12, 1)},
+        "roofline": roof,
+        "roofline_down": roof_dn,
+        "kernel_ms_per_step": {k: round(tot / steps, 3) for k, (n, tot) in kern.items()},
     }
-    print(json.dumps(res), flush=True)
+    return res, w, x, ids, wts
 
 
 if __name__ == "__main__":

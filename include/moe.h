@@ -179,7 +179,8 @@ moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t 
  * w_gate, w_up: device e4m3 [E, I, H]; s_gate, s_up: fp32 [E, I/128, H/128].
  * w_down: device e4m3 [E, H, I]; s_down: fp32 [E, H/128, I/128].
  * The three weight stacks are in the packed layout of moe_pack_weight
- * (the scales stay row-major).
+ * (the scales stay row-major).  The layout cannot be checked: row-major
+ * (unpacked) stacks, as a checkpoint stores them, give undefined results.
  * y_rows: device fp32 [T*k, H] in expert-sorted order.
  * ws: device workspace of moe_expert_ffn_workspace(dims, T, regime) bytes.
  * regime: see moe_regime_t; DECODE requires T <= MOE_DECODE_MAX_TOKENS.
@@ -344,7 +345,8 @@ moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H, const uint
  *
  * host_w_*: pinned host e4m3 weights, packed as for moe_expert_ffn ([E,I,H]
  * for gate/up, [E,H,I] for down, each expert's matrix in the layout of
- * moe_pack_weight); host_s_*: pinned host fp32 scales.
+ * moe_pack_weight; row-major stacks give undefined results); host_s_*:
+ * pinned host fp32 scales.
  * dev_ring: device, moe_ring_bytes(dims, slots) bytes, three sub-rings
  * [slots][I*H] of W_gate, W_up and [slots][H*I] of W_down (slot s holds one
  * expert in each).  dev_ring_scales: device, moe_ring_scale_bytes(dims,

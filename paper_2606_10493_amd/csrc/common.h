@@ -255,6 +255,24 @@ void prof_after(hipStream_t s);
     ::moe::prof_after((STREAM));                                        \
   } while (0)
 
+// Expert-sorted rows of one prefill GEMM launch pair: n_chunks chunks of
+// tokens, each sorted by expert on its own; the launch covers n_units
+// consecutive experts (its weight stacks hold exactly those).  Chunk c's
+// offsets of those experts are offsets[c * off_stride + u], u = 0..n_units,
+// relative to the chunk's first sorted row c * chunk_rows; its sorted_src
+// entries are chunk-relative slots (token t - c * chunk_tokens).  A resident
+// layer is one chunk of all its experts.
+struct PrefillRows {
+  const int32_t* offsets;
+  int64_t off_stride;
+  int n_units, n_chunks;
+  int64_t chunk_rows;   // sorted rows per chunk (chunk_tokens * k)
+  int chunk_tokens;
+  int32_t tokens;       // activation rows of the gate/up projections (all chunks)
+  int64_t rows;         // sorted rows of all chunks (activation rows of the down projection)
+  int64_t max_mtiles;   // bound on the launch's 128-row m-tiles (sizes the grid and the descriptor table)
+};
+
 void set_error(const char* fmt, ...);
 moe_status_t fail(moe_status_t st, const char* fmt, ...);
 moe_status_t check_launch(const char* what);

@@ -71,14 +71,15 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 struct PrefillArgs {
   const uint8_t* a;           // e4m3 activations [a_rows, K]
   const float* sa;            // [a_rows, K/128]
-  const int32_t* sorted_src;  // GATEUP: A row of sorted row p = sorted_src[p] / topk; DOWN: NULL (A row = p)
+  const int32_t* sorted_src;  // GATEUP: A row of sorted row p = sorted_src[p] / topk (+ the chunk's first token); DOWN: NULL (A row = p)
   int topk;
   int a_rows;
-  const int32_t* offsets;     // [E+1]
-  const int32_t* mtile_start; // [E+1] exclusive scan of ceil(M_e/128)
+  const int32_t* mtile_start; // [n_seg+1] exclusive scan of the segments' m-tile counts
   const int4* desc;           // [max_mtiles] m-tile block descriptors (prefill_tiles_kernel)
   int64_t max_mtiles;         // bound on the m-tiles (sizes desc)
-  int E;
+  int n_seg;                  // segments: (expert, chunk) pairs, seg = expert * n_chunks + chunk
+  int n_chunks;               // row chunks (1 for a resident layer)
+  int chunk_tokens;           // GATEUP: tokens per chunk (the token of a row of chunk c is sorted_src / topk + c * chunk_tokens)
   const uint8_t* w0;          // GATEUP: W_gate [E, N, K]; DOWN: W_down [E, N, K]; packed tiles
   const float* s0;
   const uint8_t* w1;          // GATEUP: W_up, packed tiles
@@ -90,26 +91,45 @@ struct PrefillArgs {
   float* sh;                  // GATEUP output [rows, N/128]
 };
 
-// mtile_start = exclusive scan of the experts' m-tile counts, and for every
-// m-tile index b in [mtile_start[e], mtile_start[e+1]) the descriptor
-// desc[b] = (e, mtile_start[e], offsets[e], offsets[e+1]), from which a GEMM
-// workgroup derives its tile with one uniform load (no search over experts).
-__global__ __launch_bounds__(1024) void prefill_tiles_kernel(const int32_t* __restrict__ offsets, int E,
+// The rows of a launch form segments, one per (expert, chunk) pair: segment
+// seg = u * n_chunks + c holds the rows of expert u in chunk c, rows
+// [c * chunk_rows + offsets[c * off_stride + u], c * chunk_rows +
+// offsets[c * off_stride + u + 1]) of the launch's sorted order (a resident
+// layer is one chunk, so a segment is an expert).  Segments are numbered
+// expert-major, so the chunks of one expert (which read the same weights)
+// are neighbours.  mtile_start = exclusive scan of the segments' m-tile
+// counts ceil(M / 128), and for every m-tile index b in [mtile_start[seg],
+// mtile_start[seg+1]) the descriptor desc[b] = (seg, mtile_start[seg], row0,
+// row1), from which a GEMM workgroup derives its tile with one uniform load
+// (no search).  Segments are taken 1024 at a time with a running total.
+__global__ __launch_bounds__(1024) void prefill_tiles_kernel(const int32_t* __restrict__ offsets, int64_t off_stride,
+                                                             int n_units, int n_chunks, int64_t chunk_rows,
                                                              int32_t* __restrict__ mtile_start,
                                                              int4* __restrict__ desc, int64_t max_mtiles) {
   __shared__ int wave_tot[16];
-  const int e = threadIdx.x;
-  const int o0 = e < E ? offsets[e] : 0, o1 = e < E ? offsets[e + 1] : 0;
-  const int c = (e < E && o1 > o0) ? (o1 - o0 + kBM - 1) / kBM : 0;
-  int total;
-  const int excl = block_exclusive_scan(c, wave_tot, &total);
-  if (e < E) mtile_start[e] = excl;
-  if (e == 0) mtile_start[E] = total;
-  for (int b = excl; b < excl + c && b < max_mtiles; ++b) desc[b] = make_int4(e, excl, o0, o1);
+  const int n_seg = n_units * n_chunks;
+  int carry = 0;
+  for (int base = 0; base < n_seg; base += 1024) {
+    const int seg = base + (int)threadIdx.x;
+    int o0 = 0, o1 = 0;
+    if (seg < n_seg) {
+      const int u = seg / n_chunks, c = seg - u * n_chunks;
+      const int32_t* oc = offsets + c * off_stride;
+      o0 = (int)(c * chunk_rows) + oc[u];
+      o1 = (int)(c * chunk_rows) + oc[u + 1];
+    }
+    const int cnt = (seg < n_seg && o1 > o0) ? (o1 - o0 + kBM - 1) / kBM : 0;
+    int total;
+    const int excl = carry + block_exclusive_scan(cnt, wave_tot, &total);
+    if (seg < n_seg) mtile_start[seg] = excl;
+    for (int b = excl; b < excl + cnt && b < max_mtiles; ++b) desc[b] = make_int4(seg, excl, o0, o1);
+    carry += total;
+  }
+  if (threadIdx.x == 0) mtile_start[n_seg] = carry;
 }
 
-// The tiles workspace: mtile_start [E+1] (padded to 16 bytes), then desc [max_mtiles].
-size_t tiles_desc_offset(int64_t n_experts) { return ((size_t)(n_experts + 1) * sizeof(int32_t) + 15) & ~(size_t)15; }
+// The tiles workspace: mtile_start [n_seg+1] (padded to 16 bytes), then desc [max_mtiles].
+size_t tiles_desc_offset(int64_t n_seg) { return ((size_t)(n_seg + 1) * sizeof(int32_t) + 15) & ~(size_t)15; }
 
 // LDS byte offset of 16-byte chunk c (0..7) of row `row` in a 128-byte-row
 // tile.  gfx950's LDS serves 256 bytes per clock (64 four-byte banks), so
@@ -124,9 +144,9 @@ __device__ __forceinline__ v16f mfma_f8_32x32x64(const v8i& a, const v8i& b, con
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
 }
 
-// The tile of work item `item`: expert e owns items [mtile_start[e],
-// mtile_start[e+1]) * n_tiles in n-tile-major order, item = mtile_start[e] *
-// n_tiles + nt * mcount_e + mt.  The m-tiles that read the same weight slice
+// The tile of work item `item`: segment seg (an expert's rows in one chunk)
+// owns items [mtile_start[seg], mtile_start[seg+1]) * n_tiles in n-tile-major
+// order, item = mtile_start[seg] * n_tiles + nt * mcount + mt.  The m-tiles that read the same weight slice
 // (same nt) are neighbours, so they run together on one XCD and the slice
 // comes from HBM once (m-tile major order fetched the weights once per
 // m-tile).  The expert's ceil(M/32) row groups are dealt evenly over its
@@ -137,12 +157,13 @@ __device__ __forceinline__ v16f mfma_f8_32x32x64(const v8i& a, const v8i& b, con
 // tail tile ran about 3.6 times faster than the full tiles and fetched the
 // slice ahead of them; gate/up read 1.7 times its algorithmic bytes).
 struct Tile {
-  int e, m0, mc, nt;  // expert, first sorted row, rows, n-tile
+  int e, chunk, m0, mc, nt;  // expert, chunk, first sorted row, rows, n-tile
 };
 
 __device__ __forceinline__ Tile tile_of(const PrefillArgs& p, int item) {
   const int4 d = p.desc[item / p.n_tiles];
-  const int e = d.x, s0 = d.y, o0 = d.z, o1 = d.w;
+  const int seg = d.x, s0 = d.y, o0 = d.z, o1 = d.w;
+  const int e = seg / p.n_chunks;
   const int mcount = (o1 - o0 + kBM - 1) / kBM;
   const int local = item - s0 * p.n_tiles;
   const int ntx = local / mcount;
@@ -151,7 +172,7 @@ __device__ __forceinline__ Tile tile_of(const PrefillArgs& p, int item) {
   const int base = q / mcount, extra = q - base * mcount;
   const int first = o0 + 32 * (mt * base + min(mt, extra));
   const int groups = base + (mt < extra ? 1 : 0);
-  return Tile{e, first, min(32 * groups, o1 - first), ntx};
+  return Tile{e, seg - e * p.n_chunks, first, min(32 * groups, o1 - first), ntx};
 }
 
 template <bool GATEUP>
@@ -167,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 
   // XCD-major work item over the real items (the grid is an upper bound):
   // XCD x takes items [x*per, (x+1)*per) in order.
-  int total = p.mtile_start[p.E];
+  int total = p.mtile_start[p.n_seg];
   if (total > p.max_mtiles) total = (int)p.max_mtiles;  // inconsistent offsets: only described m-tiles run
   const int real = total * p.n_tiles;  // < 2^31 (the grid bound is checked on the host)
   const int per = (real + kXcd - 1) / kXcd;
@@ -232,7 +253,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 #pragma unroll
     for (int s = 0; s < kRing - 1; ++s) MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
     if (tid < kBM) {
-      const int srow = p.sorted_src ? (int)raw / p.topk : m0 + tid;
+      const int srow = p.sorted_src ? (int)raw / p.topk + tile.chunk * p.chunk_tokens : m0 + tid;
       arow[tid] = (tid < mc && srow >= 0 && srow < p.a_rows) ? srow : -1;
     } else if (tid - kBM < 2 * nb) {
       sw_lds[tid - kBM] = __uint_as_float(raw);
@@ -601,47 +622,53 @@ moe_status_t prefill_shape_check(const moe_dims_t& d) {
 // Bound on the 128-row m-tiles of R routed rows over E experts.
 int64_t prefill_max_mtiles(int64_t R, int64_t E) { return (R + kBM - 1) / kBM + (R < E ? R : E); }
 
-// mtile_start [E+1] and the m-tile descriptors [max_mtiles].
-size_t prefill_tiles_bytes(int64_t n_experts, int64_t max_mtiles) {
-  return tiles_desc_offset(n_experts) + (size_t)max_mtiles * sizeof(int4);
+// mtile_start [n_seg+1] and the m-tile descriptors [max_mtiles].
+size_t prefill_tiles_bytes(int64_t n_seg, int64_t max_mtiles) {
+  return tiles_desc_offset(n_seg) + (size_t)max_mtiles * sizeof(int4);
 }
 
 size_t prefill_tile_workspace(const moe_dims_t& d, int32_t T) {
   return prefill_tiles_bytes(d.n_experts, prefill_max_mtiles((int64_t)T * d.topk, d.n_experts));
 }
 
-// Gate/up then down over the expert-sorted rows described by offsets[0..E].
-// max_mtiles bounds the number of 128-row tiles over all experts (it sizes
-// the grid); a_rows is the number of activation rows (tokens).
-moe_status_t run_ffn_prefill_view(const moe_dims_t& d, int64_t max_mtiles, int32_t a_rows, const uint8_t* qx,
-                                  const float* sx, const int32_t* offsets, const int32_t* sorted_src,
-                                  const uint8_t* w_gate, const float* s_gate, const uint8_t* w_up, const float* s_up,
-                                  const uint8_t* w_down, const float* s_down, float* y_rows, uint8_t* qh, float* sh,
-                                  int32_t* tiles, hipStream_t stream) {
+// Gate/up then down over the expert-sorted rows that r describes (segments
+// of n_units experts in n_chunks chunks, see prefill_tiles_kernel).  The
+// weight stacks hold the r.n_units experts; qx/sx hold r.tokens rows,
+// sorted_src, qh/sh and y_rows r.rows rows (chunk c's from row c *
+// r.chunk_rows).
+moe_status_t run_ffn_prefill_view(const moe_dims_t& d, const PrefillRows& r, const uint8_t* qx, const float* sx,
+                                  const int32_t* sorted_src, const uint8_t* w_gate, const float* s_gate,
+                                  const uint8_t* w_up, const float* s_up, const uint8_t* w_down, const float* s_down,
+                                  float* y_rows, uint8_t* qh, float* sh, int32_t* tiles, hipStream_t stream) {
   moe_status_t st0 = prefill_shape_check(d);
   if (st0 != MOE_OK) return st0;
-  int4* desc = reinterpret_cast<int4*>(reinterpret_cast<uint8_t*>(tiles) + tiles_desc_offset(d.n_experts));
-  MOE_LAUNCH("prefill_tiles", prefill_tiles_kernel, dim3(1), dim3(1024), 0, stream, offsets, d.n_experts, tiles, desc,
-             max_mtiles);
+  const int64_t n_seg = (int64_t)r.n_units * r.n_chunks;
+  if (n_seg > 0x7fffffff || r.rows > 0x7fffffff)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: %lld segments, %lld rows", (long long)n_seg, (long long)r.rows);
+  int4* desc = reinterpret_cast<int4*>(reinterpret_cast<uint8_t*>(tiles) + tiles_desc_offset(n_seg));
+  MOE_LAUNCH("prefill_tiles", prefill_tiles_kernel, dim3(1), dim3(1024), 0, stream, r.offsets, r.off_stride,
+             r.n_units, r.n_chunks, r.chunk_rows, tiles, desc, r.max_mtiles);
   moe_status_t st = check_launch("prefill_tiles");
   if (st != MOE_OK) return st;
 
   PrefillArgs g{};
-  g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = a_rows;
-  g.offsets = offsets; g.mtile_start = tiles; g.desc = desc; g.max_mtiles = max_mtiles; g.E = d.n_experts;
+  g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = r.tokens;
+  g.mtile_start = tiles; g.desc = desc; g.max_mtiles = r.max_mtiles;
+  g.n_seg = (int)n_seg; g.n_chunks = r.n_chunks; g.chunk_tokens = r.chunk_tokens;
   g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
   g.N = d.inter; g.K = d.hidden; g.n_tiles = d.inter / kBlock;
   g.qh = qh; g.sh = sh; g.y = nullptr;
-  st = launch_prefill<true>(g, max_mtiles, stream);
+  st = launch_prefill<true>(g, r.max_mtiles, stream);
   if (st != MOE_OK) return st;
 
   PrefillArgs dn{};
-  dn.a = qh; dn.sa = sh; dn.sorted_src = nullptr; dn.topk = d.topk; dn.a_rows = (int)((int64_t)a_rows * d.topk);
-  dn.offsets = offsets; dn.mtile_start = tiles; dn.desc = desc; dn.max_mtiles = max_mtiles; dn.E = d.n_experts;
+  dn.a = qh; dn.sa = sh; dn.sorted_src = nullptr; dn.topk = d.topk; dn.a_rows = (int)r.rows;
+  dn.mtile_start = tiles; dn.desc = desc; dn.max_mtiles = r.max_mtiles;
+  dn.n_seg = (int)n_seg; dn.n_chunks = r.n_chunks; dn.chunk_tokens = 0;
   dn.w0 = w_down; dn.s0 = s_down; dn.w1 = nullptr; dn.s1 = nullptr;
   dn.N = d.hidden; dn.K = d.inter; dn.n_tiles = d.hidden / kBN;
   dn.y = y_rows; dn.qh = nullptr; dn.sh = nullptr;
-  return launch_prefill<false>(dn, max_mtiles, stream);
+  return launch_prefill<false>(dn, r.max_mtiles, stream);
 }
 
 moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, const float* sx,
@@ -649,9 +676,12 @@ moe_status_t run_ffn_prefill(const moe_dims_t& d, int32_t T, const uint8_t* qx, 
                              const float* s_gate, const uint8_t* w_up, const float* s_up, const uint8_t* w_down,
                              const float* s_down, float* y_rows, uint8_t* qh, float* sh, int32_t* tiles,
                              hipStream_t stream) {
-  const int64_t max_mtiles = prefill_max_mtiles((int64_t)T * d.topk, d.n_experts);
-  return run_ffn_prefill_view(d, max_mtiles, T, qx, sx, offsets, sorted_src, w_gate, s_gate, w_up, s_up, w_down,
-                              s_down, y_rows, qh, sh, tiles, stream);
+  PrefillRows r{};
+  r.offsets = offsets; r.off_stride = 0; r.n_units = d.n_experts; r.n_chunks = 1; r.chunk_rows = 0;
+  r.chunk_tokens = 0; r.tokens = T; r.rows = (int64_t)T * d.topk;
+  r.max_mtiles = prefill_max_mtiles(r.rows, d.n_experts);
+  return run_ffn_prefill_view(d, r, qx, sx, sorted_src, w_gate, s_gate, w_up, s_up, w_down, s_down, y_rows, qh, sh,
+                              tiles, stream);
 }
 
 }  // namespace moe

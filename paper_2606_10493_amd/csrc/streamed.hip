@@ -19,11 +19,13 @@
 // Because copy(g) is enqueued after compute(g - R/G) and compute(g) after
 // copy(g), every wait refers to the intended record.
 //
-// Tokens: all T are quantized at once; the permutation, the expert FFN and
-// the combine work per chunk of chunk_tokens tokens.  The FFN of a group on
-// chunk c reads a G-expert view of chunk c's offsets (offsets pointer + e0),
-// so the kernels and every row's arithmetic are those of the resident path:
-// each output row is bit-identical to moe_expert_ffn with the prefill regime.
+// Tokens: all T are quantized at once; the permutation and the combine work
+// per chunk of chunk_tokens tokens.  The FFN of a group is one launch pair
+// (gate/up, down) over its rows in every chunk: each (expert, chunk) pair is
+// a segment of the launch, read through a G-expert window of each chunk's
+// offsets (offsets pointer + e0), so the tiles never mix chunks and the
+// kernels and every row's arithmetic are those of the resident path: each
+// output row is bit-identical to moe_expert_ffn with the prefill regime.
 #include <vector>
 
 #include "common.h"
@@ -36,12 +38,11 @@ struct moe_stream_ctx {
 
 namespace moe {
 
-moe_status_t run_ffn_prefill_view(const moe_dims_t& d, int64_t max_mtiles, int32_t a_rows, const uint8_t* qx,
-                                  const float* sx, const int32_t* offsets, const int32_t* sorted_src,
-                                  const uint8_t* w_gate, const float* s_gate, const uint8_t* w_up, const float* s_up,
-                                  const uint8_t* w_down, const float* s_down, float* y_rows, uint8_t* qh, float* sh,
-                                  int32_t* tiles, hipStream_t stream);
-size_t prefill_tiles_bytes(int64_t n_experts, int64_t max_mtiles);
+moe_status_t run_ffn_prefill_view(const moe_dims_t& d, const PrefillRows& r, const uint8_t* qx, const float* sx,
+                                  const int32_t* sorted_src, const uint8_t* w_gate, const float* s_gate,
+                                  const uint8_t* w_up, const float* s_up, const uint8_t* w_down, const float* s_down,
+                                  float* y_rows, uint8_t* qh, float* sh, int32_t* tiles, hipStream_t stream);
+size_t prefill_tiles_bytes(int64_t n_seg, int64_t max_mtiles);
 moe_status_t prefill_shape_check(const moe_dims_t& d);
 
 namespace {
@@ -71,10 +72,12 @@ StreamLayout layout(const moe_dims_t& d, int32_t T, int32_t chunk_tokens) {
   L.sorted_src = take((size_t)L.n_chunks * ck * sizeof(int32_t));
   L.dest_row = take((size_t)L.n_chunks * ck * sizeof(int32_t));
   L.perm_ws = take(moe_permute_workspace(chunk_tokens, d.topk, d.n_experts));
-  L.qh = take((size_t)ck * I);
-  L.sh = take((size_t)ck * (I / kBlock) * sizeof(float));
-  L.tiles = take(prefill_tiles_bytes(E, (ck + 127) / 128 + E));  // views of G <= E experts, chunk rows
-  L.y = take((size_t)T * k * H * sizeof(float));
+  const int64_t R = (int64_t)T * k;  // sorted rows of all chunks
+  L.qh = take((size_t)R * I);
+  L.sh = take((size_t)R * (I / kBlock) * sizeof(float));
+  // segments of G <= E experts in every chunk
+  L.tiles = take(prefill_tiles_bytes(E * L.n_chunks, (R + 127) / 128 + E * L.n_chunks));
+  L.y = take((size_t)R * H * sizeof(float));
   L.total = off;
   return L;
 }
@@ -189,8 +192,9 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
   }
 
   // Experts are streamed and run in groups of G consecutive experts, held in
-  // G consecutive ring slots, so that one launch covers enough rows to fill
-  // the GPU (about 2048 rows per chunk).  G divides R.
+  // G consecutive ring slots; one GEMM launch pair covers the group's rows
+  // of every chunk (segments of one expert in one chunk), so a launch sees
+  // about 2048 rows per chunk of the group.  G divides R.
   int G = 1;
   {
     const int64_t rows_per_expert = ((int64_t)L.chunk * k + E - 1) / E;
@@ -199,8 +203,6 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
     for (int g = (int)want; g >= 1; --g)
       if (R % g == 0) { G = g; break; }
   }
-  const moe_dims_t view{d.hidden, d.inter, G, d.topk};
-  const int64_t max_mtiles = ((int64_t)L.chunk * k + 127) / 128 + G;  // G experts, at most chunk rows each
   uint8_t* ring_gate = dev_ring;
   uint8_t* ring_up = dev_ring + (size_t)R * wmat;
   uint8_t* ring_down = dev_ring + 2 * (size_t)R * wmat;
@@ -223,20 +225,24 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
         hipMemcpyAsync(ring_sdown + slot0 * smat, host_s_down + e0 * smat, nb_s, hipMemcpyHostToDevice, copy))
       return fail(MOE_ERR_HIP, "moe_ffn_streamed: copy of experts %lld..", (long long)e0);
     if (hipEventRecord(ctx->on[slot0], copy) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record ON");
-    // Model: the group's rows of every chunk, one launch set per chunk.
+    // Model: the group's rows of every chunk in one launch pair.
     if (hipStreamWaitEvent(compute, ctx->on[slot0], 0) != hipSuccess)
       return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait ON");
-    const moe_dims_t vd{view.hidden, view.inter, g_here, view.topk};
-    for (int64_t c = 0; c < L.n_chunks; ++c) {
-      const int32_t t0 = (int32_t)(c * L.chunk);
-      const int32_t tc = (int32_t)((T - t0) < L.chunk ? (T - t0) : L.chunk);
-      st = run_ffn_prefill_view(vd, max_mtiles, tc, qx + (int64_t)t0 * H, sx + (int64_t)t0 * (H / kBlock),
-                                offsets + c * (E + 1) + e0, sorted_src + c * L.chunk * k, ring_gate + slot0 * wmat,
-                                ring_sgate + slot0 * smat, ring_up + slot0 * wmat, ring_sup + slot0 * smat,
-                                ring_down + slot0 * wmat, ring_sdown + slot0 * smat, y + c * L.chunk * k * H, qh,
-                                sh, tiles, compute);
-      if (st != MOE_OK) return st;
-    }
+    PrefillRows rows{};
+    rows.offsets = offsets + e0;
+    rows.off_stride = E + 1;
+    rows.n_units = g_here;
+    rows.n_chunks = (int)L.n_chunks;
+    rows.chunk_rows = L.chunk * k;
+    rows.chunk_tokens = (int)L.chunk;
+    rows.tokens = T;
+    rows.rows = (int64_t)T * k;
+    rows.max_mtiles = (rows.rows + 127) / 128 + (int64_t)g_here * L.n_chunks;
+    const moe_dims_t vd{d.hidden, d.inter, g_here, d.topk};
+    st = run_ffn_prefill_view(vd, rows, qx, sx, sorted_src, ring_gate + slot0 * wmat, ring_sgate + slot0 * smat,
+                              ring_up + slot0 * wmat, ring_sup + slot0 * smat, ring_down + slot0 * wmat,
+                              ring_sdown + slot0 * smat, y, qh, sh, tiles, compute);
+    if (st != MOE_OK) return st;
     for (int s = slot0; s < slot0 + g_here; ++s) {
       if (hipEventRecord(ctx->off[s], compute) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record OFF");
       ctx->off_recorded[s] = 1;

@@ -119,3 +119,39 @@ def rel_err(got_f32: np.ndarray, ref_f32: np.ndarray) -> float:
 
 def bits_to_f32(t: torch.Tensor) -> np.ndarray:
     return oracle.bf16_to_f32(t.cpu().numpy().view(np.uint16))
+
+
+def oracle_expert_weights_pooled(w: synth.Workload, experts, layer: int = 0, batch: int = 16):
+    """oracle_expert_weights for many experts: the fp32 matrices are re-drawn on
+    the GPU in batches and quantized by the oracle on a pool of CPU processes."""
+    import oracle_pool
+    experts = [int(e) for e in experts]
+    jobs = [(e, which) for e in experts for which in range(3)]
+    mats = {}
+    for i in range(0, len(jobs), batch):
+        part = jobs[i:i + batch]
+        f32s = [synth.expert_weight_device(w, layer, e, which).cpu().numpy() for e, which in part]
+        for key, qs in zip(part, oracle_pool.quantize_weights(f32s)):
+            mats[key] = qs
+        del f32s
+    return {e: mats[(e, 0)] + mats[(e, 1)] + mats[(e, 2)] for e in experts}
+
+
+def oracle_tokens_grouped(x_bits, ids, wts, tokens, ow):
+    """Oracle output rows (bf16 bits) of some tokens, the layer's steps in order:
+    quantize the tokens, sort their slots by expert, run each expert once over
+    its rows, combine in slot order (the experts of the tokens, relabelled in
+    ascending order, so the sort and the combine order are those of the layer)."""
+    tokens = list(tokens)
+    qx, sx = oracle.quant_act(x_bits[tokens])
+    sub = np.asarray(ids[tokens])
+    k = sub.shape[1]
+    uniq = sorted(set(sub.reshape(-1).tolist()))
+    relabel = np.vectorize({e: i for i, e in enumerate(uniq)}.get)(sub).astype(np.int32)
+    offsets, src, dest = oracle.permute(relabel, len(uniq))
+    y = np.zeros((len(tokens) * k, x_bits.shape[1]), np.float32)
+    for i, e in enumerate(uniq):
+        p0, p1 = int(offsets[i]), int(offsets[i + 1])
+        rows = src[p0:p1] // k
+        y[p0:p1] = oracle.expert_rows(qx[rows], sx[rows], *ow[e])
+    return oracle.combine(y, dest, np.asarray(wts[tokens]))

@@ -68,13 +68,39 @@ def _check(name, x, wr, bias, k, n_group, topk_group, scaling, moe):
     assert np.all(same | close), "ids differ on a token without a near tie"
     assert close.mean() <= 0.15  # most tokens are compared bit for bit
     assert np.allclose(wts[same], r_w[same], rtol=0, atol=1e-5 * scaling)
+    e_all = sel.shape[1]
+    gsize = e_all // n_group
+    gscore = ro.group_scores(sel, n_group) if n_group > 1 else None
+    scores = inter["scores"]
     for t in np.nonzero(~same)[0]:  # near ties: a valid choice under the oracle keys within EPS
-        got = set(ids[t].tolist())
-        assert len(got) == k
-        chosen_min = min(sel[t, list(got)])
-        others = [sel[t, e] for e in range(sel.shape[1]) if e not in got and e // (sel.shape[1] // n_group) in
-                  set(i // (sel.shape[1] // n_group) for i in got)]
+        row = ids[t].tolist()
+        got = set(row)
+        assert len(got) == k and all(0 <= e < e_all for e in row)
+        # groups: at most topk_group of them, each scoring within EPS of the
+        # topk_group-th best group; completed with the best other groups
+        used = sorted(set(e // gsize for e in row))
+        assert len(used) <= topk_group
+        if gscore is not None:
+            thr = np.sort(gscore[t])[::-1][topk_group - 1]
+            assert all(gscore[t, g] >= thr - EPS for g in used), (t, used)
+            rest = [g for g in np.argsort(-gscore[t], kind="stable").tolist() if g not in used]
+            kept = set(used) | set(rest[:topk_group - len(used)])
+        else:
+            kept = {0}
+        # experts: no expert of a kept group left out beats a chosen one by more than EPS
+        chosen_min = min(sel[t, row])
+        others = [sel[t, e] for e in range(e_all) if e not in got and e // gsize in kept]
         assert not others or max(others) <= chosen_min + EPS
+        # listed by decreasing key (within EPS)
+        keys = sel[t, row]
+        assert np.all(keys[:-1] >= keys[1:] - EPS)
+        # weights of the chosen ids: oracle scores normalised in slot order
+        sv = scores[t, row].astype(np.float32)
+        tot = np.float32(0.0)
+        for v in sv:
+            tot = np.float32(tot + v)
+        w_ref = (sv / tot * np.float32(scaling)).astype(np.float32)
+        assert np.allclose(wts[t], w_ref, rtol=0, atol=1e-5 * scaling), (t, wts[t], w_ref)
 
 
 def test_router_tiny_plain_topk(moe):

@@ -7,9 +7,9 @@ block, the row-scale and expert-row loads with their stand-in rows, and the
 output stores) is recomputed here, and each address is checked against the
 size of the buffer it points into.  Shapes: the tiny layer, ragged tail
 tiles with skewed routing, the DeepSeek-V3 prefill chunk (8192 tokens,
-uniform) and a streamed group view (G experts of a 4096-token chunk, row
-positions absolute in the chunk, scales of a ring whose end is the group's
-last slot).
+uniform) and the streamed path's launch over one group of G experts in
+every chunk (segments of one expert in one chunk, row positions absolute
+over the chunks, scales of a ring whose end is the group's last slot).
 """
 import numpy as np
 import pytest
@@ -21,21 +21,28 @@ def _max_mtiles(R, E):
     return (R + BM - 1) // BM + min(R, E)
 
 
-def _describe(offsets, E, max_mtiles):
-    """prefill_tiles_kernel: mtile_start and the per-m-tile descriptors."""
-    m = np.diff(offsets[: E + 1])
-    c = np.where(m > 0, (m + BM - 1) // BM, 0)
-    start = np.concatenate([[0], np.cumsum(c)])
+def _describe(chunk_offsets, n_units, n_chunks, chunk_rows, max_mtiles):
+    """prefill_tiles_kernel: segments seg = u * n_chunks + c (expert u's rows of
+    chunk c, absolute rows c * chunk_rows + chunk c's offsets), their m-tile
+    scan and the per-m-tile descriptors."""
+    segs = []
+    for u in range(n_units):
+        for c in range(n_chunks):
+            oc = chunk_offsets[c]
+            segs.append((c * chunk_rows + int(oc[u]), c * chunk_rows + int(oc[u + 1])))
+    cnt = [(o1 - o0 + BM - 1) // BM if o1 > o0 else 0 for o0, o1 in segs]
+    start = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64)
     desc = {}
-    for e in range(E):
-        for b in range(start[e], start[e] + c[e]):
+    for seg, (o0, o1) in enumerate(segs):
+        for b in range(start[seg], start[seg] + cnt[seg]):
             if b < max_mtiles:
-                desc[b] = (e, start[e], int(offsets[e]), int(offsets[e + 1]))
+                desc[b] = (seg, int(start[seg]), o0, o1)
     return start, desc
 
 
-def _tile_of(desc, n_tiles, item):
-    e, s0, o0, o1 = desc[item // n_tiles]
+def _tile_of(desc, n_tiles, n_chunks, item):
+    seg, s0, o0, o1 = desc[item // n_tiles]
+    e, chunk = divmod(seg, n_chunks)
     mcount = (o1 - o0 + BM - 1) // BM
     local = item - s0 * n_tiles
     ntx, mt = divmod(local, mcount)
@@ -43,24 +50,31 @@ def _tile_of(desc, n_tiles, item):
     base, extra = divmod(q, mcount)
     first = o0 + 32 * (mt * base + min(mt, extra))
     groups = base + (1 if mt < extra else 0)
-    return e, first, min(32 * groups, o1 - first), ntx
+    return e, chunk, first, min(32 * groups, o1 - first), ntx
 
 
 def _packed_lane_offset(h, kq, r):
     return 1024 * h + 512 * (kq & 1) + 256 * (kq >> 1) + 16 * r
 
 
-def replay(gateup, E, N, K, topk, a_rows, offsets, sorted_src, R):
+def replay(gateup, E, N, K, topk, a_rows, offsets, sorted_src, R, n_chunks=1, chunk_rows=0, chunk_tokens=0,
+           max_mtiles=None):
     """Checks every address one launch computes; returns the number of items run.
 
-    a_rows: rows of the activation operand (tokens for gate/up, routed rows
-    for down); R: rows of the sorted order (sorted_src and the outputs).
+    E: experts of the launch (its weight stacks); offsets: [E+1] for one
+    chunk, or a list of n_chunks such windows (chunk c's rows start at c *
+    chunk_rows, its sorted_src entries are chunk-relative slots); a_rows:
+    rows of the activation operand (tokens for gate/up, routed rows for
+    down); R: rows of the sorted order (sorted_src and the outputs).
     """
     nb = K // 128
     n_tiles = N // 128 if gateup else N // BN
-    max_mtiles = _max_mtiles(R, E)
-    start, desc = _describe(offsets, E, max_mtiles)
-    total = min(int(start[E]), max_mtiles)
+    chunk_offsets = offsets if n_chunks > 1 else [offsets]
+    n_seg = E * n_chunks
+    if max_mtiles is None:
+        max_mtiles = _max_mtiles(R, E)
+    start, desc = _describe(chunk_offsets, E, n_chunks, chunk_rows, max_mtiles)
+    total = min(int(start[n_seg]), max_mtiles)
     real = total * n_tiles
     grid = (max_mtiles * n_tiles + XCD - 1) // XCD * XCD
     per = (real + XCD - 1) // XCD
@@ -77,7 +91,8 @@ def replay(gateup, E, N, K, topk, a_rows, offsets, sorted_src, R):
         if item >= real:
             continue
         ran += 1
-        e, m0, mc, nt = _tile_of(desc, n_tiles, item)
+        e, chunk, m0, mc, nt = _tile_of(desc, n_tiles, n_chunks, item)
+        assert 0 <= e < E and 0 <= chunk < n_chunks
         assert 0 < mc <= BM and m0 >= 0 and m0 + mc <= R
         # (1) one 4-byte load per thread: a sorted_src entry or a weight scale.
         ti = np.minimum(tid, mc - 1)
@@ -96,7 +111,7 @@ def replay(gateup, E, N, K, topk, a_rows, offsets, sorted_src, R):
         # missing ones: the tile's last row, row 0 if that one is invalid).
         rows = np.arange(BM)
         if gateup:
-            srow = np.array([sorted_src[m0 + min(t, mc - 1)] // topk for t in rows])
+            srow = np.array([sorted_src[m0 + min(t, mc - 1)] // topk + chunk * chunk_tokens for t in rows])
         else:
             srow = m0 + rows
         arow = np.where((rows < mc) & (srow >= 0) & (srow < a_rows), srow, -1)
@@ -166,19 +181,30 @@ def test_prefill_addresses_deepseek_prefill_chunk():
     assert n_dn == 28 * (n_gu // 16)
 
 
-def test_prefill_addresses_streamed_group_view():
-    """A group of G experts of one 4096-token chunk, as the streamed path runs
-    it: offsets are a window of the chunk's offsets (absolute row positions),
-    the weight and scale stacks hold exactly the G experts (the group ends at
-    the ring's last slot)."""
-    H, I, E, k, T, G = 7168, 2048, 256, 8, 4096, 16
+def test_prefill_addresses_streamed_group_over_chunks():
+    """The streamed path's launch pair of one group of G experts over all
+    chunks: each chunk sorted on its own (offsets and chunk-relative slots),
+    row positions absolute over the chunks (the last chunk partial), the
+    weight and scale stacks holding exactly the G experts (a group that ends
+    at the ring's last slot)."""
+    H, I, E, k, T, G, chunk = 7168, 2048, 256, 8, 1500, 16, 512
     ids = _routing(T, E, k, 0.8, 1)
-    offsets, src = _sorted(ids, E)
+    n_chunks = -(-T // chunk)
+    offs, srcs = [], []
+    for c in range(n_chunks):
+        o, s = _sorted(ids[c * chunk:(c + 1) * chunk], E)
+        offs.append(o)
+        srcs.append(s)
+    src_all = np.concatenate(srcs)       # chunk c's entries at c * chunk * k (the last chunk partial)
     R = T * k
-    for e0 in (0, 128, E - G):
-        view = offsets[e0:e0 + G + 1]
-        max_mt = _max_mtiles(R, G)
-        # the streamed path sizes the grid with the chunk's rows plus G
-        assert max_mt >= (R + 127) // 128 + G
-        replay(True, G, I, H, k, T, view - 0, src, R)
-        replay(False, G, H, I, k, R, view, None, R)
+    assert src_all.size == R
+    for e0 in (0, 112, E - G):
+        window = [o[e0:e0 + G + 1] for o in offs]
+        mm = (R + 127) // 128 + G * n_chunks
+        for gateup in (True, False):
+            n = replay(gateup, G, I if gateup else H, H if gateup else I, k, T if gateup else R, window,
+                       src_all if gateup else None, R, n_chunks=n_chunks, chunk_rows=chunk * k, chunk_tokens=chunk,
+                       max_mtiles=mm)
+            segs = [(c, u) for u in range(G) for c in range(n_chunks)]
+            tiles = sum(-(-int(offs[c][e0 + u + 1] - offs[c][e0 + u]) // 128) for c, u in segs)
+            assert n == tiles * (I // 128 if gateup else H // 256)
