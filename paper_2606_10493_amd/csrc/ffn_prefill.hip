@@ -71,15 +71,15 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 struct PrefillArgs {
   const uint8_t* a;           // e4m3 activations [a_rows, K]
   const float* sa;            // [a_rows, K/128]
-  const int32_t* sorted_src;  // GATEUP: A row of sorted row p = sorted_src[p] / topk (+ the chunk's first token); DOWN: NULL (A row = p)
+  const int32_t* sorted_src;  // GATEUP without row tables: A row of sorted row p = sorted_src[p] / topk; else unused
+  const int32_t* row_pos;     // NULL: tile rows are sorted positions; else the sorted position of launch row v
+  const int32_t* row_tok;     // GATEUP with row_pos: the token (A row) of launch row v
   int topk;
   int a_rows;
-  const int32_t* mtile_start; // [n_seg+1] exclusive scan of the segments' m-tile counts
+  const int32_t* mtile_start; // [n_units+1] exclusive scan of the experts' m-tile counts
   const int4* desc;           // [max_mtiles] m-tile block descriptors (prefill_tiles_kernel)
   int64_t max_mtiles;         // bound on the m-tiles (sizes desc)
-  int n_seg;                  // segments: (expert, chunk) pairs, seg = expert * n_chunks + chunk
-  int n_chunks;               // row chunks (1 for a resident layer)
-  int chunk_tokens;           // GATEUP: tokens per chunk (the token of a row of chunk c is sorted_src / topk + c * chunk_tokens)
+  int n_units;                // experts of the launch
   const uint8_t* w0;          // GATEUP: W_gate [E, N, K]; DOWN: W_down [E, N, K]; packed tiles
   const float* s0;
   const uint8_t* w1;          // GATEUP: W_up, packed tiles
@@ -91,45 +91,84 @@ struct PrefillArgs {
   float* sh;                  // GATEUP output [rows, N/128]
 };
 
-// The rows of a launch form segments, one per (expert, chunk) pair: segment
-// seg = u * n_chunks + c holds the rows of expert u in chunk c, rows
-// [c * chunk_rows + offsets[c * off_stride + u], c * chunk_rows +
-// offsets[c * off_stride + u + 1]) of the launch's sorted order (a resident
-// layer is one chunk, so a segment is an expert).  Segments are numbered
-// expert-major, so the chunks of one expert (which read the same weights)
-// are neighbours.  mtile_start = exclusive scan of the segments' m-tile
-// counts ceil(M / 128), and for every m-tile index b in [mtile_start[seg],
-// mtile_start[seg+1]) the descriptor desc[b] = (seg, mtile_start[seg], row0,
-// row1), from which a GEMM workgroup derives its tile with one uniform load
-// (no search).  Segments are taken 1024 at a time with a running total.
+// The rows of a launch.  One chunk (a resident layer): expert u owns the
+// sorted positions [offsets[u], offsets[u+1]).  Several chunks, each sorted
+// on its own (chunk c's positions start at c * chunk_rows, its offsets at
+// offsets + c * off_stride): expert u owns M_u = the sum of its rows over
+// the chunks, numbered as launch rows [vstart[u], vstart[u] + M_u) in chunk
+// order (prefill_rows_kernel maps each launch row to its sorted position and
+// token), so the tiles of an expert span chunks and all of them read the
+// expert's weight slices together.  mtile_start = exclusive scan of the
+// experts' m-tile counts ceil(M_u / 128), and for every m-tile index b in
+// [mtile_start[u], mtile_start[u+1]) desc[b] = (u, mtile_start[u], first
+// row, end row), from which a GEMM workgroup derives its tile with one
+// uniform load (no search).  Experts are taken 1024 at a time with running
+// totals.
 __global__ __launch_bounds__(1024) void prefill_tiles_kernel(const int32_t* __restrict__ offsets, int64_t off_stride,
-                                                             int n_units, int n_chunks, int64_t chunk_rows,
+                                                             int n_units, int n_chunks,
                                                              int32_t* __restrict__ mtile_start,
+                                                             int32_t* __restrict__ vstart,
                                                              int4* __restrict__ desc, int64_t max_mtiles) {
   __shared__ int wave_tot[16];
-  const int n_seg = n_units * n_chunks;
-  int carry = 0;
-  for (int base = 0; base < n_seg; base += 1024) {
-    const int seg = base + (int)threadIdx.x;
-    int o0 = 0, o1 = 0;
-    if (seg < n_seg) {
-      const int u = seg / n_chunks, c = seg - u * n_chunks;
-      const int32_t* oc = offsets + c * off_stride;
-      o0 = (int)(c * chunk_rows) + oc[u];
-      o1 = (int)(c * chunk_rows) + oc[u + 1];
+  int carry_t = 0, carry_v = 0;
+  for (int base = 0; base < n_units; base += 1024) {
+    const int u = base + (int)threadIdx.x;
+    int o0 = 0, m = 0;
+    if (u < n_units) {
+      if (n_chunks == 1) {
+        o0 = offsets[u];
+        m = offsets[u + 1] - o0;
+      } else {
+        for (int c = 0; c < n_chunks; ++c) m += offsets[c * off_stride + u + 1] - offsets[c * off_stride + u];
+      }
     }
-    const int cnt = (seg < n_seg && o1 > o0) ? (o1 - o0 + kBM - 1) / kBM : 0;
-    int total;
-    const int excl = carry + block_exclusive_scan(cnt, wave_tot, &total);
-    if (seg < n_seg) mtile_start[seg] = excl;
-    for (int b = excl; b < excl + cnt && b < max_mtiles; ++b) desc[b] = make_int4(seg, excl, o0, o1);
-    carry += total;
+    const int cnt = m > 0 ? (m + kBM - 1) / kBM : 0;
+    int tot_t, tot_v;
+    const int excl = carry_t + block_exclusive_scan(cnt, wave_tot, &tot_t);
+    const int v0 = carry_v + block_exclusive_scan(m, wave_tot, &tot_v);
+    if (n_chunks > 1) o0 = v0;
+    if (u < n_units) {
+      mtile_start[u] = excl;
+      vstart[u] = v0;
+    }
+    for (int b = excl; b < excl + cnt && b < max_mtiles; ++b) desc[b] = make_int4(u, excl, o0, o0 + m);
+    carry_t += tot_t;
+    carry_v += tot_v;
   }
-  if (threadIdx.x == 0) mtile_start[n_seg] = carry;
+  if (threadIdx.x == 0) {
+    mtile_start[n_units] = carry_t;
+    vstart[n_units] = carry_v;
+  }
 }
 
-// The tiles workspace: mtile_start [n_seg+1] (padded to 16 bytes), then desc [max_mtiles].
-size_t tiles_desc_offset(int64_t n_seg) { return ((size_t)(n_seg + 1) * sizeof(int32_t) + 15) & ~(size_t)15; }
+// Row tables of a launch over several chunks: block (c, u) writes the
+// launch rows of expert u's rows in chunk c, in order: row_pos = the sorted
+// position, row_tok = the token (the chunk-relative slot / topk plus the
+// chunk's first token).
+__global__ __launch_bounds__(256) void prefill_rows_kernel(const int32_t* __restrict__ offsets, int64_t off_stride,
+                                                           int64_t chunk_rows, int chunk_tokens,
+                                                           const int32_t* __restrict__ sorted_src, int topk,
+                                                           const int32_t* __restrict__ vstart,
+                                                           int32_t* __restrict__ row_pos,
+                                                           int32_t* __restrict__ row_tok) {
+  const int c = blockIdx.x, u = blockIdx.y;
+  int v = vstart[u];
+  for (int cc = 0; cc < c; ++cc) v += offsets[cc * off_stride + u + 1] - offsets[cc * off_stride + u];
+  const int p0 = offsets[c * off_stride + u];
+  const int cnt = offsets[c * off_stride + u + 1] - p0;
+  const int64_t base = (int64_t)c * chunk_rows + p0;
+  for (int r = threadIdx.x; r < cnt; r += blockDim.x) {
+    const int64_t pos = base + r;
+    row_pos[v + r] = (int32_t)pos;
+    row_tok[v + r] = sorted_src[pos] / topk + c * chunk_tokens;
+  }
+}
+
+// The tiles workspace: mtile_start [n_units+1], vstart [n_units+1] (each
+// padded to 16 bytes), desc [max_mtiles]; with several chunks also row_pos
+// and row_tok [rows] each.
+size_t tiles_index_bytes(int64_t n_units) { return ((size_t)(n_units + 1) * sizeof(int32_t) + 15) & ~(size_t)15; }
+size_t tiles_desc_offset(int64_t n_units) { return 2 * tiles_index_bytes(n_units); }
 
 // LDS byte offset of 16-byte chunk c (0..7) of row `row` in a 128-byte-row
 // tile.  gfx950's LDS serves 256 bytes per clock (64 four-byte banks), so
@@ -144,9 +183,9 @@ __device__ __forceinline__ v16f mfma_f8_32x32x64(const v8i& a, const v8i& b, con
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
 }
 
-// The tile of work item `item`: segment seg (an expert's rows in one chunk)
-// owns items [mtile_start[seg], mtile_start[seg+1]) * n_tiles in n-tile-major
-// order, item = mtile_start[seg] * n_tiles + nt * mcount + mt.  The m-tiles that read the same weight slice
+// The tile of work item `item`: expert u owns items [mtile_start[u],
+// mtile_start[u+1]) * n_tiles in n-tile-major order, item = mtile_start[u] *
+// n_tiles + nt * mcount_u + mt.  The m-tiles that read the same weight slice
 // (same nt) are neighbours, so they run together on one XCD and the slice
 // comes from HBM once (m-tile major order fetched the weights once per
 // m-tile).  The expert's ceil(M/32) row groups are dealt evenly over its
@@ -157,13 +196,12 @@ __device__ __forceinline__ v16f mfma_f8_32x32x64(const v8i& a, const v8i& b, con
 // tail tile ran about 3.6 times faster than the full tiles and fetched the
 // slice ahead of them; gate/up read 1.7 times its algorithmic bytes).
 struct Tile {
-  int e, chunk, m0, mc, nt;  // expert, chunk, first sorted row, rows, n-tile
+  int e, m0, mc, nt;  // expert, first row (a sorted position, or a launch row with row tables), rows, n-tile
 };
 
 __device__ __forceinline__ Tile tile_of(const PrefillArgs& p, int item) {
   const int4 d = p.desc[item / p.n_tiles];
-  const int seg = d.x, s0 = d.y, o0 = d.z, o1 = d.w;
-  const int e = seg / p.n_chunks;
+  const int e = d.x, s0 = d.y, o0 = d.z, o1 = d.w;
   const int mcount = (o1 - o0 + kBM - 1) / kBM;
   const int local = item - s0 * p.n_tiles;
   const int ntx = local / mcount;
@@ -172,13 +210,14 @@ __device__ __forceinline__ Tile tile_of(const PrefillArgs& p, int item) {
   const int base = q / mcount, extra = q - base * mcount;
   const int first = o0 + 32 * (mt * base + min(mt, extra));
   const int groups = base + (mt < extra ? 1 : 0);
-  return Tile{e, seg - e * p.n_chunks, first, min(32 * groups, o1 - first), ntx};
+  return Tile{e, first, min(32 * groups, o1 - first), ntx};
 }
 
 template <bool GATEUP>
 __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  __shared__ int arow[kBM];
+  __shared__ int arow[kBM];   // A row (token for GATEUP, sorted position for DOWN) of tile row t, -1 if none
+  __shared__ int orow[kBM];   // sorted position (output row) of tile row t < mc
   __shared__ float rowmax[8][kBM];
 
   const int tid = threadIdx.x;
@@ -188,7 +227,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
 
   // XCD-major work item over the real items (the grid is an upper bound):
   // XCD x takes items [x*per, (x+1)*per) in order.
-  int total = p.mtile_start[p.n_seg];
+  int total = p.mtile_start[p.n_units];
   if (total > p.max_mtiles) total = (int)p.max_mtiles;  // inconsistent offsets: only described m-tiles run
   const int real = total * p.n_tiles;  // < 2^31 (the grid bound is checked on the host)
   const int per = (real + kXcd - 1) / kXcd;
@@ -236,25 +275,43 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
   // 4-7).
   auto issue_indices_and_weights = [&]() {
     // One unconditional 4-byte load per thread from a per-thread address
-    // (threads 0-127: the row's sorted_src entry, clamped to the tile; the
-    // others: their weight-scale entry, clamped to the table), so that no
-    // branch makes the weight loads below wait for it.  Without sorted_src
-    // (DOWN) threads 0-127 read the tile's first weight-scale entry, whose
-    // value they ignore: the weight-scale index tw stays in [0, 2 nb) for
-    // every thread, so the address is inside the expert's scale rows.
+    // (threads 0-127: the row's index, clamped to the tile -- GATEUP: its
+    // sorted_src entry or, with row tables, its token; DOWN with row tables:
+    // its sorted position; the others: their weight-scale entry, clamped to
+    // the table), so that no branch makes the weight loads below wait for
+    // it.  Without a row index (DOWN over one chunk) threads 0-127 read the
+    // tile's first weight-scale entry, whose value they ignore: the
+    // weight-scale index tw stays in [0, 2 nb) for every thread, so the
+    // address is inside the expert's scale rows.  GATEUP with row tables
+    // loads the row's sorted position as well (threads 0-127; the others
+    // load their first address again).
     const int ti = min(tid, mc - 1);
     const int tw = tid < kBM ? 0 : min(tid - kBM, 2 * nb - 1);
     const int h = tw / nb, b = tw - h * nb;
     const int64_t wrow = (int64_t)tile.e * (p.N / kBlock) + (GATEUP ? nt : 2 * nt + h);
     const float* sw_src = ((GATEUP && h) ? p.s1 : p.s0) + wrow * nb + b;
-    const uint32_t* src = (tid < kBM && p.sorted_src) ? reinterpret_cast<const uint32_t*>(p.sorted_src + m0 + ti)
-                                                      : reinterpret_cast<const uint32_t*>(sw_src);
+    const int32_t* rsrc = GATEUP ? (p.row_tok ? p.row_tok : p.sorted_src) : p.row_pos;
+    const uint32_t* src = (tid < kBM && rsrc) ? reinterpret_cast<const uint32_t*>(rsrc + m0 + ti)
+                                              : reinterpret_cast<const uint32_t*>(sw_src);
     const uint32_t raw = *src;
+    uint32_t raw_pos = 0;
+    if (GATEUP) {
+      const uint32_t* psrc = (tid < kBM && p.row_pos) ? reinterpret_cast<const uint32_t*>(p.row_pos + m0 + ti) : src;
+      raw_pos = *psrc;
+    }
 #pragma unroll
     for (int s = 0; s < kRing - 1; ++s) MOE_PF_WLOAD(s, s < nb ? s : nb - 1);
     if (tid < kBM) {
-      const int srow = p.sorted_src ? (int)raw / p.topk + tile.chunk * p.chunk_tokens : m0 + tid;
+      int srow, pos;
+      if (GATEUP) {
+        srow = p.row_tok ? (int)raw : (int)raw / p.topk;
+        pos = p.row_pos ? (int)raw_pos : m0 + tid;
+      } else {
+        srow = p.row_pos ? (int)raw : m0 + tid;
+        pos = srow;
+      }
       arow[tid] = (tid < mc && srow >= 0 && srow < p.a_rows) ? srow : -1;
+      orow[tid] = pos;
     } else if (tid - kBM < 2 * nb) {
       sw_lds[tid - kBM] = __uint_as_float(raw);
     }
@@ -531,7 +588,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     for (int j = 0; j < 4; ++j) {
       const int t = j * 32 + r32;
       if (t < mc) {
-        float* dst = p.y + (int64_t)(m0 + t) * p.N + nt * kBN + wave * 32 + g2 * 4;
+        float* dst = p.y + (int64_t)orow[t] * p.N + nt * kBN + wave * 32 + g2 * 4;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           *reinterpret_cast<v4f*>(dst + q * 8) = v4f{acc[j][4 * q], acc[j][4 * q + 1], acc[j][4 * q + 2], acc[j][4 * q + 3]};
@@ -570,7 +627,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
       const uint32_t packed = quantize4_e4m3(hq[0], hq[1], hq[2], hq[3], s);
       *reinterpret_cast<uint32_t*>(qtile + swz(t, wave) + 8 * half + 4 * g2) = packed;
     }
-    if (wave == 0 && g2 == 0 && t < mc) p.sh[(int64_t)(m0 + t) * (p.N / kBlock) + nt] = s;
+    if (wave == 0 && g2 == 0 && t < mc) p.sh[(int64_t)orow[t] * (p.N / kBlock) + nt] = s;
   }
   __syncthreads();
   // 128 rows x 128 bytes = 1024 16-byte chunks, 2 per thread.
@@ -579,7 +636,7 @@ __global__ __launch_bounds__(kThreads) void ffn_prefill_kernel(PrefillArgs p) {
     const int c = tid + i * kThreads;
     const int row = c >> 3, col = (c & 7) * 16;
     if (row < mc)
-      *reinterpret_cast<uint4*>(p.qh + (int64_t)(m0 + row) * p.N + nt * kBlock + col) =
+      *reinterpret_cast<uint4*>(p.qh + (int64_t)orow[row] * p.N + nt * kBlock + col) =
           *reinterpret_cast<const uint4*>(qtile + swz(row, c & 7));
   }
   }  // GATEUP epilogue
@@ -622,39 +679,58 @@ moe_status_t prefill_shape_check(const moe_dims_t& d) {
 // Bound on the 128-row m-tiles of R routed rows over E experts.
 int64_t prefill_max_mtiles(int64_t R, int64_t E) { return (R + kBM - 1) / kBM + (R < E ? R : E); }
 
-// mtile_start [n_seg+1] and the m-tile descriptors [max_mtiles].
-size_t prefill_tiles_bytes(int64_t n_seg, int64_t max_mtiles) {
-  return tiles_desc_offset(n_seg) + (size_t)max_mtiles * sizeof(int4);
+// The tiles workspace of a launch over n_units experts: the index tables,
+// the m-tile descriptors [max_mtiles] and, for a launch over several chunks
+// (table_rows > 0), the row tables [table_rows] each.
+size_t prefill_tiles_bytes(int64_t n_units, int64_t max_mtiles, int64_t table_rows) {
+  const size_t tab = ((size_t)table_rows * sizeof(int32_t) + 15) & ~(size_t)15;
+  return tiles_desc_offset(n_units) + (size_t)max_mtiles * sizeof(int4) + 2 * tab;
 }
 
 size_t prefill_tile_workspace(const moe_dims_t& d, int32_t T) {
-  return prefill_tiles_bytes(d.n_experts, prefill_max_mtiles((int64_t)T * d.topk, d.n_experts));
+  return prefill_tiles_bytes(d.n_experts, prefill_max_mtiles((int64_t)T * d.topk, d.n_experts), 0);
 }
 
-// Gate/up then down over the expert-sorted rows that r describes (segments
-// of n_units experts in n_chunks chunks, see prefill_tiles_kernel).  The
-// weight stacks hold the r.n_units experts; qx/sx hold r.tokens rows,
-// sorted_src, qh/sh and y_rows r.rows rows (chunk c's from row c *
-// r.chunk_rows).
+// Gate/up then down over the expert-sorted rows that r describes (the
+// experts' rows of one chunk, or of several chunks each sorted on its own;
+// see prefill_tiles_kernel).  The weight stacks hold the r.n_units experts;
+// qx/sx hold r.tokens rows, sorted_src, qh/sh and y_rows r.rows rows (chunk
+// c's from row c * r.chunk_rows).  tiles: prefill_tiles_bytes(r.n_units,
+// r.max_mtiles, r.n_chunks > 1 ? r.rows : 0) bytes, 16-byte aligned.
 moe_status_t run_ffn_prefill_view(const moe_dims_t& d, const PrefillRows& r, const uint8_t* qx, const float* sx,
                                   const int32_t* sorted_src, const uint8_t* w_gate, const float* s_gate,
                                   const uint8_t* w_up, const float* s_up, const uint8_t* w_down, const float* s_down,
                                   float* y_rows, uint8_t* qh, float* sh, int32_t* tiles, hipStream_t stream) {
   moe_status_t st0 = prefill_shape_check(d);
   if (st0 != MOE_OK) return st0;
-  const int64_t n_seg = (int64_t)r.n_units * r.n_chunks;
-  if (n_seg > 0x7fffffff || r.rows > 0x7fffffff)
-    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: %lld segments, %lld rows", (long long)n_seg, (long long)r.rows);
-  int4* desc = reinterpret_cast<int4*>(reinterpret_cast<uint8_t*>(tiles) + tiles_desc_offset(n_seg));
+  if (r.rows > 0x7fffffff || r.n_units < 1 || r.n_chunks < 1 || (int64_t)r.n_chunks * r.n_units > 0x7fffffff)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: %lld rows, %d experts x %d chunks", (long long)r.rows,
+                r.n_units, r.n_chunks);
+  if (r.n_chunks > 65535 || r.n_units > 65535)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "ffn_prefill: %d chunks x %d experts", r.n_chunks, r.n_units);
+  uint8_t* tb = reinterpret_cast<uint8_t*>(tiles);
+  int32_t* vstart = reinterpret_cast<int32_t*>(tb + tiles_index_bytes(r.n_units));
+  int4* desc = reinterpret_cast<int4*>(tb + tiles_desc_offset(r.n_units));
+  int32_t* row_pos = nullptr;
+  int32_t* row_tok = nullptr;
   MOE_LAUNCH("prefill_tiles", prefill_tiles_kernel, dim3(1), dim3(1024), 0, stream, r.offsets, r.off_stride,
-             r.n_units, r.n_chunks, r.chunk_rows, tiles, desc, r.max_mtiles);
+             r.n_units, r.n_chunks, tiles, vstart, desc, r.max_mtiles);
   moe_status_t st = check_launch("prefill_tiles");
   if (st != MOE_OK) return st;
+  if (r.n_chunks > 1) {
+    row_pos = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(desc) + (size_t)r.max_mtiles * sizeof(int4));
+    row_tok = row_pos + ((r.rows + 3) & ~(int64_t)3);
+    MOE_LAUNCH("prefill_rows", prefill_rows_kernel, dim3((unsigned)r.n_chunks, (unsigned)r.n_units), dim3(256), 0,
+               stream, r.offsets, r.off_stride, r.chunk_rows, r.chunk_tokens, sorted_src, d.topk, vstart, row_pos,
+               row_tok);
+    st = check_launch("prefill_rows");
+    if (st != MOE_OK) return st;
+  }
 
   PrefillArgs g{};
-  g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.topk = d.topk; g.a_rows = r.tokens;
-  g.mtile_start = tiles; g.desc = desc; g.max_mtiles = r.max_mtiles;
-  g.n_seg = (int)n_seg; g.n_chunks = r.n_chunks; g.chunk_tokens = r.chunk_tokens;
+  g.a = qx; g.sa = sx; g.sorted_src = sorted_src; g.row_pos = row_pos; g.row_tok = row_tok;
+  g.topk = d.topk; g.a_rows = r.tokens;
+  g.mtile_start = tiles; g.desc = desc; g.max_mtiles = r.max_mtiles; g.n_units = r.n_units;
   g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
   g.N = d.inter; g.K = d.hidden; g.n_tiles = d.inter / kBlock;
   g.qh = qh; g.sh = sh; g.y = nullptr;
@@ -662,9 +738,9 @@ moe_status_t run_ffn_prefill_view(const moe_dims_t& d, const PrefillRows& r, con
   if (st != MOE_OK) return st;
 
   PrefillArgs dn{};
-  dn.a = qh; dn.sa = sh; dn.sorted_src = nullptr; dn.topk = d.topk; dn.a_rows = (int)r.rows;
-  dn.mtile_start = tiles; dn.desc = desc; dn.max_mtiles = r.max_mtiles;
-  dn.n_seg = (int)n_seg; dn.n_chunks = r.n_chunks; dn.chunk_tokens = 0;
+  dn.a = qh; dn.sa = sh; dn.sorted_src = nullptr; dn.row_pos = row_pos; dn.row_tok = nullptr;
+  dn.topk = d.topk; dn.a_rows = (int)r.rows;
+  dn.mtile_start = tiles; dn.desc = desc; dn.max_mtiles = r.max_mtiles; dn.n_units = r.n_units;
   dn.w0 = w_down; dn.s0 = s_down; dn.w1 = nullptr; dn.s1 = nullptr;
   dn.N = d.hidden; dn.K = d.inter; dn.n_tiles = d.hidden / kBN;
   dn.y = y_rows; dn.qh = nullptr; dn.sh = nullptr;

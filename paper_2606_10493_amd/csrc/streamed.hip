@@ -21,11 +21,13 @@
 //
 // Tokens: all T are quantized at once; the permutation and the combine work
 // per chunk of chunk_tokens tokens.  The FFN of a group is one launch pair
-// (gate/up, down) over its rows in every chunk: each (expert, chunk) pair is
-// a segment of the launch, read through a G-expert window of each chunk's
-// offsets (offsets pointer + e0), so the tiles never mix chunks and the
-// kernels and every row's arithmetic are those of the resident path: each
-// output row is bit-identical to moe_expert_ffn with the prefill regime.
+// (gate/up, down) over its rows in every chunk, read through a G-expert
+// window of each chunk's offsets (offsets pointer + e0): an expert's rows of
+// all chunks are numbered as one run of launch rows (tables map each to its
+// sorted position and token), so its 128-row tiles span chunks and read its
+// weight slices together.  The kernels and every row's arithmetic are those
+// of the resident path: each output row is bit-identical to moe_expert_ffn
+// with the prefill regime.
 #include <vector>
 
 #include "common.h"
@@ -42,7 +44,7 @@ moe_status_t run_ffn_prefill_view(const moe_dims_t& d, const PrefillRows& r, con
                                   const int32_t* sorted_src, const uint8_t* w_gate, const float* s_gate,
                                   const uint8_t* w_up, const float* s_up, const uint8_t* w_down, const float* s_down,
                                   float* y_rows, uint8_t* qh, float* sh, int32_t* tiles, hipStream_t stream);
-size_t prefill_tiles_bytes(int64_t n_seg, int64_t max_mtiles);
+size_t prefill_tiles_bytes(int64_t n_units, int64_t max_mtiles, int64_t table_rows);
 moe_status_t prefill_shape_check(const moe_dims_t& d);
 
 namespace {
@@ -75,8 +77,8 @@ StreamLayout layout(const moe_dims_t& d, int32_t T, int32_t chunk_tokens) {
   const int64_t R = (int64_t)T * k;  // sorted rows of all chunks
   L.qh = take((size_t)R * I);
   L.sh = take((size_t)R * (I / kBlock) * sizeof(float));
-  // segments of G <= E experts in every chunk
-  L.tiles = take(prefill_tiles_bytes(E * L.n_chunks, (R + 127) / 128 + E * L.n_chunks));
+  // G <= E experts over all chunks (row tables of all rows)
+  L.tiles = take(prefill_tiles_bytes(E, (R + 127) / 128 + E, R));
   L.y = take((size_t)R * H * sizeof(float));
   L.total = off;
   return L;
@@ -193,8 +195,8 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
 
   // Experts are streamed and run in groups of G consecutive experts, held in
   // G consecutive ring slots; one GEMM launch pair covers the group's rows
-  // of every chunk (segments of one expert in one chunk), so a launch sees
-  // about 2048 rows per chunk of the group.  G divides R.
+  // of every chunk (an expert's tiles span chunks), so a launch sees about
+  // 2048 rows per chunk of the group.  G divides R.
   int G = 1;
   {
     const int64_t rows_per_expert = ((int64_t)L.chunk * k + E - 1) / E;
@@ -237,7 +239,7 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
     rows.chunk_tokens = (int)L.chunk;
     rows.tokens = T;
     rows.rows = (int64_t)T * k;
-    rows.max_mtiles = (rows.rows + 127) / 128 + (int64_t)g_here * L.n_chunks;
+    rows.max_mtiles = (rows.rows + 127) / 128 + g_here;
     const moe_dims_t vd{d.hidden, d.inter, g_here, d.topk};
     st = run_ffn_prefill_view(vd, rows, qx, sx, sorted_src, ring_gate + slot0 * wmat, ring_sgate + slot0 * smat,
                               ring_up + slot0 * wmat, ring_sup + slot0 * smat, ring_down + slot0 * wmat,

@@ -8,8 +8,9 @@ output stores) is recomputed here, and each address is checked against the
 size of the buffer it points into.  Shapes: the tiny layer, ragged tail
 tiles with skewed routing, the DeepSeek-V3 prefill chunk (8192 tokens,
 uniform) and the streamed path's launch over one group of G experts in
-every chunk (segments of one expert in one chunk, row positions absolute
-over the chunks, scales of a ring whose end is the group's last slot).
+every chunk (an expert's rows of all chunks numbered as one run of launch
+rows mapped to sorted positions and tokens by row tables, scales of a ring
+whose end is the group's last slot).
 """
 import numpy as np
 import pytest
@@ -21,28 +22,43 @@ def _max_mtiles(R, E):
     return (R + BM - 1) // BM + min(R, E)
 
 
-def _describe(chunk_offsets, n_units, n_chunks, chunk_rows, max_mtiles):
-    """prefill_tiles_kernel: segments seg = u * n_chunks + c (expert u's rows of
-    chunk c, absolute rows c * chunk_rows + chunk c's offsets), their m-tile
-    scan and the per-m-tile descriptors."""
-    segs = []
-    for u in range(n_units):
-        for c in range(n_chunks):
-            oc = chunk_offsets[c]
-            segs.append((c * chunk_rows + int(oc[u]), c * chunk_rows + int(oc[u + 1])))
-    cnt = [(o1 - o0 + BM - 1) // BM if o1 > o0 else 0 for o0, o1 in segs]
+def _describe(chunk_offsets, n_units, max_mtiles):
+    """prefill_tiles_kernel: per expert u its rows (one chunk: sorted positions
+    [off[u], off[u+1]); several chunks: launch rows [vstart[u], vstart[u] +
+    M_u), M_u summed over the chunks), the m-tile scan and the descriptors."""
+    one = len(chunk_offsets) == 1
+    m = [sum(int(oc[u + 1] - oc[u]) for oc in chunk_offsets) for u in range(n_units)]
+    vstart = np.concatenate([[0], np.cumsum(m)]).astype(np.int64)
+    cnt = [(x + BM - 1) // BM if x > 0 else 0 for x in m]
     start = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64)
     desc = {}
-    for seg, (o0, o1) in enumerate(segs):
-        for b in range(start[seg], start[seg] + cnt[seg]):
+    for u in range(n_units):
+        o0 = int(chunk_offsets[0][u]) if one else int(vstart[u])
+        for b in range(start[u], start[u] + cnt[u]):
             if b < max_mtiles:
-                desc[b] = (seg, int(start[seg]), o0, o1)
-    return start, desc
+                desc[b] = (u, int(start[u]), o0, o0 + m[u])
+    return start, vstart, desc
 
 
-def _tile_of(desc, n_tiles, n_chunks, item):
-    seg, s0, o0, o1 = desc[item // n_tiles]
-    e, chunk = divmod(seg, n_chunks)
+def _row_tables(chunk_offsets, n_units, chunk_rows, chunk_tokens, sorted_src, topk, vstart):
+    """prefill_rows_kernel: launch row -> (sorted position, token)."""
+    n = int(vstart[-1])
+    pos = np.full(n, -1, np.int64)
+    tok = np.full(n, -1, np.int64)
+    for u in range(n_units):
+        v = int(vstart[u])
+        for c, oc in enumerate(chunk_offsets):
+            p0, cnt = int(oc[u]), int(oc[u + 1] - oc[u])
+            pp = c * chunk_rows + p0 + np.arange(cnt)
+            pos[v:v + cnt] = pp
+            tok[v:v + cnt] = np.asarray(sorted_src)[pp] // topk + c * chunk_tokens
+            v += cnt
+    assert np.all(pos >= 0)
+    return pos, tok
+
+
+def _tile_of(desc, n_tiles, item):
+    e, s0, o0, o1 = desc[item // n_tiles]
     mcount = (o1 - o0 + BM - 1) // BM
     local = item - s0 * n_tiles
     ntx, mt = divmod(local, mcount)
@@ -50,7 +66,7 @@ def _tile_of(desc, n_tiles, n_chunks, item):
     base, extra = divmod(q, mcount)
     first = o0 + 32 * (mt * base + min(mt, extra))
     groups = base + (1 if mt < extra else 0)
-    return e, chunk, first, min(32 * groups, o1 - first), ntx
+    return e, first, min(32 * groups, o1 - first), ntx
 
 
 def _packed_lane_offset(h, kq, r):
@@ -65,16 +81,20 @@ def replay(gateup, E, N, K, topk, a_rows, offsets, sorted_src, R, n_chunks=1, ch
     chunk, or a list of n_chunks such windows (chunk c's rows start at c *
     chunk_rows, its sorted_src entries are chunk-relative slots); a_rows:
     rows of the activation operand (tokens for gate/up, routed rows for
-    down); R: rows of the sorted order (sorted_src and the outputs).
+    down); R: rows of the sorted order (sorted_src, the row tables and the
+    outputs).
     """
     nb = K // 128
     n_tiles = N // 128 if gateup else N // BN
     chunk_offsets = offsets if n_chunks > 1 else [offsets]
-    n_seg = E * n_chunks
     if max_mtiles is None:
         max_mtiles = _max_mtiles(R, E)
-    start, desc = _describe(chunk_offsets, E, n_chunks, chunk_rows, max_mtiles)
-    total = min(int(start[n_seg]), max_mtiles)
+    start, vstart, desc = _describe(chunk_offsets, E, max_mtiles)
+    tables = n_chunks > 1
+    if tables:
+        row_pos, row_tok = _row_tables(chunk_offsets, E, chunk_rows, chunk_tokens, sorted_src, topk, vstart)
+        assert row_pos.size <= R
+    total = min(int(start[E]), max_mtiles)
     real = total * n_tiles
     grid = (max_mtiles * n_tiles + XCD - 1) // XCD * XCD
     per = (real + XCD - 1) // XCD
@@ -91,29 +111,36 @@ def replay(gateup, E, N, K, topk, a_rows, offsets, sorted_src, R, n_chunks=1, ch
         if item >= real:
             continue
         ran += 1
-        e, chunk, m0, mc, nt = _tile_of(desc, n_tiles, n_chunks, item)
-        assert 0 <= e < E and 0 <= chunk < n_chunks
+        e, m0, mc, nt = _tile_of(desc, n_tiles, item)
+        assert 0 <= e < E
         assert 0 < mc <= BM and m0 >= 0 and m0 + mc <= R
-        # (1) one 4-byte load per thread: a sorted_src entry or a weight scale.
+        # (1) one 4-byte load per thread: a row index (sorted_src, or a row
+        # table) or a weight scale; GATEUP with tables also the row's position.
         ti = np.minimum(tid, mc - 1)
         tw = np.where(tid < BM, 0, np.minimum(tid - BM, 2 * nb - 1))
         h, b = tw // nb, tw % nb
         wrow = e * (N // 128) + (nt if gateup else 2 * nt + h)
         sidx = wrow * nb + b
-        uses_src = (tid < BM) & gateup
-        assert np.all(np.where(uses_src, m0 + ti < R, (sidx >= 0) & (sidx < scale_entries)))
+        has_index = gateup or tables
+        uses_src = (tid < BM) & has_index
+        table_len = row_pos.size if tables else R
+        assert np.all(np.where(uses_src, m0 + ti < table_len, (sidx >= 0) & (sidx < scale_entries)))
         # (2) packed weights: every K block (the ring loads clamp to nb - 1).
         grp = nt * (128 // 16) + wave if gateup else nt * (BN // 16) + 2 * wave + (r32 >> 4)
         w0 = e * N * K + grp * nb * TILE_BYTES + _packed_lane_offset(0, 2 * g2, r32 & 15)
         assert np.all(w0 >= 0)
         assert np.all(w0 + (nb - 1) * TILE_BYTES + 1536 + 16 <= E * N * K)
         # (3) activation rows and their scales (stand-in rows for invalid or
-        # missing ones: the tile's last row, row 0 if that one is invalid).
+        # missing ones: the tile's last row, row 0 if that one is invalid),
+        # and the output rows.
         rows = np.arange(BM)
-        if gateup:
-            srow = np.array([sorted_src[m0 + min(t, mc - 1)] // topk + chunk * chunk_tokens for t in rows])
+        vrow = m0 + np.minimum(rows, mc - 1)
+        if tables:
+            pos = row_pos[vrow]
+            srow = row_tok[vrow] if gateup else pos
         else:
-            srow = m0 + rows
+            pos = m0 + rows
+            srow = np.asarray(sorted_src)[vrow] // topk if gateup else pos
         arow = np.where((rows < mc) & (srow >= 0) & (srow < a_rows), srow, -1)
         a_last = arow[mc - 1] if arow[mc - 1] >= 0 else 0
         ar = np.where(arow >= 0, arow, a_last)
@@ -122,18 +149,20 @@ def replay(gateup, E, N, K, topk, a_rows, offsets, sorted_src, R, n_chunks=1, ch
         c = np.concatenate([tid, tid + THREADS])
         a_off = ar[c >> 3] * K + (c & 7) * 16
         assert np.all(a_off + (nb - 1) * 128 + 16 <= a_rows * K)           # expert-row loads
-        # (4) stores of the rows below mc.
+        orow = pos[:mc]
+        assert np.all((orow >= 0) & (orow < R))
+        # (4) stores of the rows below mc, at their output rows.
         if gateup:
             row = c >> 3
             live = row < mc
-            q_off = (m0 + row) * N + nt * 128 + (c & 7) * 16
+            q_off = orow[np.minimum(row, mc - 1)] * N + nt * 128 + (c & 7) * 16
             assert np.all(q_off[live] + 16 <= R * N)
-            assert m0 + mc - 1 < R and (m0 + mc - 1) * (N // 128) + nt < R * (N // 128)
+            assert np.all(orow * (N // 128) + nt < R * (N // 128))
         else:
             for j in range(4):
                 t = j * 32 + r32
                 live = t < mc
-                dst = (m0 + t) * N + nt * BN + wave * 32 + g2 * 4
+                dst = orow[np.minimum(t, mc - 1)] * N + nt * BN + wave * 32 + g2 * 4
                 assert np.all(dst[live] + 3 * 8 + 4 <= R * N)
     return ran
 
@@ -184,7 +213,8 @@ def test_prefill_addresses_deepseek_prefill_chunk():
 def test_prefill_addresses_streamed_group_over_chunks():
     """The streamed path's launch pair of one group of G experts over all
     chunks: each chunk sorted on its own (offsets and chunk-relative slots),
-    row positions absolute over the chunks (the last chunk partial), the
+    an expert's tiles spanning chunks through the row tables (the last chunk
+    partial), the
     weight and scale stacks holding exactly the G experts (a group that ends
     at the ring's last slot)."""
     H, I, E, k, T, G, chunk = 7168, 2048, 256, 8, 1500, 16, 512
@@ -200,11 +230,10 @@ def test_prefill_addresses_streamed_group_over_chunks():
     assert src_all.size == R
     for e0 in (0, 112, E - G):
         window = [o[e0:e0 + G + 1] for o in offs]
-        mm = (R + 127) // 128 + G * n_chunks
+        mm = (R + 127) // 128 + G
         for gateup in (True, False):
             n = replay(gateup, G, I if gateup else H, H if gateup else I, k, T if gateup else R, window,
-                       src_all if gateup else None, R, n_chunks=n_chunks, chunk_rows=chunk * k, chunk_tokens=chunk,
-                       max_mtiles=mm)
-            segs = [(c, u) for u in range(G) for c in range(n_chunks)]
-            tiles = sum(-(-int(offs[c][e0 + u + 1] - offs[c][e0 + u]) // 128) for c, u in segs)
+                       src_all, R, n_chunks=n_chunks, chunk_rows=chunk * k, chunk_tokens=chunk, max_mtiles=mm)
+            rows_u = [sum(int(o[e0 + u + 1] - o[e0 + u]) for o in offs) for u in range(G)]
+            tiles = sum(-(-m // 128) for m in rows_u)
             assert n == tiles * (I // 128 if gateup else H // 256)
