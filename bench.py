@@ -352,6 +352,21 @@ def time_streamed(moe, torch, synth, cache, name, steps, warmup):
         compute.wait_stream(copy)
 
     copy_ms = [timed(copies, 1) for _ in range(3)]
+    # Copy-only time of each layer on its own, and where its pinned host
+    # buffers sit (pages per NUMA node).
+    per_layer = []
+    for li, host in enumerate(host_layers):
+        def one_layer(host=host):
+            with torch.cuda.stream(copy):
+                for e0 in range(0, w.n_experts, slots):
+                    n = min(slots, w.n_experts - e0)
+                    for m in range(3):
+                        ring_parts[m][: n * per_slot[0]].copy_(host[2 * m][e0:e0 + n].view(-1), non_blocking=True)
+                        scale_parts[m][: n * per_slot[1]].copy_(host[2 * m + 1][e0:e0 + n].view(-1),
+                                                               non_blocking=True)
+            compute.wait_stream(copy)
+        per_layer.append({"layer": li, "copy_only_ms": [round(timed(one_layer, 1), 3) for _ in range(2)],
+                          "host_pages_per_numa_node": numa_pages([t.data_ptr() for t in host])})
     # Kernel durations of the timed number of steps with the library's launch events.
     kern = profile_steps(moe, torch, step, steps, 4000 * n_layers)
     ctx.close()
@@ -360,7 +375,32 @@ def time_streamed(moe, torch, synth, cache, name, steps, warmup):
     out0 = outs[(n_layers - 1) % 2].cpu().numpy()
     if not np.all(np.isfinite((out0.view(np.uint16).astype(np.uint32) << 16).view(np.float32))):
         raise RuntimeError("non-finite output")
-    return w, ids_all, routes[0][1], x, ms, copy_ms, h2d_bytes, kern
+    return w, ids_all, routes[0][1], x, ms, copy_ms, h2d_bytes, kern, per_layer
+
+
+def numa_pages(ptrs):
+    """Host memory placement: pages per NUMA node of the mappings that hold the
+    given host addresses (from /proc/self/maps and /proc/self/numa_maps)."""
+    try:
+        maps = []
+        with open("/proc/self/maps") as f:
+            for line in f:
+                a, b = line.split()[0].split("-")
+                maps.append((int(a, 16), int(b, 16)))
+        nodes = {}
+        with open("/proc/self/numa_maps") as f:
+            for line in f:
+                parts = line.split()
+                nodes[int(parts[0], 16)] = {p.split("=")[0]: int(p.split("=")[1]) for p in parts[1:]
+                                            if p.startswith("N") and "=" in p}
+    except OSError:
+        return None
+    out = {}
+    for start, end in maps:
+        if any(start <= p < end for p in ptrs):
+            for n, c in nodes.get(start, {}).items():
+                out[n] = out.get(n, 0) + c
+    return out
 
 
 def cpu_baseline(torch, synth, w, x, ids, wts, budget_s, tokens):
@@ -492,8 +532,8 @@ def main_resident(args, moe, torch, synth, cache, steps, warmup, layers_n):
 
 
 def main_streamed(args, moe, torch, synth, cache, steps, warmup):
-    w, ids, wts, x, ms, copy_ms, h2d_bytes, kern = time_streamed(moe, torch, synth, cache, args.workload, steps,
-                                                                 warmup)
+    w, ids, wts, x, ms, copy_ms, h2d_bytes, kern, per_layer = time_streamed(moe, torch, synth, cache, args.workload,
+                                                                            steps, warmup)
     n_layers = max(1, w.layers)
     alg = algorithmic(w.with_tokens(w.tokens * n_layers), ids)
     gu_n, gu_ms = kern.get("ffn_prefill_gateup", (0, 0.0))
@@ -519,7 +559,8 @@ def main_streamed(args, moe, torch, synth, cache, steps, warmup):
                       "exposed_compute_ms": round(ms - copy_best, 3),
                       "gemm_kernel_ms_per_step": round((gu_ms + dn_ms) / steps, 3),
                       "gemm_TFLOPs": round((alg["gateup_flops"] + alg["down_flops"]) /
-                                           ((gu_ms + dn_ms) / steps * 1e-3) / 1e12, 1)},
+                                           ((gu_ms + dn_ms) / steps * 1e-3) / 1e12, 1),
+                      "per_layer": per_layer},
         "roofline": roof,
         "roofline_down": roof_dn,
         "kernel_ms_per_step": {k: round(tot / steps, 3) for k, (n, tot) in kern.items()},

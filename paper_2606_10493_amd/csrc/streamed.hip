@@ -12,8 +12,9 @@
 // needed).  Experts go in groups of G consecutive experts held in G
 // consecutive slots (the ring is three sub-rings, gate | up | down, each
 // [R][matrix], so a group looks like a small weight tensor to the kernels).
-// G is the largest divisor of R that gives about 2048 rows per launch, so a
-// launch fills the GPU.  Enqueue order per group g (slot group v = g mod R/G):
+// G is the largest divisor of R, at most R / 2, that gives about 2048 rows
+// per launch, so a launch fills the GPU and the ring has two slot groups or
+// more.  Enqueue order per group g (slot group v = g mod R/G):
 //   copy:    [wait OFF[v] if g >= R/G]  6 copies (W, S of gate/up/down)  record ON[v]
 //   compute: wait ON[v]  FFN(group) over every chunk's rows           record OFF[v]
 // Because copy(g) is enqueued after compute(g - R/G) and compute(g) after
@@ -197,11 +198,14 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
   // G consecutive ring slots; one GEMM launch pair covers the group's rows
   // of every chunk (an expert's tiles span chunks), so a launch sees about
   // 2048 rows per chunk of the group.  G divides R.
+  // With R > 1 there are at least two slot groups (G <= R / 2), so a group's
+  // copy overlaps the previous group's kernels (a ping-pong ring at R = 2).
   int G = 1;
   {
     const int64_t rows_per_expert = ((int64_t)L.chunk * k + E - 1) / E;
     int64_t want = (2048 + rows_per_expert - 1) / rows_per_expert;
-    if (want > R) want = R;
+    const int64_t cap = R > 1 ? R / 2 : 1;
+    if (want > cap) want = cap;
     for (int g = (int)want; g >= 1; --g)
       if (R % g == 0) { G = g; break; }
   }

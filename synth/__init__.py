@@ -73,6 +73,9 @@ WORKLOADS = {
     # streamed one after the other through a ring of 32 expert slots.
     "slp4_ring32": Workload("slp4_ring32", 7168, 2048, 256, 8, 4096, "zipf", 0.8, chunk_tokens=4096,
                             layers=4, ring_slots=32),
+    # The same stack through a ping-pong ring of two expert slots.
+    "slp4_ring2": Workload("slp4_ring2", 7168, 2048, 256, 8, 4096, "zipf", 0.8, chunk_tokens=4096,
+                           layers=4, ring_slots=2),
 }
 
 
