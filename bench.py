@@ -452,11 +452,20 @@ def main():
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
               "the multi-GPU expert-parallel path is not built", file=sys.stderr)
         sys.exit(2)
+    import synth
+    w_main = synth.WORKLOADS[args.workload]
+    if w_main.layers > 1 and "HSA_ENABLE_SDMA" not in os.environ:
+        # A stack of layers through a small ring waits for a slot before most
+        # group copies: shader copies (SDMA off) resolve those waits with
+        # shorter gaps between copies than the DMA engines (measured: 803 vs
+        # 893 ms per 4-layer step of slp4_ring32); a single layer per step is
+        # as fast or faster on the DMA engines, the runtime's default.  Set
+        # before the HIP runtime starts.
+        os.environ["HSA_ENABLE_SDMA"] = "0"
     import numpy as np  # noqa: F401
     import torch
 
     import paper_2606_10493_amd as moe
-    import synth
 
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
@@ -550,7 +559,9 @@ def main_streamed(args, moe, torch, synth, cache, steps, warmup):
         "config": {"workload": args.workload, "hidden": w.hidden, "inter": w.inter, "n_experts": w.n_experts,
                    "topk": w.topk, "tokens": w.tokens, "chunk_tokens": w.chunk_tokens, "routing": w.routing,
                    "zipf_s": w.zipf_s, "layers": n_layers, "ring_slots": w.ring_slots or w.n_experts,
-                   "entry": "moe_ffn_streamed"},
+                   "entry": "moe_ffn_streamed",
+                   "host_to_device": os.environ.get("HSA_ENABLE_SDMA") == "0" and "shader copies (HSA_ENABLE_SDMA=0)"
+                   or "runtime default (DMA engines)"},
         "streaming": {"h2d_bytes": h2d_bytes, "copy_only_ms": [round(c, 3) for c in copy_ms],
                       "h2d_GBps_copy_only": round(h2d_gbs, 2),
                       "h2d_GBps_in_layer": round(h2d_bytes / (ms * 1e-3) / 1e9, 2),

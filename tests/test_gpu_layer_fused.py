@@ -45,6 +45,7 @@ CASES = [
     (1024, 512, 16, 4, 4, "uniform", "decode"),     # h quantized in the down kernel
     (1024, 512, 16, 4, 5, "zipf", "decode"),        # separate h quantization
     (768, 384, 32, 8, 2, "zipf", "decode"),         # T * k = 16, three K blocks over four waves
+    (512, 256, 4, 4, 2, "uniform", "decode"),       # k == E, T = 2: every expert has both tokens
     (768, 384, 32, 8, 4, "zipf", "decode"),         # T * k = 32: separate down and combine
     (768, 384, 32, 8, 17, "uniform", "decode"),     # two token operands, separate down and combine
     (768, 384, 32, 8, 33, "zipf", "decode"),        # four token operands
@@ -94,13 +95,16 @@ def test_fused_layer_back_to_back_calls_share_a_workspace(moe):
         assert np.array_equal(out.cpu().numpy(), ref.out.cpu().numpy()), t
 
 
-@pytest.mark.parametrize("regime", ["decode", "prefill"])
-def test_fused_layer_reports_bad_ids(moe, regime):
+@pytest.mark.parametrize("regime,tokens", [("decode", 24), ("prefill", 24), ("decode", 2), ("decode", 3)])
+def test_fused_layer_reports_bad_ids(moe, regime, tokens):
+    """Bad routing ids are reported and parked as by the separate sort, also
+    for the smallest batches (T = 2, 3: one-row experts, fused down + combine)."""
     rg = moe.MOE_REGIME_DECODE if regime == "decode" else moe.MOE_REGIME_PREFILL
-    w, x, ids, wts = _layer_inputs(512, 256, 8, 2, 24, "uniform", seed=6)
+    w, x, ids, wts = _layer_inputs(512, 256, 8, 2, tokens, "uniform", seed=6)
     ids = ids.copy()
-    ids[3, 1] = 8          # out of range
-    ids[7, 1] = ids[7, 0]  # repeated in one token
+    bad = (0, 1) if tokens <= 3 else (3, 7)
+    ids[bad[0], 1] = 8                  # out of range
+    ids[bad[1], 1] = ids[bad[1], 0]     # repeated in one token
     wg, wu, wd = synth.weights_host(w)
     dweights = quantize_weights_gpu(moe, wg, wu, wd)
     a = _run(moe, w, x, ids, wts, dweights, rg, fused=True)
@@ -108,7 +112,7 @@ def test_fused_layer_reports_bad_ids(moe, regime):
     st = int(a.dev_status.item())
     assert st == int(b.dev_status.item())
     assert st & moe.MOE_DEV_BAD_EXPERT_ID and st & moe.MOE_DEV_DUP_EXPERT_ID
-    good = [t for t in range(w.tokens) if t not in (3, 7)]  # outputs of the bad tokens are unspecified
+    good = [t for t in range(w.tokens) if t not in bad]  # outputs of the bad tokens are unspecified
     assert np.array_equal(a.out.cpu().numpy()[good], b.out.cpu().numpy()[good])
 
 
