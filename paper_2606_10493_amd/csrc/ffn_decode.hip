@@ -189,8 +189,8 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       auto load_w = [&](int bk, v8i (&w)[G][NT]) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-          w[0][nt] = load_v8i_packed(wrow0[nt] + bk * kTileBytes);
-          if (G == 2) w[G - 1][nt] = load_v8i_packed(wrow1[nt] + bk * kTileBytes);
+          w[0][nt] = load_v8i_packed_stream(wrow0[nt] + bk * kTileBytes);
+          if (G == 2) w[G - 1][nt] = load_v8i_packed_stream(wrow1[nt] + bk * kTileBytes);
         }
       };
       // The wave's weight scales, lane i holding the scale of its i-th K
