@@ -190,6 +190,30 @@ def _run_layer(H, I, E, k, T, zipf_s, seed):
     return n_gu, n_dn, offsets
 
 
+def test_work_items_cover_every_tile_once():
+    """The work-item order (an expert's m-tiles n-tile major) is a bijection
+    onto (m-tile, n-tile) pairs, and an expert's m-tiles partition its rows,
+    for experts of 0 to 21 m-tiles and ragged tails."""
+    rng = np.random.default_rng(3)
+    m = [0, 1, 31, 128, 129, 1000, 1024, 1025, 2047, 2560] + list(rng.integers(0, 2700, 20))
+    offsets = np.concatenate([[0], np.cumsum(m)]).astype(np.int64)
+    for n_tiles in (1, 3, 16, 28):
+        start, _, desc = _describe([offsets], len(m), 10**9)
+        seen = {}
+        for item in range(int(start[-1]) * n_tiles):
+            e, first, mc, nt = _tile_of(desc, n_tiles, item)
+            assert 0 <= nt < n_tiles and 0 < mc <= BM
+            assert (e, first, nt) not in seen
+            seen[(e, first, nt)] = mc
+        for u in range(len(m)):
+            for nt in range(n_tiles):
+                pos = int(offsets[u])
+                for f, c in sorted((f, c) for (e, f, t), c in seen.items() if e == u and t == nt):
+                    assert f == pos
+                    pos += c
+                assert pos == int(offsets[u + 1])
+
+
 @pytest.mark.parametrize("H,I,E,k,T,zipf_s", [
     (256, 128, 8, 2, 16, 0.0),        # the tiny layer
     (512, 256, 16, 4, 300, 1.2),      # ragged tails, skewed routing
