@@ -45,9 +45,19 @@ DEFAULT_ALSO = "prefill8k,decode64_zipf,decode4,decode1,decode1_w8a16,router"
 # runs scaled by a plain 1 GiB copy (FETCH x2.000, WRITE x1.000), recorded in
 # the *_hbm_traffic summaries under profiles/.  Valid only while the kernel's
 # source file is the one measured (sha256 prefix).
+# Decode entries are per step (all launches of the kernel in a step), prefill
+# entries per launch (the mean over the launches of a step), as the rooflines
+# that carry them.
+_DEC, _PRE = "paper_2606_10493_amd/csrc/ffn_decode.hip", "paper_2606_10493_amd/csrc/ffn_prefill.hip"
 TRAFFIC = {
-    ("decode1", "ffn_decode_gateup"): {"bytes": 235600711, "source": "paper_2606_10493_amd/csrc/ffn_decode.hip",
-                                       "sha256_prefix": "1099a418eefb5545"},
+    ("decode1", "ffn_decode_gateup"): {"bytes": 235600484, "source": _DEC, "sha256_prefix": "2223320b6c467d26"},
+    ("decode64_zipf", "ffn_decode_gateup"): {"bytes": 4603759047, "source": _DEC, "sha256_prefix": "2223320b6c467d26"},
+    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9690456307, "source": _PRE, "sha256_prefix": "bcc2471a61dcf209"},
+    ("prefill8k", "ffn_prefill_down"): {"bytes": 6147884717, "source": _PRE, "sha256_prefix": "bcc2471a61dcf209"},
+    ("prefill32k_streamed", "ffn_prefill_gateup"): {"bytes": 1728348894, "source": _PRE,
+                                                    "sha256_prefix": "bcc2471a61dcf209"},
+    ("prefill32k_streamed", "ffn_prefill_down"): {"bytes": 1291486186, "source": _PRE,
+                                                  "sha256_prefix": "bcc2471a61dcf209"},
 }
 
 
