@@ -382,6 +382,40 @@ moe_status_t moe_ffn_streamed(moe_dims_t dims, int32_t T, int32_t chunk_tokens, 
                               hipStream_t compute, hipStream_t copy);
 
 /*
+ * The ring schedule that moe_ffn_streamed enqueues for one layer (System
+ * Design, Stream-loading Prefill: the loader's copies with their ON events,
+ * the model's launches with their OFF events), computed on the host without
+ * any GPU call, for testing and inspection.  Experts go in groups of
+ * consecutive experts in slots expert mod ring_slots; per group, in enqueue
+ * order: on the copy stream WAIT_OFF(s) for each slot s of the group that
+ * already holds an OFF record, COPY, RECORD_ON(first slot); on the compute
+ * stream WAIT_ON(first slot), LAUNCH, RECORD_OFF(s) for each slot.  A wait
+ * refers to the latest record of that event enqueued before it.
+ *
+ * op fields: WAIT_OFF, RECORD_ON, WAIT_ON, RECORD_OFF: a = slot;
+ * COPY: experts a .. a + b - 1 into slots c .. c + b - 1; LAUNCH: the FFN of
+ * experts a .. a + b - 1 read from slots c .. c + b - 1.
+ * off_recorded: host uint8[ring_slots], nonzero where a slot holds an OFF
+ * record from an earlier call on the same ring (zeros for a new context);
+ * updated in place, as a call leaves the context.  ops: host array of cap
+ * entries; *n_ops receives the count.  Returns MOE_ERR_WORKSPACE (with
+ * *n_ops set, ops and off_recorded untouched) when cap is too small, and the
+ * argument and shape errors of moe_ffn_streamed.  T == 0 gives no ops.
+ */
+typedef struct {
+  int32_t op;       /* MOE_SOP_* */
+  int32_t a, b, c;
+} moe_stream_op_t;
+#define MOE_SOP_WAIT_OFF 1
+#define MOE_SOP_COPY 2
+#define MOE_SOP_RECORD_ON 3
+#define MOE_SOP_WAIT_ON 4
+#define MOE_SOP_LAUNCH 5
+#define MOE_SOP_RECORD_OFF 6
+moe_status_t moe_stream_schedule(moe_dims_t dims, int32_t T, int32_t chunk_tokens, int32_t ring_slots,
+                                 uint8_t* off_recorded, moe_stream_op_t* ops, int32_t cap, int32_t* n_ops);
+
+/*
  * Diagnostics: per-launch kernel timing.  After moe_profile_begin(n), every
  * kernel launch of the library (at most n) is bracketed by two HIP events
  * recorded on its stream.  moe_profile_end() stops recording, waits for the

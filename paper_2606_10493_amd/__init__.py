@@ -15,7 +15,8 @@ from ._lib import (  # noqa: F401
     LIB_PATH, MoEError, lib, MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED_SHAPE,
     MOE_ERR_WORKSPACE, MOE_ERR_HIP, MOE_REGIME_AUTO, MOE_REGIME_DECODE, MOE_REGIME_PREFILL,
     MOE_DEV_BAD_EXPERT_ID, MOE_DEV_DUP_EXPERT_ID, MOE_DECODE_MAX_TOKENS, MOE_NOALLOC_SCRATCH_BYTES, MoeDims,
-    MoeRouterCfg,
+    MoeRouterCfg, MoeStreamOp, MOE_SOP_WAIT_OFF, MOE_SOP_COPY, MOE_SOP_RECORD_ON, MOE_SOP_WAIT_ON, MOE_SOP_LAUNCH,
+    MOE_SOP_RECORD_OFF,
     EXPORTED_SYMBOLS,
 )
 from ._lib import check as _check
@@ -219,6 +220,25 @@ def moe_ring_scale_bytes(dims: MoeDims, ring_slots: int) -> int:
 
 def moe_ffn_streamed_workspace(dims: MoeDims, T: int, chunk_tokens: int) -> int:
     return int(lib.moe_ffn_streamed_workspace(dims, T, chunk_tokens))
+
+
+def moe_stream_schedule(dims: MoeDims, T: int, chunk_tokens: int, ring_slots: int, off_recorded=None):
+    """The ring schedule moe_ffn_streamed enqueues for one layer (host only).
+
+    Returns (ops, off_recorded): ops a list of (op, a, b, c) tuples in
+    enqueue order (MOE_SOP_* codes, fields as in include/moe.h), and the
+    per-slot OFF-record flags the call leaves in the context (pass them to
+    the next layer's call on the same ring)."""
+    rec = (ctypes.c_uint8 * ring_slots)(*(bytes(ring_slots) if off_recorded is None else off_recorded))
+    n = ctypes.c_int32(0)
+    st = lib.moe_stream_schedule(dims, T, chunk_tokens, ring_slots, ctypes.cast(rec, ctypes.c_void_p), None, 0,
+                                 ctypes.byref(n))
+    if st not in (MOE_OK, MOE_ERR_WORKSPACE):
+        _check(st)
+    ops = (MoeStreamOp * max(n.value, 1))()
+    _check(lib.moe_stream_schedule(dims, T, chunk_tokens, ring_slots, ctypes.cast(rec, ctypes.c_void_p),
+                                   ctypes.cast(ops, ctypes.c_void_p), n.value, ctypes.byref(n)))
+    return [(o.op, o.a, o.b, o.c) for o in ops[:n.value]], bytes(rec)
 
 
 def _need_pinned(t, dtype_bytes, name):

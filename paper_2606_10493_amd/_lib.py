@@ -22,6 +22,13 @@ MOE_NOALLOC_SCRATCH_BYTES = 32 << 20
 MOE_DEV_BAD_EXPERT_ID = 1
 MOE_DEV_DUP_EXPERT_ID = 2
 
+MOE_SOP_WAIT_OFF = 1
+MOE_SOP_COPY = 2
+MOE_SOP_RECORD_ON = 3
+MOE_SOP_WAIT_ON = 4
+MOE_SOP_LAUNCH = 5
+MOE_SOP_RECORD_OFF = 6
+
 
 class MoeDims(ctypes.Structure):
     _fields_ = [("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
@@ -31,6 +38,10 @@ class MoeDims(ctypes.Structure):
 class MoeRouterCfg(ctypes.Structure):
     _fields_ = [("n_group", ctypes.c_int32), ("topk_group", ctypes.c_int32), ("routed_scaling", ctypes.c_float),
                 ("shared_expert", ctypes.c_int32)]
+
+
+class MoeStreamOp(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int32), ("a", ctypes.c_int32), ("b", ctypes.c_int32), ("c", ctypes.c_int32)]
 
 
 class MoEError(RuntimeError):
@@ -79,6 +90,7 @@ _SIGS = {
     "moe_ring_bytes": (_S, [MoeDims, _I]),
     "moe_ring_scale_bytes": (_S, [MoeDims, _I]),
     "moe_ffn_streamed_workspace": (_S, [MoeDims, _I, _I]),
+    "moe_stream_schedule": (_ST, [MoeDims, _I, _I, _I, _P, _P, _I, ctypes.POINTER(ctypes.c_int32)]),
     "moe_ffn_streamed": (_ST, [MoeDims, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S,
                                 _P, _P]),
     "moe_profile_begin": (_ST, [_I]),

@@ -85,6 +85,60 @@ StreamLayout layout(const moe_dims_t& d, int32_t T, int32_t chunk_tokens) {
   return L;
 }
 
+// Experts per slot group: the largest divisor of R, at most R / 2 when R > 1
+// (so the ring has two slot groups or more and a group's copy overlaps the
+// previous group's kernels: a ping-pong ring at R = 2), that gives about
+// 2048 rows per chunk to a launch.
+int ring_group_size(int64_t chunk_tokens, int64_t k, int64_t E, int R) {
+  const int64_t rows_per_expert = (chunk_tokens * k + E - 1) / E;
+  int64_t want = (2048 + rows_per_expert - 1) / rows_per_expert;
+  const int64_t cap = R > 1 ? R / 2 : 1;
+  if (want > cap) want = cap;
+  for (int g = (int)want; g >= 1; --g)
+    if (R % g == 0) return g;
+  return 1;
+}
+
+// The ring schedule of one layer call in enqueue order (host only).  Per
+// group of G consecutive experts e0 .. e0 + g - 1 in slots slot0 = e0 mod R
+// onwards:
+//   copy stream:    WAIT_OFF(s) for each slot s of the group that holds an
+//                   OFF record (the kernels that read it last, in this call
+//                   or an earlier one), COPY(e0, g, slot0), RECORD_ON(slot0);
+//   compute stream: WAIT_ON(slot0), LAUNCH(e0, g, slot0), RECORD_OFF(s) for
+//                   each slot of the group.
+// A wait refers to the event's latest record enqueued before it, so copy(g)
+// (enqueued after compute(g - R/G)) waits for that compute, and compute(g)
+// for copy(g).  off_recorded (one flag per slot, in/out) carries the OFF
+// records across calls on one ring.
+void plan_ring(int64_t E, int G, int R, std::vector<char>& off_recorded, std::vector<moe_stream_op_t>& ops) {
+  for (int64_t e0 = 0; e0 < E; e0 += G) {
+    const int g = (int)((E - e0) < G ? (E - e0) : G);
+    const int slot0 = (int)(e0 % R);
+    for (int s = slot0; s < slot0 + g; ++s)
+      if (off_recorded[s]) ops.push_back({MOE_SOP_WAIT_OFF, s, 0, 0});
+    ops.push_back({MOE_SOP_COPY, (int32_t)e0, g, slot0});
+    ops.push_back({MOE_SOP_RECORD_ON, slot0, 0, 0});
+    ops.push_back({MOE_SOP_WAIT_ON, slot0, 0, 0});
+    ops.push_back({MOE_SOP_LAUNCH, (int32_t)e0, g, slot0});
+    for (int s = slot0; s < slot0 + g; ++s) {
+      ops.push_back({MOE_SOP_RECORD_OFF, s, 0, 0});
+      off_recorded[s] = 1;
+    }
+  }
+}
+
+moe_status_t check_streamed_dims(const moe_dims_t& d, int32_t T, int32_t chunk_tokens, const char* who) {
+  if (d.hidden <= 0 || d.inter <= 0 || d.n_experts < 1 || d.n_experts > 1024 || d.topk < 1 || d.topk > 32 ||
+      d.topk > d.n_experts || T < 0 || chunk_tokens < 1)
+    return fail(MOE_ERR_INVALID_ARG, "%s: H=%d I=%d E=%d k=%d T=%d chunk=%d", who, d.hidden, d.inter, d.n_experts,
+                d.topk, T, chunk_tokens);
+  if (d.hidden % 256 || d.inter % kBlock)
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "%s: H must be a multiple of 256 and I of 128", who);
+  // The prefill kernels' limits (K, LDS, expert matrix size), before anything is enqueued.
+  return prefill_shape_check(d);
+}
+
 }  // namespace
 }  // namespace moe
 
@@ -136,6 +190,27 @@ extern "C" size_t moe_ffn_streamed_workspace(moe_dims_t d, int32_t T, int32_t ch
   return layout(d, T, chunk_tokens).total;
 }
 
+extern "C" moe_status_t moe_stream_schedule(moe_dims_t d, int32_t T, int32_t chunk_tokens, int32_t ring_slots,
+                                            uint8_t* off_recorded, moe_stream_op_t* ops, int32_t cap,
+                                            int32_t* n_ops) {
+  moe_status_t st = check_streamed_dims(d, T, chunk_tokens, "moe_stream_schedule");
+  if (st != MOE_OK) return st;
+  if (ring_slots < 1 || ring_slots > 4096 || !off_recorded || !n_ops || cap < 0)
+    return fail(MOE_ERR_INVALID_ARG, "moe_stream_schedule: ring_slots=%d cap=%d", ring_slots, cap);
+  *n_ops = 0;
+  if (T == 0) return MOE_OK;
+  std::vector<char> rec(ring_slots);
+  for (int s = 0; s < ring_slots; ++s) rec[s] = off_recorded[s] ? 1 : 0;
+  std::vector<moe_stream_op_t> plan;
+  plan_ring(d.n_experts, ring_group_size(chunk_tokens, d.topk, d.n_experts, ring_slots), ring_slots, rec, plan);
+  *n_ops = (int32_t)plan.size();
+  if (!ops || cap < (int32_t)plan.size())
+    return fail(MOE_ERR_WORKSPACE, "moe_stream_schedule: %d ops, room for %d", (int)plan.size(), cap);
+  for (size_t i = 0; i < plan.size(); ++i) ops[i] = plan[i];
+  for (int s = 0; s < ring_slots; ++s) off_recorded[s] = (uint8_t)rec[s];
+  return MOE_OK;
+}
+
 extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_tokens, const uint16_t* x_bf16,
                                          const int32_t* topk_ids, const float* topk_w, const uint8_t* host_w_gate,
                                          const float* host_s_gate, const uint8_t* host_w_up, const float* host_s_up,
@@ -143,16 +218,9 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
                                          float* dev_ring_scales, moe_stream_ctx_t ctx, uint16_t* out_bf16,
                                          int32_t* dev_status, void* ws, size_t ws_bytes, hipStream_t compute,
                                          hipStream_t copy) {
-  if (d.hidden <= 0 || d.inter <= 0 || d.n_experts < 1 || d.n_experts > 1024 || d.topk < 1 || d.topk > 32 ||
-      d.topk > d.n_experts || T < 0 || chunk_tokens < 1)
-    return fail(MOE_ERR_INVALID_ARG, "moe_ffn_streamed: H=%d I=%d E=%d k=%d T=%d chunk=%d", d.hidden, d.inter,
-                d.n_experts, d.topk, T, chunk_tokens);
-  if (d.hidden % 256 || d.inter % kBlock)
-    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_ffn_streamed: H must be a multiple of 256 and I of 128");
-  if (!ctx) return fail(MOE_ERR_INVALID_ARG, "moe_ffn_streamed: null stream context");
-  // The prefill kernels' limits (K, LDS, expert matrix size), before anything is enqueued.
-  moe_status_t st0 = prefill_shape_check(d);
+  moe_status_t st0 = check_streamed_dims(d, T, chunk_tokens, "moe_ffn_streamed");
   if (st0 != MOE_OK) return st0;
+  if (!ctx) return fail(MOE_ERR_INVALID_ARG, "moe_ffn_streamed: null stream context");
   if (T == 0) return MOE_OK;
   if ((int64_t)T * d.topk > 0x7fffffff) return fail(MOE_ERR_UNSUPPORTED_SHAPE, "moe_ffn_streamed: T*k overflows");
   if (!x_bf16 || !topk_ids || !topk_w || !host_w_gate || !host_s_gate || !host_w_up || !host_s_up || !host_w_down ||
@@ -196,18 +264,13 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
 
   // Experts are streamed and run in groups of G consecutive experts, held in
   // G consecutive ring slots; one GEMM launch pair covers the group's rows
-  // of every chunk (an expert's tiles span chunks), so a launch sees about
-  // 2048 rows per chunk of the group.  G divides R.
-  // With R > 1 there are at least two slot groups (G <= R / 2), so a group's
-  // copy overlaps the previous group's kernels (a ping-pong ring at R = 2).
-  int G = 1;
+  // of every chunk (an expert's tiles span chunks).  The schedule
+  // (plan_ring) is executed op by op.
+  const int G = ring_group_size(L.chunk, k, E, R);
+  std::vector<moe_stream_op_t> plan;
   {
-    const int64_t rows_per_expert = ((int64_t)L.chunk * k + E - 1) / E;
-    int64_t want = (2048 + rows_per_expert - 1) / rows_per_expert;
-    const int64_t cap = R > 1 ? R / 2 : 1;
-    if (want > cap) want = cap;
-    for (int g = (int)want; g >= 1; --g)
-      if (R % g == 0) { G = g; break; }
+    std::vector<char> rec(ctx->off_recorded);
+    plan_ring(E, G, R, rec, plan);
   }
   uint8_t* ring_gate = dev_ring;
   uint8_t* ring_up = dev_ring + (size_t)R * wmat;
@@ -215,43 +278,59 @@ extern "C" moe_status_t moe_ffn_streamed(moe_dims_t d, int32_t T, int32_t chunk_
   float* ring_sgate = dev_ring_scales;
   float* ring_sup = dev_ring_scales + (size_t)R * smat;
   float* ring_sdown = dev_ring_scales + 2 * (size_t)R * smat;
-  for (int64_t e0 = 0; e0 < E; e0 += G) {
-    const int g_here = (int)((E - e0) < G ? (E - e0) : G);
-    const int slot0 = (int)(e0 % R);
-    // Loader: each slot of the group is free once the kernels that read it last ran.
-    for (int s = slot0; s < slot0 + g_here; ++s)
-      if (ctx->off_recorded[s] && hipStreamWaitEvent(copy, ctx->off[s], 0) != hipSuccess)
-        return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait OFF");
-    const size_t nb_w = (size_t)g_here * wmat, nb_s = (size_t)g_here * smat * sizeof(float);
-    if (hipMemcpyAsync(ring_gate + slot0 * wmat, host_w_gate + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
-        hipMemcpyAsync(ring_up + slot0 * wmat, host_w_up + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
-        hipMemcpyAsync(ring_down + slot0 * wmat, host_w_down + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
-        hipMemcpyAsync(ring_sgate + slot0 * smat, host_s_gate + e0 * smat, nb_s, hipMemcpyHostToDevice, copy) ||
-        hipMemcpyAsync(ring_sup + slot0 * smat, host_s_up + e0 * smat, nb_s, hipMemcpyHostToDevice, copy) ||
-        hipMemcpyAsync(ring_sdown + slot0 * smat, host_s_down + e0 * smat, nb_s, hipMemcpyHostToDevice, copy))
-      return fail(MOE_ERR_HIP, "moe_ffn_streamed: copy of experts %lld..", (long long)e0);
-    if (hipEventRecord(ctx->on[slot0], copy) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record ON");
-    // Model: the group's rows of every chunk in one launch pair.
-    if (hipStreamWaitEvent(compute, ctx->on[slot0], 0) != hipSuccess)
-      return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait ON");
-    PrefillRows rows{};
-    rows.offsets = offsets + e0;
-    rows.off_stride = E + 1;
-    rows.n_units = g_here;
-    rows.n_chunks = (int)L.n_chunks;
-    rows.chunk_rows = L.chunk * k;
-    rows.chunk_tokens = (int)L.chunk;
-    rows.tokens = T;
-    rows.rows = (int64_t)T * k;
-    rows.max_mtiles = (rows.rows + 127) / 128 + g_here;
-    const moe_dims_t vd{d.hidden, d.inter, g_here, d.topk};
-    st = run_ffn_prefill_view(vd, rows, qx, sx, sorted_src, ring_gate + slot0 * wmat, ring_sgate + slot0 * smat,
-                              ring_up + slot0 * wmat, ring_sup + slot0 * smat, ring_down + slot0 * wmat,
-                              ring_sdown + slot0 * smat, y, qh, sh, tiles, compute);
-    if (st != MOE_OK) return st;
-    for (int s = slot0; s < slot0 + g_here; ++s) {
-      if (hipEventRecord(ctx->off[s], compute) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record OFF");
-      ctx->off_recorded[s] = 1;
+  for (const moe_stream_op_t& op : plan) {
+    switch (op.op) {
+      case MOE_SOP_WAIT_OFF:  // loader: the slot is free once the kernels that read it last ran
+        if (hipStreamWaitEvent(copy, ctx->off[op.a], 0) != hipSuccess)
+          return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait OFF");
+        break;
+      case MOE_SOP_COPY: {
+        const int64_t e0 = op.a;
+        const int slot0 = op.c;
+        const size_t nb_w = (size_t)op.b * wmat, nb_s = (size_t)op.b * smat * sizeof(float);
+        if (hipMemcpyAsync(ring_gate + slot0 * wmat, host_w_gate + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
+            hipMemcpyAsync(ring_up + slot0 * wmat, host_w_up + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
+            hipMemcpyAsync(ring_down + slot0 * wmat, host_w_down + e0 * wmat, nb_w, hipMemcpyHostToDevice, copy) ||
+            hipMemcpyAsync(ring_sgate + slot0 * smat, host_s_gate + e0 * smat, nb_s, hipMemcpyHostToDevice, copy) ||
+            hipMemcpyAsync(ring_sup + slot0 * smat, host_s_up + e0 * smat, nb_s, hipMemcpyHostToDevice, copy) ||
+            hipMemcpyAsync(ring_sdown + slot0 * smat, host_s_down + e0 * smat, nb_s, hipMemcpyHostToDevice, copy))
+          return fail(MOE_ERR_HIP, "moe_ffn_streamed: copy of experts %lld..", (long long)e0);
+        break;
+      }
+      case MOE_SOP_RECORD_ON:
+        if (hipEventRecord(ctx->on[op.a], copy) != hipSuccess) return fail(MOE_ERR_HIP, "moe_ffn_streamed: record ON");
+        break;
+      case MOE_SOP_WAIT_ON:
+        if (hipStreamWaitEvent(compute, ctx->on[op.a], 0) != hipSuccess)
+          return fail(MOE_ERR_HIP, "moe_ffn_streamed: wait ON");
+        break;
+      case MOE_SOP_LAUNCH: {  // model: the group's rows of every chunk in one launch pair
+        const int64_t e0 = op.a;
+        const int g_here = op.b, slot0 = op.c;
+        PrefillRows rows{};
+        rows.offsets = offsets + e0;
+        rows.off_stride = E + 1;
+        rows.n_units = g_here;
+        rows.n_chunks = (int)L.n_chunks;
+        rows.chunk_rows = L.chunk * k;
+        rows.chunk_tokens = (int)L.chunk;
+        rows.tokens = T;
+        rows.rows = (int64_t)T * k;
+        rows.max_mtiles = (rows.rows + 127) / 128 + g_here;
+        const moe_dims_t vd{d.hidden, d.inter, g_here, d.topk};
+        st = run_ffn_prefill_view(vd, rows, qx, sx, sorted_src, ring_gate + slot0 * wmat, ring_sgate + slot0 * smat,
+                                  ring_up + slot0 * wmat, ring_sup + slot0 * smat, ring_down + slot0 * wmat,
+                                  ring_sdown + slot0 * smat, y, qh, sh, tiles, compute);
+        if (st != MOE_OK) return st;
+        break;
+      }
+      case MOE_SOP_RECORD_OFF:
+        if (hipEventRecord(ctx->off[op.a], compute) != hipSuccess)
+          return fail(MOE_ERR_HIP, "moe_ffn_streamed: record OFF");
+        ctx->off_recorded[op.a] = 1;
+        break;
+      default:
+        return fail(MOE_ERR_INVALID_ARG, "moe_ffn_streamed: bad schedule op %d", op.op);
     }
   }
 
