@@ -61,7 +61,7 @@ StreamLayout layout(const moe_dims_t& d, int32_t T, int32_t chunk_tokens) {
   StreamLayout L{};
   const int64_t H = d.hidden, I = d.inter, E = d.n_experts, k = d.topk;
   L.chunk = chunk_tokens;
-  L.n_chunks = (T + chunk_tokens - 1) / chunk_tokens;
+  L.n_chunks = ((int64_t)T + chunk_tokens - 1) / chunk_tokens;
   const int64_t ck = (int64_t)chunk_tokens * k;  // rows of one chunk
   size_t off = 0;
   auto take = [&](size_t bytes) {
