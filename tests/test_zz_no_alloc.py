@@ -80,3 +80,49 @@ def test_noalloc_rejects_a_call_beyond_its_scratch(moe, layer):
         moe.moe_ffn_layer_noalloc(d, T, moe.MOE_REGIME_PREFILL, bf16_dev(x), torch.from_numpy(ids).cuda(),
                                   torch.from_numpy(wts).cuda(), *layer, out)
     assert ei.value.status == moe.MOE_ERR_WORKSPACE and "scratch" in str(ei.value)
+
+
+@pytest.mark.parametrize("regime_name,T", [("decode", 4), ("prefill", 100)])
+def test_noalloc_call_replays_from_a_hip_graph(moe, layer, regime_name, T):
+    """The callers this entry point is for: one call captured in a HIP graph
+    (nothing allocated inside it), replayed three times.  Before each replay
+    the static input gets new activations, and eager work runs on the same
+    GPU (moe_ffn_layer with its own workspace on the new input, for the
+    reference, and a noalloc call of another size, which rewrites the
+    scratch array); every replay must equal the reference bit for bit."""
+    import numpy as np
+
+    regime = moe.MOE_REGIME_DECODE if regime_name == "decode" else moe.MOE_REGIME_PREFILL
+    d = moe.MoeDims(W.hidden, W.inter, W.n_experts, W.topk)
+    x0, ids, wts = _inputs(T)
+    dx, dids, dw = bf16_dev(x0), torch.from_numpy(ids).cuda(), torch.from_numpy(wts).cuda()
+    out = torch.empty((T, W.hidden), dtype=torch.int16, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    moe.moe_ffn_layer_noalloc(d, T, regime, dx, dids, dw, *layer, out, st)  # first call on the device: set-up
+    torch.cuda.synchronize()
+    log(f"noalloc graph {regime_name}: capturing T={T}")
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(g, stream=side):
+        moe.moe_ffn_layer_noalloc(d, T, regime, dx, dids, dw, *layer, out, st)
+    torch.cuda.synchronize()
+
+    xo, ido, wo = _inputs(3)
+    other = torch.empty((3, W.hidden), dtype=torch.int16, device="cuda")
+    ws = torch.empty(max(256, moe.moe_ffn_layer_workspace(d, T, regime)), dtype=torch.uint8, device="cuda")
+    rng = np.random.default_rng(17)
+    for rep in range(3):
+        x = synth.bf16_bits_from_f32(rng.standard_normal((T, W.hidden)).astype(np.float32) * (1.0 + rep))
+        dx.copy_(bf16_dev(x))
+        ref = torch.empty_like(out)
+        st_ref = torch.zeros(1, dtype=torch.int32, device="cuda")
+        moe.moe_ffn_layer(d, T, regime, dx, dids, dw, *layer, ref, st_ref, ws)
+        moe.moe_ffn_layer_noalloc(d, 3, moe.MOE_REGIME_DECODE, bf16_dev(xo), torch.from_numpy(ido).cuda(),
+                                  torch.from_numpy(wo).cuda(), *layer, other)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        log(f"noalloc graph {regime_name}: replay {rep}")
+        assert int(st.item()) == 0 and int(st_ref.item()) == 0
+        assert torch.equal(out, ref), f"replay {rep} differs from the eager call on the same input"
