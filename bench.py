@@ -291,10 +291,11 @@ def time_streamed(moe, torch, synth, cache, name, steps, warmup):
     import numpy as np
     w = synth.WORKLOADS[name]
     n_layers = max(1, w.layers)
+    n_sets = w.weight_sets or n_layers  # distinct weight layers; layer l uses set l mod n_sets
     x = synth.activations(w)
     routes = [synth.routing(w, layer=l) for l in range(n_layers)]
     host_layers = []
-    for l in range(n_layers):
+    for l in range(n_sets):
         dev_layer = cache.get(w, l)
         log(f"pinning a host copy of weight layer {l}")
         host = []
@@ -325,8 +326,8 @@ def time_streamed(moe, torch, synth, cache, name, steps, warmup):
     def step(_i=0):
         inp = dx
         for l in range(n_layers):
-            moe.moe_ffn_streamed(dims, w.chunk_tokens, inp, dids[l], dws[l], host_layers[l], ring, ring_s, ctx,
-                                 outs[l % 2], status, ws, compute, copy)
+            moe.moe_ffn_streamed(dims, w.chunk_tokens, inp, dids[l], dws[l], host_layers[l % n_sets], ring, ring_s,
+                                 ctx, outs[l % 2], status, ws, compute, copy)
             inp = outs[l % 2]
 
     def timed(fn, n):
@@ -352,7 +353,7 @@ def time_streamed(moe, torch, synth, cache, name, steps, warmup):
 
     def copies():
         with torch.cuda.stream(copy):
-            for host in host_layers:
+            for host in (host_layers[l % n_sets] for l in range(n_layers)):
                 for e0 in range(0, w.n_experts, slots):
                     n = min(slots, w.n_experts - e0)
                     for m in range(3):
@@ -378,9 +379,9 @@ def time_streamed(moe, torch, synth, cache, name, steps, warmup):
         per_layer.append({"layer": li, "copy_only_ms": [round(timed(one_layer, 1), 3) for _ in range(2)],
                           "host_pages_per_numa_node": numa_pages([t.data_ptr() for t in host])})
     # Kernel durations of the timed number of steps with the library's launch events.
-    kern = profile_steps(moe, torch, step, steps, 4000 * n_layers)
+    kern = profile_steps(moe, torch, step, steps, max(4000, 200 * n_layers))
     ctx.close()
-    h2d_bytes = sum(t.numel() * t.element_size() for host in host_layers for t in host)
+    h2d_bytes = sum(t.numel() * t.element_size() for l in range(n_layers) for t in host_layers[l % n_sets])
     ids_all = np.concatenate([ids for ids, _ in routes])
     out0 = outs[(n_layers - 1) % 2].cpu().numpy()
     if not np.all(np.isfinite((out0.view(np.uint16).astype(np.uint32) << 16).view(np.float32))):
@@ -560,6 +561,9 @@ def main_streamed(args, moe, torch, synth, cache, steps, warmup):
     copy_best = min(copy_ms)
     h2d_gbs = h2d_bytes / (copy_best * 1e-3) / 1e9
     note = "launches per step: one per expert group (over all 4096-token chunks)"
+    if os.environ.get("HSA_ENABLE_SDMA") == "0":
+        note += ("; with shader copies the copy kernels share the compute units with the expert kernels, so "
+                 "these launch durations include waiting for them")
     roof = prefill_roofline(alg["gateup_flops"] * steps, kern, "ffn_prefill_gateup", args.workload, note)
     roof_dn = prefill_roofline(alg["down_flops"] * steps, kern, "ffn_prefill_down", args.workload, note)
     res = {
@@ -569,6 +573,7 @@ def main_streamed(args, moe, torch, synth, cache, steps, warmup):
         "config": {"workload": args.workload, "hidden": w.hidden, "inter": w.inter, "n_experts": w.n_experts,
                    "topk": w.topk, "tokens": w.tokens, "chunk_tokens": w.chunk_tokens, "routing": w.routing,
                    "zipf_s": w.zipf_s, "layers": n_layers, "ring_slots": w.ring_slots or w.n_experts,
+                   "weight_sets": w.weight_sets or n_layers,
                    "entry": "moe_ffn_streamed",
                    "host_to_device": os.environ.get("HSA_ENABLE_SDMA") == "0" and "shader copies (HSA_ENABLE_SDMA=0)"
                    or "runtime default (DMA engines)"},

@@ -53,6 +53,7 @@ class Workload:
     seed: int = 0
     layers: int = 1         # >1: a stack of layers streamed through one ring
     ring_slots: int = 0     # streamed: ring size in experts (0: all experts of a layer)
+    weight_sets: int = 0    # stacks: distinct weight layers, layer l using set l mod weight_sets (0: one per layer)
 
     def with_tokens(self, t: int) -> "Workload":
         return dataclasses.replace(self, tokens=t)
@@ -76,6 +77,13 @@ WORKLOADS = {
     # The same stack through a ping-pong ring of two expert slots.
     "slp4_ring2": Workload("slp4_ring2", 7168, 2048, 256, 8, 4096, "zipf", 0.8, chunk_tokens=4096,
                            layers=4, ring_slots=2),
+    # The 58 routed-expert layers of a DeepSeek-V3-class model streamed
+    # through one ring of 32 expert slots, each layer with its own routing;
+    # the weights cycle over 4 drawn layers (58 distinct layers would need
+    # 654 GB of pinned host memory), so every call still copies its whole
+    # 11.28 GB over the host link.
+    "slp58_ring32": Workload("slp58_ring32", 7168, 2048, 256, 8, 4096, "zipf", 0.8, chunk_tokens=4096,
+                             layers=58, ring_slots=32, weight_sets=4),
 }
 
 
