@@ -120,3 +120,59 @@ def test_layer_on_crafted_scales(moe, regime, fused):
         f"err {errs.max():.3e}; token output maxima 2^{np.log2(mags[mags > 0]).min():.0f}.."
         f"2^{np.log2(mags.max()):.0f}")
     assert errs.max() <= TOL
+
+
+def _crafted_fullsize(seed=12, E=4, K=2):
+    """The same construction at the DeepSeek-V3 widths (H = 7168, I = 2048)
+    over 4 experts: gate/up run 56 K blocks (the prefill GEMM's 16-slot
+    row-scale batch, the decode kernel's K halves), down 16."""
+    h, i = 7168, 2048
+    rng = np.random.default_rng(seed)
+
+    def blocks(shape):
+        w = 0.02 * rng.standard_normal(shape, dtype=np.float32)
+        sc = np.exp2(rng.integers(-8, 9, (shape[0], shape[1] // 128, shape[2] // 128))).astype(np.float32)
+        w *= np.repeat(np.repeat(sc, 128, axis=1), 128, axis=2)
+        return w
+
+    wg, wu, wd = blocks((E, i, h)), blocks((E, i, h)), blocks((E, h, i))
+    wg[1, :128, -128:] = 0.0
+    return (wg, wu, wd), rng
+
+
+@pytest.fixture(scope="module")
+def fullsize(moe):
+    log("crafted full-width layer: drawing and quantizing 4 experts at H=7168, I=2048")
+    (wg, wu, wd), rng = _crafted_fullsize()
+    ow = oracle.prepare_weights(wg, wu, wd)
+    dweights = quantize_weights_gpu(moe, wg, wu, wd)
+    for j, (dq, rq) in enumerate(zip(dweights, ow)):
+        assert np.array_equal(dq.cpu().numpy(), pack_reference(rq) if j % 2 == 0 else rq)
+    return ow, dweights, rng
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("regime,tokens", [("decode", 48), ("prefill", 300)])
+def test_fullwidth_layer_on_crafted_scales(moe, fullsize, regime, tokens):
+    """48 decode tokens (about 24 rows per expert) and 300 prefill tokens
+    (150 rows per expert: two m-tiles each), one moe_ffn_layer call each,
+    every token against the oracle with the per-token bound."""
+    ow, dweights, rng0 = fullsize
+    rng = np.random.default_rng(100 + tokens)
+    h, i, e, k = 7168, 2048, 4, 2
+    x = rng.standard_normal((tokens, h)).astype(np.float32)
+    x *= np.repeat(np.exp2(rng.integers(-16, 17, (tokens, h // 128))).astype(np.float32), 128, axis=1)
+    x[0] = 0.0
+    xb = synth.bf16_bits_from_f32(x)
+    ids = np.stack([rng.choice(e, k, replace=False) for _ in range(tokens)]).astype(np.int32)
+    wts = rng.uniform(0.1, 1.0, (tokens, k)).astype(np.float32)
+    rg = moe.MOE_REGIME_DECODE if regime == "decode" else moe.MOE_REGIME_PREFILL
+    log(f"crafted full-width {regime}: T={tokens}")
+    ref = oracle.bf16_to_f32(oracle.moe_layer(xb, ids, wts, ow))
+    buf = moe.MoELayerBuffers(h, i, e, k, tokens, rg, fused=True)
+    moe.run_layer(buf, bf16_dev(xb), to_dev(ids), to_dev(wts), dweights)
+    torch.cuda.synchronize()
+    assert int(buf.dev_status.item()) == 0
+    errs = _per_token_err(bits_to_f32(buf.out), ref)
+    log(f"crafted full-width {regime}: worst token {int(errs.argmax())} err {errs.max():.3e}")
+    assert errs.max() <= TOL
