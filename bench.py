@@ -54,9 +54,9 @@ TRAFFIC = {
     ("decode64_zipf", "ffn_decode_gateup"): {"bytes": 4603759047, "source": _DEC, "sha256_prefix": "2223320b6c467d26"},
     ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9690456307, "source": _PRE, "sha256_prefix": "bcc2471a61dcf209"},
     ("prefill8k", "ffn_prefill_down"): {"bytes": 6147884717, "source": _PRE, "sha256_prefix": "bcc2471a61dcf209"},
-    ("prefill32k_streamed", "ffn_prefill_gateup"): {"bytes": 1728348894, "source": _PRE,
+    ("prefill32k_streamed", "ffn_prefill_gateup"): {"bytes": 1717477867, "source": _PRE,
                                                     "sha256_prefix": "bcc2471a61dcf209"},
-    ("prefill32k_streamed", "ffn_prefill_down"): {"bytes": 1291486186, "source": _PRE,
+    ("prefill32k_streamed", "ffn_prefill_down"): {"bytes": 1288853330, "source": _PRE,
                                                   "sha256_prefix": "bcc2471a61dcf209"},
 }
 
