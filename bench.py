@@ -41,13 +41,12 @@ METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
 DEFAULT_WORKLOAD = "prefill32k_streamed"
 DEFAULT_ALSO = "prefill8k,decode64_zipf,decode4,decode1,decode1_w8a16,router"
 
-# HBM bytes per launch of a kernel, from rocprofv3 FETCH_SIZE and WRITE_SIZE
-# runs scaled by a plain 1 GiB copy (FETCH x2.000, WRITE x1.000), recorded in
-# the *_hbm_traffic summaries under profiles/.  Valid only while the kernel's
-# source file is the one measured (sha256 prefix).
-# Decode entries are per step (all launches of the kernel in a step), prefill
-# entries per launch (the mean over the launches of a step), as the rooflines
-# that carry them.
+# HBM bytes moved by a kernel, from rocprofv3 FETCH_SIZE and WRITE_SIZE runs
+# scaled by a plain 1 GiB copy (FETCH x2.000, WRITE x1.000), recorded in the
+# profiles/ summaries of each workload.  Valid only while the kernel's source
+# file is the one measured (sha256 prefix).  Decode entries are per step (all
+# launches of the kernel in a step), prefill entries per launch (the mean over
+# the launches of a step), as the rooflines that carry them.
 _DEC, _PRE = "paper_2606_10493_amd/csrc/ffn_decode.hip", "paper_2606_10493_amd/csrc/ffn_prefill.hip"
 TRAFFIC = {
     ("decode1", "ffn_decode_gateup"): {"bytes": 235600484, "source": _DEC, "sha256_prefix": "2223320b6c467d26"},
