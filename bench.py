@@ -37,6 +37,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 FP8_PEAK_TFLOPS = 5000.0     # MI355X dense FP8 MFMA
+BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA (the router's logits GEMM)
 METRIC = "FP8 MoE expert-FFN tokens/s; decode HBM GB/s; prefill FP8 MFMA TFLOPS"
 DEFAULT_WORKLOAD = "prefill32k_streamed"
 DEFAULT_ALSO = "prefill8k,decode64_zipf,decode4,decode1,decode1_w8a16,router"
@@ -51,6 +52,9 @@ _DEC, _PRE = "paper_2606_10493_amd/csrc/ffn_decode.hip", "paper_2606_10493_amd/c
 TRAFFIC = {
     ("decode1", "ffn_decode_gateup"): {"bytes": 235600484, "source": _DEC, "sha256_prefix": "2223320b6c467d26"},
     ("decode64_zipf", "ffn_decode_gateup"): {"bytes": 4603759047, "source": _DEC, "sha256_prefix": "2223320b6c467d26"},
+    ("decode4", "ffn_decode_gateup"): {"bytes": 942042780, "source": _DEC, "sha256_prefix": "2223320b6c467d26"},
+    ("decode1_w8a16", "ffn_decode_w8a16_gateup"): {"bytes": 235617550, "source": _DEC,
+                                                   "sha256_prefix": "2223320b6c467d26"},
     ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9690456307, "source": _PRE, "sha256_prefix": "bcc2471a61dcf209"},
     ("prefill8k", "ffn_prefill_down"): {"bytes": 6147884717, "source": _PRE, "sha256_prefix": "bcc2471a61dcf209"},
     ("prefill32k_streamed", "ffn_prefill_gateup"): {"bytes": 1717477867, "source": _PRE,
@@ -245,7 +249,8 @@ def resident_summary(moe, torch, synth, cache, extra, steps, warmup, layers_n, f
         us = 1000.0 * tot / steps
         ach = alg["gateup_bytes"] / (us * 1e-6) / 1e9   # same weight bytes; activations counted as in W8A8
         res["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                           "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+                           "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                           "traffic": measured_traffic(extra, dom)}
     elif decode:
         res["roofline"] = decode_roofline(alg, kern, steps, base_name)
         res["layer_frac_hbm"] = round(alg["layer_weight_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
@@ -503,7 +508,14 @@ def main():
     for extra in [a for a in args.also.split(",") if a and a != args.workload]:
         log(f"also: {extra}")
         if extra == "router":
-            also["router"] = {"tokens": w.tokens, "kernel_us": time_router(moe, torch, synth, w, r_steps, r_warm)}
+            kus = time_router(moe, torch, synth, w, r_steps, r_warm)
+            also["router"] = {"tokens": w.tokens, "kernel_us": kus}
+            if kus.get("router_logits"):
+                # logits = x W_r^T: 2 T H E FLOPs of bf16 MFMA (the selection is latency-bound and small)
+                tf = 2.0 * w.tokens * w.hidden * w.n_experts / (kus["router_logits"] * 1e-6) / 1e12
+                also["router"]["roofline"] = {"kernel": "router_logits", "bound": "mfma", "achieved": round(tf, 1),
+                                              "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                              "frac": round(tf / BF16_PEAK_TFLOPS, 4), "traffic": None}
             continue
         base = extra[:-len("_w8a16")] if extra.endswith("_w8a16") else extra
         if synth.WORKLOADS[base].chunk_tokens:
