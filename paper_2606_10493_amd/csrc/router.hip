@@ -19,8 +19,9 @@
 //   router_logits_tiled_kernel (256 tokens or more): 128 x 256 tiles through
 //     LDS, also over K slices, the same partial layout.
 //   router_select_kernel: one wave per token sums the KS partials in slice
-//     order, applies the sigmoid and the bias, keeps the best groups, finds
-//     the k-th largest key by a radix select over its bits and orders the k
+//     order, applies the sigmoid and the bias, keeps the best groups, and
+//     takes the k largest keys in k argmax rounds (k <= 16), or finds the
+//     k-th largest key by a radix select over its bits and orders the k
 //     chosen experts; lanes 0 .. k-1 write ids and weights.
 #include "common.h"
 
@@ -33,6 +34,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kRouterMaxExperts = 1024; // one selection thread per expert
 constexpr int kRouterMaxGroups = 64;
 constexpr int kRouterMinChunk = 128;    // K elements per logits workgroup at least
+constexpr int kArgmaxMaxK = 16;         // selection by k argmax rounds up to this k, a radix select beyond
 
 __global__ __launch_bounds__(256) void router_logits_kernel(const uint16_t* __restrict__ x, int T, int H,
                                                             const uint16_t* __restrict__ w, int E, int kchunk,
@@ -154,11 +156,15 @@ __device__ __forceinline__ bool beats(float va, int ia, float vb, int ib) {
 //   * group scores: for each group the two largest keys, by a wave
 //     reduction of (largest, second) pairs; lane g ranks group g against
 //     the others and the topk_group best are kept;
-//   * the k-th largest kept key (in the (value, index) order) by a radix
-//     select over the 32 bits of the keys mapped to ordered integers: each
-//     bit costs PER ballots, with no per-expert comparisons against all E;
-//   * the k chosen experts (keys above the k-th, and the lowest indices of
-//     those equal to it) are ordered among themselves through LDS.
+//   * k <= 16: k rounds of a wave argmax over (key, index), each taking the
+//     largest remaining key, which gives the experts in slot order (k = 8:
+//     8 rounds of 6 shuffle steps against 32 dependent radix steps plus an
+//     ordering pass);
+//   * larger k: the k-th largest kept key (in the (value, index) order) by a
+//     radix select over the 32 bits of the keys mapped to ordered integers:
+//     each bit costs PER ballots, with no per-expert comparisons against all
+//     E; the k chosen experts (keys above the k-th, and the lowest indices of
+//     those equal to it) are then ordered among themselves through LDS.
 // ids / wts rows have k_out = k (+1 with a shared expert) columns.
 __device__ __forceinline__ uint32_t ordered_bits(float v) {
   const uint32_t u = __float_as_uint(v);
@@ -297,6 +303,63 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
       const int kept = __shfl(kept_group, e < E ? e / epg : 0);
       if (!kept) key[i] = -INFINITY;
     }
+  }
+
+  if (k <= kArgmaxMaxK) {
+    // Small k: k rounds of a wave argmax over (key, expert index), each round
+    // taking the largest remaining key (the lower index on equal keys), so
+    // the experts come out in slot order (decreasing key) with no ordering
+    // step; lane j keeps slot j's expert and sigmoid score.
+    int my_e = 0;
+    float my_s = 0.0f;
+    for (int j = 0; j < k; ++j) {
+      float bk = key[0];
+      int be = lane;
+#pragma unroll
+      for (int i = 1; i < PER; ++i)
+        if (key[i] > bk) {  // registers hold increasing indices: ties keep the lower one
+          bk = key[i];
+          be = lane + 64 * i;
+        }
+#pragma unroll
+      for (int m = 1; m < 64; m <<= 1) {  // butterfly: every lane ends with the same best
+        const float ok = __shfl_xor(bk, m);
+        const int oe = __shfl_xor(be, m);
+        if (beats(ok, oe, bk, be)) {
+          bk = ok;
+          be = oe;
+        }
+      }
+      float sv = s[0];
+#pragma unroll
+      for (int i = 1; i < PER; ++i)
+        if ((be >> 6) == i) sv = s[i];
+      sv = __shfl(sv, be & 63);
+      if (lane == j) {
+        my_e = be;
+        my_s = sv;
+      }
+#pragma unroll
+      for (int i = 0; i < PER; ++i)
+        if (lane + 64 * i == be) key[i] = -INFINITY;
+    }
+    if (lane < k) {
+      ids[t * k_out + lane] = my_e;
+      sel_s[slot][lane] = my_s;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (lane < k) {
+      float total = 0.0f;
+      for (int j = 0; j < k; ++j) total += sel_s[slot][j];
+      wts[t * k_out + lane] = (my_s / total) * scaling;
+    }
+    if (shared >= 0 && lane == 0) {
+      ids[t * k_out + k] = shared;
+      wts[t * k_out + k] = 1.0f;
+    }
+    return;
   }
 
   // Radix select of the k-th largest key: prefix of the ordered bits, and
