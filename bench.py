@@ -55,12 +55,12 @@ TRAFFIC = {
     ("decode4", "ffn_decode_gateup"): {"bytes": 942042780, "source": _DEC, "sha256_prefix": "2223320b6c467d26"},
     ("decode1_w8a16", "ffn_decode_w8a16_gateup"): {"bytes": 235617550, "source": _DEC,
                                                    "sha256_prefix": "2223320b6c467d26"},
-    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9690456307, "source": _PRE, "sha256_prefix": "bcc2471a61dcf209"},
-    ("prefill8k", "ffn_prefill_down"): {"bytes": 6147884717, "source": _PRE, "sha256_prefix": "bcc2471a61dcf209"},
-    ("prefill32k_streamed", "ffn_prefill_gateup"): {"bytes": 1717477867, "source": _PRE,
-                                                    "sha256_prefix": "bcc2471a61dcf209"},
-    ("prefill32k_streamed", "ffn_prefill_down"): {"bytes": 1288853330, "source": _PRE,
-                                                  "sha256_prefix": "bcc2471a61dcf209"},
+    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9697626778, "source": _PRE, "sha256_prefix": "7fb3d6681d45a9dc"},
+    ("prefill8k", "ffn_prefill_down"): {"bytes": 6157209830, "source": _PRE, "sha256_prefix": "7fb3d6681d45a9dc"},
+    ("prefill32k_streamed", "ffn_prefill_gateup"): {"bytes": 1366489044, "source": _PRE,
+                                                    "sha256_prefix": "7fb3d6681d45a9dc"},
+    ("prefill32k_streamed", "ffn_prefill_down"): {"bytes": 1098404608, "source": _PRE,
+                                                  "sha256_prefix": "7fb3d6681d45a9dc"},
 }
 
 

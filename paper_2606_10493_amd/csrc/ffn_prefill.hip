@@ -64,6 +64,7 @@ constexpr int kStages = 3;              // LDS stages of the ping-pong pipeline
 constexpr int kSaStride = kBM + 1;      // floats per K block of the row-scale table
 constexpr int kRing = 3;                // weight K blocks in registers
 constexpr int kXcd = 8;
+constexpr int kBand = 8;                // m-tiles per band of the work-item order (see tile_of)
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float v16f __attribute__((ext_vector_type(16)));
@@ -184,11 +185,16 @@ __device__ __forceinline__ v16f mfma_f8_32x32x64(const v8i& a, const v8i& b, con
 }
 
 // The tile of work item `item`: expert u owns items [mtile_start[u],
-// mtile_start[u+1]) * n_tiles in n-tile-major order, item = mtile_start[u] *
-// n_tiles + nt * mcount_u + mt.  The m-tiles that read the same weight slice
-// (same nt) are neighbours, so they run together on one XCD and the slice
-// comes from HBM once (m-tile major order fetched the weights once per
-// m-tile).  The expert's ceil(M/32) row groups are dealt evenly over its
+// mtile_start[u+1]) * n_tiles, in bands of kBand consecutive m-tiles, each
+// band n-tile major: item = mtile_start[u] * n_tiles + kBand * n_tiles *
+// band + nt * width + (mt - kBand * band) (width = the band's m-tiles; an
+// expert with at most kBand m-tiles is one band).  The m-tiles that read the
+// same weight slice (same nt) are neighbours, so they run together on one
+// XCD and the slice comes from HBM once per band (m-tile major order
+// fetched the weights once per m-tile); and an expert with many m-tiles
+// re-reads its token rows once per band pass instead of once per n-tile
+// (one n-tile-major pass over 141 m-tiles evicts them from L2 before the
+// next n-tile reads them again).  The expert's ceil(M/32) row groups are dealt evenly over its
 // mcount tiles (tile mt gets q/mcount groups, one more for mt < q % mcount):
 // the same MFMA work as full tiles plus a tail, but tiles of similar size,
 // which advance through their shared weight slice at similar speed, so the
@@ -204,8 +210,11 @@ __device__ __forceinline__ Tile tile_of(const PrefillArgs& p, int item) {
   const int e = d.x, s0 = d.y, o0 = d.z, o1 = d.w;
   const int mcount = (o1 - o0 + kBM - 1) / kBM;
   const int local = item - s0 * p.n_tiles;
-  const int ntx = local / mcount;
-  const int mt = local - ntx * mcount;
+  const int band = local / (kBand * p.n_tiles);
+  const int bw = min(kBand, mcount - band * kBand);
+  const int in_band = local - band * kBand * p.n_tiles;
+  const int ntx = in_band / bw;
+  const int mt = band * kBand + (in_band - ntx * bw);
   const int q = (o1 - o0 + 31) >> 5;
   const int base = q / mcount, extra = q - base * mcount;
   const int first = o0 + 32 * (mt * base + min(mt, extra));

@@ -15,7 +15,7 @@ whose end is the group's last slot).
 import numpy as np
 import pytest
 
-BM, BN, THREADS, XCD, TILE_BYTES = 128, 256, 512, 8, 2048
+BM, BN, THREADS, XCD, TILE_BYTES, BAND = 128, 256, 512, 8, 2048, 8
 
 
 def _max_mtiles(R, E):
@@ -61,7 +61,10 @@ def _tile_of(desc, n_tiles, item):
     e, s0, o0, o1 = desc[item // n_tiles]
     mcount = (o1 - o0 + BM - 1) // BM
     local = item - s0 * n_tiles
-    ntx, mt = divmod(local, mcount)
+    band = local // (BAND * n_tiles)
+    width = min(BAND, mcount - band * BAND)
+    ntx, mt = divmod(local - band * BAND * n_tiles, width)
+    mt += band * BAND
     q = (o1 - o0 + 31) >> 5
     base, extra = divmod(q, mcount)
     first = o0 + 32 * (mt * base + min(mt, extra))
@@ -191,9 +194,10 @@ def _run_layer(H, I, E, k, T, zipf_s, seed):
 
 
 def test_work_items_cover_every_tile_once():
-    """The work-item order (an expert's m-tiles n-tile major) is a bijection
-    onto (m-tile, n-tile) pairs, and an expert's m-tiles partition its rows,
-    for experts of 0 to 21 m-tiles and ragged tails."""
+    """The work-item order (an expert's m-tiles in bands of 8, each band
+    n-tile major) is a bijection onto (m-tile, n-tile) pairs, and an expert's
+    m-tiles partition its rows, for experts of 0 to 21 m-tiles (one band, two
+    and a partial third) and ragged tails."""
     rng = np.random.default_rng(3)
     m = [0, 1, 31, 128, 129, 1000, 1024, 1025, 2047, 2560] + list(rng.integers(0, 2700, 20))
     offsets = np.concatenate([[0], np.cumsum(m)]).astype(np.int64)
