@@ -25,6 +25,8 @@
 //     chosen experts; lanes 0 .. k-1 write ids and weights.
 #include "common.h"
 
+#include <type_traits>
+
 namespace moe {
 
 namespace {
@@ -81,8 +83,11 @@ __global__ __launch_bounds__(256) void router_logits_kernel(const uint16_t* __re
 // 16x16x32 per 32-K step).  The 32-K tiles of both operands go through two
 // LDS stages (each thread loads 16 bytes of x and 32 bytes of W_r per step);
 // a 64-byte LDS row holds one row's 32 K values, which a quarter wave reads
-// as 16 rows x 64 contiguous bytes.
-constexpr int kRtM = 128, kRtN = 256, kRtK = 32;
+// as 16 rows x 64 contiguous bytes.  The global loads run kRtRing - 1 steps
+// ahead through a ring of registers: with one step of look-ahead a
+// workgroup had 24 KB in flight and streamed the hidden states at about a
+// quarter of HBM bandwidth, bound by the loads' latency.
+constexpr int kRtM = 128, kRtN = 256, kRtK = 32, kRtRing = 4;
 
 __global__ __launch_bounds__(512) void router_logits_tiled_kernel(const uint16_t* __restrict__ x, int T, int H,
                                                                   const uint16_t* __restrict__ w, int E, int kchunk,
@@ -105,22 +110,32 @@ __global__ __launch_bounds__(512) void router_logits_tiled_kernel(const uint16_t
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-  uint4 rx = *reinterpret_cast<const uint4*>(xg);
-  uint4 rw0 = *reinterpret_cast<const uint4*>(wg0);
-  uint4 rw1 = *reinterpret_cast<const uint4*>(wg1);
   const int nsteps = kchunk / kRtK;
-  for (int st = 0; st < nsteps; ++st) {
-    const int b = st & 1;
-    *reinterpret_cast<uint4*>(&xs[b][lr * kRtK + lk]) = rx;
-    *reinterpret_cast<uint4*>(&wsm[b][lr * kRtK + lk]) = rw0;
-    *reinterpret_cast<uint4*>(&wsm[b][(128 + lr) * kRtK + lk]) = rw1;
-    __syncthreads();
-    if (st + 1 < nsteps) {  // the next step's loads fly during this step's MFMAs
-      const int64_t o = (int64_t)(st + 1) * kRtK;
-      rx = *reinterpret_cast<const uint4*>(xg + o);
-      rw0 = *reinterpret_cast<const uint4*>(wg0 + o);
-      rw1 = *reinterpret_cast<const uint4*>(wg1 + o);
-    }
+  // Ring slot S holds step st's operands for st % kRtRing == S (steps past
+  // the end reload the last one, so every step issues the same loads).
+  uint4 rx0, rx1, rx2, rx3, rwa0, rwa1, rwa2, rwa3, rwb0, rwb1, rwb2, rwb3;
+#define MOE_RT_LOAD(S, ST)                                                      \
+  do {                                                                          \
+    const int64_t o_ = (int64_t)min((ST), nsteps - 1) * kRtK;                   \
+    rx##S = *reinterpret_cast<const uint4*>(xg + o_);                           \
+    rwa##S = *reinterpret_cast<const uint4*>(wg0 + o_);                         \
+    rwb##S = *reinterpret_cast<const uint4*>(wg1 + o_);                         \
+  } while (0)
+  // Step st in slot S: its operands into LDS stage st % 2, the barrier, the
+  // loads of step st + kRtRing - 1 into slot NEXT (stored one step ago), then
+  // the step's MFMAs.  A stage is rewritten two steps after it was read,
+  // behind the barrier of the step in between.
+#define MOE_RT_STEP(S, NEXT, ST)                                                \
+  do {                                                                          \
+    const int st_ = (ST), b_ = st_ & 1;                                         \
+    *reinterpret_cast<uint4*>(&xs[b_][lr * kRtK + lk]) = rx##S;                 \
+    *reinterpret_cast<uint4*>(&wsm[b_][lr * kRtK + lk]) = rwa##S;               \
+    *reinterpret_cast<uint4*>(&wsm[b_][(128 + lr) * kRtK + lk]) = rwb##S;       \
+    __syncthreads();                                                            \
+    MOE_RT_LOAD(NEXT, st_ + kRtRing - 1);                                       \
+    mma_stage(b_);                                                              \
+  } while (0)
+  auto mma_stage = [&](int b) {
     bf16x8 a[4], bb[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -132,7 +147,23 @@ __global__ __launch_bounds__(512) void router_logits_tiled_kernel(const uint16_t
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bb[j], acc[i][j], 0, 0, 0);
+  };
+  static_assert(kRtRing == 4, "the unrolled ring below has four slots");
+  MOE_RT_LOAD(0, 0);
+  MOE_RT_LOAD(1, 1);
+  MOE_RT_LOAD(2, 2);
+  int st = 0;
+  for (; st + kRtRing <= nsteps; st += kRtRing) {
+    MOE_RT_STEP(0, 3, st);
+    MOE_RT_STEP(1, 0, st + 1);
+    MOE_RT_STEP(2, 1, st + 2);
+    MOE_RT_STEP(3, 2, st + 3);
   }
+  if (st < nsteps) MOE_RT_STEP(0, 3, st);
+  if (st + 1 < nsteps) MOE_RT_STEP(1, 0, st + 1);
+  if (st + 2 < nsteps) MOE_RT_STEP(2, 1, st + 2);
+#undef MOE_RT_STEP
+#undef MOE_RT_LOAD
   // Lane l holds logits of tokens (64 wm + 16 i) + 4 kq + q for expert (64 wn + 16 j) + r.
 #pragma unroll
   for (int i = 0; i < 4; ++i)

@@ -142,6 +142,16 @@ def test_router_ragged_expert_tile_tiled_logits(moe, tokens):
     _check(f"E=320 T={tokens}", x, wr, bias, 6, 1, 1, 1.0, moe)
 
 
+@pytest.mark.parametrize("hidden", [1120, 1344, 1376])
+def test_router_tiled_logits_step_counts(moe, hidden):
+    """Hidden sizes whose K slices hold 5, 6 and 43 steps of 32: the tiled
+    logits kernel's four-slot ring ends on a partial round of 1, 2 and 3 steps."""
+    w = synth.Workload("router_steps", hidden, 256, 256, 8, 300, "uniform")
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.05)
+    _check(f"H={hidden} T=300", x, wr, bias, 8, 8, 4, 2.5, moe)
+
+
 def test_router_many_experts_many_tokens(moe):
     w = synth.Workload("router_wide_tiled", 1024, 256, 1024, 32, 260, "uniform")
     x = synth.activations(w)
