@@ -77,101 +77,127 @@ __global__ __launch_bounds__(256) void router_logits_kernel(const uint16_t* __re
     }
 }
 
-// Many tokens: an LDS-tiled bf16 GEMM.  Workgroup = 128 tokens x 256
+// Many tokens: an LDS-tiled bf16 GEMM.  Workgroup = TM tokens x 256
 // experts over one K slice, 512 threads; wave w computes tokens
-// 64 (w / 4) + [0, 64) against experts 64 (w % 4) + [0, 64) (16 MFMA
+// TM/2 (w / 4) + [0, TM/2) against experts 64 (w % 4) + [0, 64) (TM/8 MFMA
 // 16x16x32 per 32-K step).  The 32-K tiles of both operands go through two
-// LDS stages (each thread loads 16 bytes of x and 32 bytes of W_r per step);
-// a 64-byte LDS row holds one row's 32 K values, which a quarter wave reads
-// as 16 rows x 64 contiguous bytes.  The global loads run kRtRing - 1 steps
-// ahead through a ring of registers: with one step of look-ahead a
-// workgroup had 24 KB in flight and streamed the hidden states at about a
-// quarter of HBM bandwidth, bound by the loads' latency.
-constexpr int kRtM = 128, kRtN = 256, kRtK = 32, kRtRing = 4;
+// LDS stages (each thread loads TM/8 bytes of x and 32 bytes of W_r per
+// step); a 64-byte LDS row holds one row's 32 K values, which a quarter wave
+// reads as 16 rows x 64 contiguous bytes.  The global loads run RING - 1
+// steps ahead through a ring of registers (four slots for 128-token tiles,
+// three for 256, which need twice the registers per slot): with one step of
+// look-ahead the
+// kernel was bound by the loads' latency (224.8 us at 32768 tokens, against
+// 161.7 us with the ring).  Every tile reads the whole router weight (3.67 MB
+// at the DeepSeek-V3 shape) from L2, so from 32768 tokens on, where 128-token
+// tiles alone fill the chip, tiles of 256 tokens halve those reads (143.8
+// against 161.7 us); below, the K slices that 256-token tiles need to fill
+// the chip cost more than they save (8192 tokens: 43.8 against 43.0 us, and
+// a slower selection over twice the slices).
+constexpr int kRtN = 256, kRtK = 32;
+constexpr int kRtBigTokens = 32768;  // 256-token tiles from here on
+inline int router_tile_tokens(int64_t T) { return T >= kRtBigTokens ? 256 : 128; }
 
+template <int TM, int RING>
 __global__ __launch_bounds__(512) void router_logits_tiled_kernel(const uint16_t* __restrict__ x, int T, int H,
                                                                   const uint16_t* __restrict__ w, int E, int kchunk,
                                                                   float* __restrict__ part) {
-  __shared__ __attribute__((aligned(16))) uint16_t xs[2][kRtM * kRtK];
+  constexpr int XR = TM / 128;  // x rows per loader thread
+  constexpr int WI = TM / 32;   // 16-token MFMA tiles per wave
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2][TM * kRtK];
   __shared__ __attribute__((aligned(16))) uint16_t wsm[2][kRtN * kRtK];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, kq = lane >> 4;
   const int wm = wave >> 2, wn = wave & 3;
-  const int t0 = blockIdx.x * kRtM, e0 = blockIdx.y * kRtN, ks = blockIdx.z;
+  const int t0 = blockIdx.x * TM, e0 = blockIdx.y * kRtN, ks = blockIdx.z;
   const int64_t k0 = (int64_t)ks * kchunk;
-  // Loader: thread tid moves x row tid / 4 (16 bytes at K 8 (tid % 4)) and
-  // W_r rows tid / 4 and 128 + tid / 4; rows beyond T or E read a valid row.
+  // Loader: thread tid moves x rows tid / 4 (+ 128) and W_r rows tid / 4 and
+  // 128 + tid / 4 (16 bytes each at K 8 (tid % 4)); rows beyond T or E read
+  // a valid row.
   const int lr = tid >> 2, lk = (tid & 3) * 8;
-  const uint16_t* xg = x + (int64_t)min(t0 + lr, T - 1) * H + k0 + lk;
+  const uint16_t* xg0 = x + (int64_t)min(t0 + lr, T - 1) * H + k0 + lk;
+  const uint16_t* xg1 = x + (int64_t)min(t0 + (XR - 1) * 128 + lr, T - 1) * H + k0 + lk;
   const uint16_t* wg0 = w + (int64_t)min(e0 + lr, E - 1) * H + k0 + lk;
   const uint16_t* wg1 = w + (int64_t)min(e0 + 128 + lr, E - 1) * H + k0 + lk;
-  v4f acc[4][4];
+  v4f acc[WI][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < WI; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
   const int nsteps = kchunk / kRtK;
   // Ring slot S holds step st's operands for st % kRtRing == S (steps past
   // the end reload the last one, so every step issues the same loads).
-  uint4 rx0, rx1, rx2, rx3, rwa0, rwa1, rwa2, rwa3, rwb0, rwb1, rwb2, rwb3;
+  uint4 rxa0, rxa1, rxa2, rxa3, rxb0, rxb1, rxb2, rxb3, rwa0, rwa1, rwa2, rwa3, rwb0, rwb1, rwb2, rwb3;
 #define MOE_RT_LOAD(S, ST)                                                      \
   do {                                                                          \
     const int64_t o_ = (int64_t)min((ST), nsteps - 1) * kRtK;                   \
-    rx##S = *reinterpret_cast<const uint4*>(xg + o_);                           \
+    rxa##S = *reinterpret_cast<const uint4*>(xg0 + o_);                         \
+    if (XR > 1) rxb##S = *reinterpret_cast<const uint4*>(xg1 + o_);             \
     rwa##S = *reinterpret_cast<const uint4*>(wg0 + o_);                         \
     rwb##S = *reinterpret_cast<const uint4*>(wg1 + o_);                         \
   } while (0)
   // Step st in slot S: its operands into LDS stage st % 2, the barrier, the
-  // loads of step st + kRtRing - 1 into slot NEXT (stored one step ago), then
+  // loads of step st + RING - 1 into slot NEXT (stored one step ago), then
   // the step's MFMAs.  A stage is rewritten two steps after it was read,
   // behind the barrier of the step in between.
 #define MOE_RT_STEP(S, NEXT, ST)                                                \
   do {                                                                          \
     const int st_ = (ST), b_ = st_ & 1;                                         \
-    *reinterpret_cast<uint4*>(&xs[b_][lr * kRtK + lk]) = rx##S;                 \
+    *reinterpret_cast<uint4*>(&xs[b_][lr * kRtK + lk]) = rxa##S;                \
+    if (XR > 1) *reinterpret_cast<uint4*>(&xs[b_][(128 + lr) * kRtK + lk]) = rxb##S; \
     *reinterpret_cast<uint4*>(&wsm[b_][lr * kRtK + lk]) = rwa##S;               \
     *reinterpret_cast<uint4*>(&wsm[b_][(128 + lr) * kRtK + lk]) = rwb##S;       \
     __syncthreads();                                                            \
-    MOE_RT_LOAD(NEXT, st_ + kRtRing - 1);                                       \
+    MOE_RT_LOAD(NEXT, st_ + RING - 1);                                          \
     mma_stage(b_);                                                              \
   } while (0)
   auto mma_stage = [&](int b) {
-    bf16x8 a[4], bb[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&xs[b][(64 * wm + 16 * i + r) * kRtK + 8 * kq]));
+    bf16x8 bb[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       bb[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&wsm[b][(64 * wn + 16 * j + r) * kRtK + 8 * kq]));
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < WI; ++i) {
+      const bf16x8 a = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const uint4*>(&xs[b][(TM / 2 * wm + 16 * i + r) * kRtK + 8 * kq]));
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bb[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bb[j], acc[i][j], 0, 0, 0);
+    }
   };
-  static_assert(kRtRing == 4, "the unrolled ring below has four slots");
+  static_assert(RING == 3 || RING == 4, "the unrolled rings below have three or four slots");
   MOE_RT_LOAD(0, 0);
   MOE_RT_LOAD(1, 1);
-  MOE_RT_LOAD(2, 2);
   int st = 0;
-  for (; st + kRtRing <= nsteps; st += kRtRing) {
-    MOE_RT_STEP(0, 3, st);
-    MOE_RT_STEP(1, 0, st + 1);
-    MOE_RT_STEP(2, 1, st + 2);
-    MOE_RT_STEP(3, 2, st + 3);
+  if constexpr (RING == 4) {
+    MOE_RT_LOAD(2, 2);
+    for (; st + 4 <= nsteps; st += 4) {
+      MOE_RT_STEP(0, 3, st);
+      MOE_RT_STEP(1, 0, st + 1);
+      MOE_RT_STEP(2, 1, st + 2);
+      MOE_RT_STEP(3, 2, st + 3);
+    }
+    if (st < nsteps) MOE_RT_STEP(0, 3, st);
+    if (st + 1 < nsteps) MOE_RT_STEP(1, 0, st + 1);
+    if (st + 2 < nsteps) MOE_RT_STEP(2, 1, st + 2);
+  } else {
+    for (; st + 3 <= nsteps; st += 3) {
+      MOE_RT_STEP(0, 2, st);
+      MOE_RT_STEP(1, 0, st + 1);
+      MOE_RT_STEP(2, 1, st + 2);
+    }
+    if (st < nsteps) MOE_RT_STEP(0, 2, st);
+    if (st + 1 < nsteps) MOE_RT_STEP(1, 0, st + 1);
   }
-  if (st < nsteps) MOE_RT_STEP(0, 3, st);
-  if (st + 1 < nsteps) MOE_RT_STEP(1, 0, st + 1);
-  if (st + 2 < nsteps) MOE_RT_STEP(2, 1, st + 2);
 #undef MOE_RT_STEP
 #undef MOE_RT_LOAD
-  // Lane l holds logits of tokens (64 wm + 16 i) + 4 kq + q for expert (64 wn + 16 j) + r.
+  // Lane l holds logits of tokens (TM/2 wm + 16 i) + 4 kq + q for expert (64 wn + 16 j) + r.
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < WI; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int t = t0 + 64 * wm + 16 * i + 4 * kq + q, e = e0 + 64 * wn + 16 * j + r;
+        const int t = t0 + TM / 2 * wm + 16 * i + 4 * kq + q, e = e0 + 64 * wn + 16 * j + r;
         if (t < T && e < E) part[((int64_t)ks * T + t) * E + e] = acc[i][j][q];
       }
 }
@@ -473,7 +499,8 @@ constexpr int kRouterTiledMinTokens = 256;
 // kRouterMinChunk elements.
 int router_slices(int32_t T, int32_t H, int32_t E) {
   const bool tiled = T >= kRouterTiledMinTokens;
-  const int64_t tiles = tiled ? ((int64_t)T + kRtM - 1) / kRtM * (((int64_t)E + kRtN - 1) / kRtN)
+  const int tm = router_tile_tokens(T);
+  const int64_t tiles = tiled ? ((int64_t)T + tm - 1) / tm * (((int64_t)E + kRtN - 1) / kRtN)
                               : ((int64_t)T + 15) / 16 * (((int64_t)E + 255) / 256);
   const int64_t want = tiles >= 256 ? 1 : (256 + tiles - 1) / tiles;
   const int n32 = H / 32;
@@ -518,9 +545,14 @@ extern "C" moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H,
   const int ks = router_slices(T, H, E);
   float* part = static_cast<float*>(ws);
   if (T >= kRouterTiledMinTokens) {
-    const dim3 grid((unsigned)((T + kRtM - 1) / kRtM), (unsigned)((E + kRtN - 1) / kRtN), (unsigned)ks);
-    MOE_LAUNCH("router_logits", router_logits_tiled_kernel, grid, dim3(512), 0, stream, x_bf16, T, H, w_router_bf16,
-               E, H / ks, part);
+    const int tm = router_tile_tokens(T);
+    const dim3 grid((unsigned)((T + tm - 1) / tm), (unsigned)((E + kRtN - 1) / kRtN), (unsigned)ks);
+    if (tm == 256)
+      MOE_LAUNCH("router_logits", (router_logits_tiled_kernel<256, 3>), grid, dim3(512), 0, stream, x_bf16, T, H,
+                 w_router_bf16, E, H / ks, part);
+    else
+      MOE_LAUNCH("router_logits", (router_logits_tiled_kernel<128, 4>), grid, dim3(512), 0, stream, x_bf16, T, H,
+                 w_router_bf16, E, H / ks, part);
   } else {
     const dim3 grid((unsigned)((T + 15) / 16), (unsigned)((E + 255) / 256), (unsigned)ks);
     MOE_LAUNCH("router_logits", router_logits_kernel, grid, dim3(256), 0, stream, x_bf16, T, H, w_router_bf16, E,

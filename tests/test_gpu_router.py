@@ -152,6 +152,18 @@ def test_router_tiled_logits_step_counts(moe, hidden):
     _check(f"H={hidden} T=300", x, wr, bias, 8, 8, 4, 2.5, moe)
 
 
+@pytest.mark.parametrize("hidden", [1024, 1056, 1088])
+def test_router_256_token_tiles(moe, hidden):
+    """32868 tokens (256-token logits tiles from 32768 on, the last one
+    ragged), E = 320 (one full and one ragged 256-expert tile), one K slice
+    of 32, 33 and 34 steps: the three-slot ring ends on a partial round of
+    2, 0 and 1 steps."""
+    w = synth.Workload("router_big", hidden, 256, 320, 6, 32868, "uniform")
+    x = synth.activations(w)
+    wr, bias = synth.router_params(w, bias_std=0.02)
+    _check(f"E=320 T=32868 H={hidden}", x, wr, bias, 6, 1, 1, 1.0, moe)
+
+
 def test_router_many_experts_many_tokens(moe):
     w = synth.Workload("router_wide_tiled", 1024, 256, 1024, 32, 260, "uniform")
     x = synth.activations(w)
