@@ -207,6 +207,51 @@ __device__ __forceinline__ bool beats(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
+// The value of lane p(l) of a row of 16 lanes, for the DPP patterns below
+// (a VALU operand modifier; no LDS traffic, unlike a shuffle).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+// Lane patterns that pair every lane with one of another part of its group,
+// doubling the group each time: quads (lane ^ 1, lane ^ 2), then half rows
+// (lane 7 - i of the 8) and rows (lane 15 - i of the 16).  A reduction that
+// does not depend on the order of its operands gives every lane of a row the
+// result over the row's 16 lanes.
+constexpr int kDppQuadXor1 = 0xB1, kDppQuadXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+// Every lane gets the wave's largest (key, index) in the selection order.
+__device__ __forceinline__ void wave_argmax(float& bk, int& be) {
+  auto step = [&](float ok, int oe) {
+    if (beats(ok, oe, bk, be)) {
+      bk = ok;
+      be = oe;
+    }
+  };
+  step(dpp_f<kDppQuadXor1>(bk), dpp_i<kDppQuadXor1>(be));
+  step(dpp_f<kDppQuadXor2>(bk), dpp_i<kDppQuadXor2>(be));
+  step(dpp_f<kDppHalfMirror>(bk), dpp_i<kDppHalfMirror>(be));
+  step(dpp_f<kDppMirror>(bk), dpp_i<kDppMirror>(be));
+  // the four rows' results, as wave-uniform values
+  float k0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bk), 0));
+  int e0 = __builtin_amdgcn_readlane(be, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) {
+    const float kr = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bk), 16 * r));
+    const int er = __builtin_amdgcn_readlane(be, 16 * r);
+    if (beats(kr, er, k0, e0)) {
+      k0 = kr;
+      e0 = er;
+    }
+  }
+  bk = k0;
+  be = e0;
+}
+
 // Selection: one wave per token (four tokens per 256-thread workgroup),
 // lane l holding experts l, l + 64, ... (PER of them).  The KS partial
 // logits are summed in slice order, then:
@@ -232,7 +277,7 @@ __device__ __forceinline__ uint32_t ordered_bits(float v) {
 // each sum the slices q = w, w + 4, ... and wave 0 adds the four partial sums
 // (in wave order) before it selects, so the slices are read in one round
 // trip instead of several.
-template <int PER, bool WIDE>
+template <int PER, bool WIDE, int QB>
 __global__ __launch_bounds__(256) void router_select_kernel(const float* __restrict__ part, int KS, int T, int E,
                                                             const float* __restrict__ bias, int k, int n_group,
                                                             int topk_group, float scaling, int shared,
@@ -247,8 +292,11 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
   const int epg = E / n_group;
   const int k_out = k + (shared >= 0 ? 1 : 0);
 
-  // Logits: the KS slices summed in slice order; each batch's loads go out
-  // together (slice index clamped, so every load is unconditional).
+  // Logits: the KS slices summed in slice order; the loads of a batch of QB
+  // slices go out together (slice index clamped, so every load is
+  // unconditional).  QB follows the launch's slice count (2, 4, or 64 / PER
+  // for more slices), so a launch with one or two slices does not issue the
+  // loads of sixteen.
   float s[PER], key[PER];
   {
     float lg[PER], bv[PER];
@@ -258,7 +306,6 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
       bv[i] = bias ? bias[e] : 0.0f;
       lg[i] = 0.0f;
     }
-    constexpr int QB = (64 / PER) > 1 ? 64 / PER : 1;
     const int q_first = WIDE ? wave : 0, q_step = WIDE ? 4 : 1;
     for (int q0 = q_first; q0 < KS; q0 += QB * q_step) {
       float v[QB][PER];
@@ -307,14 +354,21 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
         b1[i] = key[i];
         b2[i] = -INFINITY;
       }
-      for (int m = 1; m < epg; m <<= 1) {
+      // (largest, second) pairs merged with a partner lane of the segment:
+      // within rows by DPP patterns (quads, half rows, rows), beyond by
+      // shuffles.
+      auto merge = [&](int i, float o1, float o2) {
+        const float n2 = fmaxf(fminf(b1[i], o1), fmaxf(b2[i], o2));
+        b1[i] = fmaxf(b1[i], o1);
+        b2[i] = n2;
+      };
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-          const float o1 = __shfl_xor(b1[i], m), o2 = __shfl_xor(b2[i], m);
-          const float n2 = fmaxf(fminf(b1[i], o1), fmaxf(b2[i], o2));
-          b1[i] = fmaxf(b1[i], o1);
-          b2[i] = n2;
-        }
+      for (int i = 0; i < PER; ++i) {
+        if (epg > 1) merge(i, dpp_f<kDppQuadXor1>(b1[i]), dpp_f<kDppQuadXor1>(b2[i]));
+        if (epg > 2) merge(i, dpp_f<kDppQuadXor2>(b1[i]), dpp_f<kDppQuadXor2>(b2[i]));
+        if (epg > 4) merge(i, dpp_f<kDppHalfMirror>(b1[i]), dpp_f<kDppHalfMirror>(b2[i]));
+        if (epg > 8) merge(i, dpp_f<kDppMirror>(b1[i]), dpp_f<kDppMirror>(b2[i]));
+        for (int m = 16; m < epg; m <<= 1) merge(i, __shfl_xor(b1[i], m), __shfl_xor(b2[i], m));
       }
       const int gpr = 64 / epg;  // groups per register
 #pragma unroll
@@ -350,15 +404,14 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
     }
     int rank = 0;
     for (int h = 0; h < n_group; ++h) {
-      const float gh = __shfl(my_group, h);
+      const float gh = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_group), h));
       rank += beats(gh, h, my_group, lane) ? 1 : 0;
     }
-    const int kept_group = (lane < n_group && rank < topk_group) ? 1 : 0;
+    const unsigned long long kept_groups = __ballot(lane < n_group && rank < topk_group);  // bit g: group g kept
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int e = lane + 64 * i;
-      const int kept = __shfl(kept_group, e < E ? e / epg : 0);
-      if (!kept) key[i] = -INFINITY;
+      if (!((kept_groups >> (e < E ? e / epg : 0)) & 1ull)) key[i] = -INFINITY;
     }
   }
 
@@ -378,20 +431,12 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
           bk = key[i];
           be = lane + 64 * i;
         }
-#pragma unroll
-      for (int m = 1; m < 64; m <<= 1) {  // butterfly: every lane ends with the same best
-        const float ok = __shfl_xor(bk, m);
-        const int oe = __shfl_xor(be, m);
-        if (beats(ok, oe, bk, be)) {
-          bk = ok;
-          be = oe;
-        }
-      }
+      wave_argmax(bk, be);  // every lane ends with the same best
       float sv = s[0];
 #pragma unroll
       for (int i = 1; i < PER; ++i)
         if ((be >> 6) == i) sv = s[i];
-      sv = __shfl(sv, be & 63);
+      sv = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sv), be & 63));
       if (lane == j) {
         my_e = be;
         my_s = sv;
@@ -563,14 +608,16 @@ extern "C" moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H,
   // Few tokens with many K slices: one token per workgroup (WIDE).
   const bool wide = ks >= 8 && T <= 64;
   const dim3 sgrid((unsigned)(wide ? T : (T + 3) / 4)), sblock(256);
+#define MOE_ROUTER_SELECT_Q(P, W, Q)                                                                               \
+  MOE_LAUNCH("router_select", (router_select_kernel<P, W, Q>), sgrid, sblock, 0, stream, part, ks, T, E, bias, k,    \
+             cfg.n_group, cfg.topk_group, cfg.routed_scaling, cfg.shared_expert, topk_ids, topk_w)
 #define MOE_ROUTER_SELECT(P)                                                                                       \
   do {                                                                                                             \
-    if (wide)                                                                                                      \
-      MOE_LAUNCH("router_select", (router_select_kernel<P, true>), sgrid, sblock, 0, stream, part, ks, T, E, bias, \
-                 k, cfg.n_group, cfg.topk_group, cfg.routed_scaling, cfg.shared_expert, topk_ids, topk_w);         \
-    else                                                                                                           \
-      MOE_LAUNCH("router_select", (router_select_kernel<P, false>), sgrid, sblock, 0, stream, part, ks, T, E,      \
-                 bias, k, cfg.n_group, cfg.topk_group, cfg.routed_scaling, cfg.shared_expert, topk_ids, topk_w);   \
+    constexpr int qb_ = (64 / (P)) > 1 ? 64 / (P) : 1;                                                             \
+    if (wide) MOE_ROUTER_SELECT_Q(P, true, qb_);                                                                   \
+    else if (ks <= 2) MOE_ROUTER_SELECT_Q(P, false, 2);                                                            \
+    else if (ks <= 4) MOE_ROUTER_SELECT_Q(P, false, 4);                                                            \
+    else MOE_ROUTER_SELECT_Q(P, false, qb_);                                                                       \
   } while (0)
   const int per = (E + 63) / 64;
   if (per <= 1) MOE_ROUTER_SELECT(1);
@@ -579,5 +626,6 @@ extern "C" moe_status_t moe_router(const uint16_t* x_bf16, int32_t T, int32_t H,
   else if (per <= 8) MOE_ROUTER_SELECT(8);
   else MOE_ROUTER_SELECT(16);
 #undef MOE_ROUTER_SELECT
+#undef MOE_ROUTER_SELECT_Q
   return check_launch("moe_router");
 }
