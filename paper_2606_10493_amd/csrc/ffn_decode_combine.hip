@@ -17,9 +17,9 @@
 // and the combine is the definition's order (combine8_of).  The output is
 // therefore bit-identical to the decode down kernel followed by moe_combine.
 //
-// Waves: 16 = (expert slot s = wave / 4) x (K part kw = wave % 4); wave
-// (s, kw) takes experts s, s + 4, ... and streams their K blocks kw, kw + 4,
-// ... as one list of items through a window of W items in registers,
+// Waves: WAVES = (expert slot s = wave / 4) x (K part kw = wave % 4); wave
+// (s, kw) takes experts s, s + WAVES / 4, ... and streams their K blocks kw,
+// kw + 4, ... as one list of items through a window of W items in registers,
 // with no barrier inside the loop.  At the end of each expert it stores the
 // expert's rows of its partial sum in LDS by expert row; after one barrier
 // the four partials of each row are summed in wave order.
@@ -29,10 +29,10 @@ namespace moe {
 
 namespace {
 
-constexpr int kDcMaxRows = 16;                // R = T * k (beyond, 224 workgroups stream too few bytes per CU)
+constexpr int kDcMaxRows = 16;                // R = T * k (beyond, H / 16 workgroups stream too few bytes per CU)
 constexpr int kDcMaxTokens = 16;              // rows of one expert: one 16-row MFMA operand
 constexpr int kDcMaxK = 2048;                 // I
-constexpr int kDcThreads = 1024;
+constexpr int kDcMaxExperts = 1024;          // four 256-expert chunks of offsets
 
 struct DownCombineArgs {
   const float* h;           // fp32 [R, K]: SiLU(G) * U rows in expert-sorted order
@@ -47,17 +47,73 @@ struct DownCombineArgs {
   uint16_t* out;            // bf16 [T, N]
 };
 
+// The active experts (those with rows) of slot `sub`: the a-th active
+// expert in expert order with a = sub + SLOTS g goes to lane g as (expert, first
+// row, row count); other lanes hold zeros.  Returns the number of active
+// experts.  NCH chunks of 256 experts cover E; all their offsets are loaded
+// first (addresses clamped to E, no branch), so the lookup costs one L2
+// latency before the weight stream can start.
+template <int NCH, int SLOTS>
+__device__ __forceinline__ int active_experts(const int32_t* __restrict__ offsets, int E, int sub, int& v_e,
+                                              int& v_p0, int& v_m) {
+  const int lane = threadIdx.x & 63;
+  int o[NCH][5];
+#pragma unroll
+  for (int q = 0; q < NCH; ++q) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) o[q][c] = offsets[min(256 * q + 64 * c + lane, E)];
+    o[q][4] = offsets[min(256 * q + 256 + lane, E)];  // lane 0's: the end of the chunk
+  }
+  int n_act = 0, found = 0;
+  v_e = 0;
+  v_p0 = 0;
+  v_m = 0;
+#pragma unroll
+  for (int q = 0; q < NCH; ++q) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int x = 256 * q + 64 * c + lane;
+      const int nxt_first = __shfl(o[q][c + 1], 0);
+      const int up = __shfl_down(o[q][c], 1);
+      const int nxt = lane < 63 ? up : nxt_first;
+      const bool on = x < E && nxt > o[q][c];
+      const unsigned long long bal = __ballot(on);
+      const int rank =
+          n_act + (int)__builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
+      // this slot's experts in this chunk, in increasing order = increasing g
+      unsigned long long want = __ballot(on && rank >= sub && ((rank - sub) & (SLOTS - 1)) == 0);
+      while (want != 0ull && found < 64) {
+        const int pos = __ffsll((long long)want) - 1;
+        const int p0 = __builtin_amdgcn_readlane(o[q][c], pos);
+        const int m = __builtin_amdgcn_readlane(nxt, pos) - p0;
+        if (lane == found) {
+          v_e = 256 * q + 64 * c + pos;
+          v_p0 = p0;
+          v_m = m;
+        }
+        ++found;
+        want &= want - 1ull;
+      }
+      n_act += __popcll(bal);
+    }
+  }
+  return n_act;
+}
+
 // NT: 16-column operands per workgroup; HQ: h row blocks per 16-lane group
 // loaded before the weight window (the rest, if R * K / 128 > 64 HQ, are
-// loaded after it); W: items in the weight window.
-template <int NT, int HQ, int W>
-__global__ __launch_bounds__(kDcThreads) void ffn_decode_down_combine_kernel(DownCombineArgs p) {
+// loaded after it); W: items in the weight window; NCH: 256-expert chunks
+// of the offsets (E <= 256 NCH); WAVES: 4 K parts x WAVES / 4 expert slots.
+template <int NT, int HQ, int W, int NCH, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void ffn_decode_down_combine_kernel(DownCombineArgs p) {
   constexpr int kCols = 16 * NT;
+  constexpr int kDcThreads = 64 * WAVES;
+  constexpr int kSlots = WAVES / 4;
+  static_assert(kSlots == 1 || kSlots == 2 || kSlots == 4, "expert slots: a power of two");
   __shared__ __attribute__((aligned(16))) uint8_t qh[kDcMaxRows * kDcMaxK];
   __shared__ float sh[kDcMaxRows * (kDcMaxK / kBlock)];
   __shared__ float part[4 * kDcMaxRows * kCols];  // [K part][expert row][column]
   __shared__ __attribute__((aligned(16))) float yl[kDcMaxRows * kCols];
-  __shared__ float wsc[kDcThreads / 64][64];  // per wave: the weight scale of item i
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -69,62 +125,35 @@ __global__ __launch_bounds__(kDcThreads) void ffn_decode_down_combine_kernel(Dow
 
   // This thread's first HQ h row blocks (g = tid/16, tid/16 + 64, ...) go
   // out first; they are quantized once the weight loads are in flight.
+  // Blocks past the last one load the last one again (not quantized), so
+  // the loads are not behind a branch whose join would wait for them.
   constexpr int kHq = HQ;
   float hv[kHq][8];
 #pragma unroll
   for (int q = 0; q < kHq; ++q) {
-    const int g = (tid >> 4) + q * (kDcThreads / 16);
-    if (g < R * nb) {
-      const int row = g / nb, b = g - row * nb;
-      load8_f32(p.h + (int64_t)row * p.K + b * kBlock + (tid & 15) * 8, hv[q]);
-    }
+    const int g = min((tid >> 4) + q * (kDcThreads / 16), R * nb - 1);
+    const int row = g / nb, b = g - row * nb;
+    load8_f32(p.h + (int64_t)row * p.K + b * kBlock + (tid & 15) * 8, hv[q]);
   }
 
-  // Active experts, found by every wave on its own with ballots over the
-  // offsets (no barrier): lane g takes expert a = sub + 4 g, the a-th
-  // expert with rows (expert order), with its first row and row count.
-  int v_e = 0, v_p0 = 0, v_m = 0, n_act = 0;
-  {
-    const int a = sub + 4 * lane;
-    for (int c0 = 0; c0 < p.E; c0 += 64) {
-      const int e = c0 + lane;
-      const int lo = e < p.E ? p.offsets[e] : 0;
-      const int hi = e < p.E ? p.offsets[e + 1] : 0;
-      const unsigned long long bal = __ballot(hi > lo);
-      const int cnt = __popcll(bal);
-      // the (a - n_act)-th set bit of bal, for the lanes whose expert is in this chunk
-      unsigned long long mk = bal;
-      int n = a - n_act, pos = 0;
-#pragma unroll
-      for (int w = 32; w >= 1; w >>= 1) {
-        const int c = __popcll(mk & ((1ull << w) - 1ull));
-        if (n >= c) {
-          n -= c;
-          mk >>= w;
-          pos += w;
-        }
-      }
-      const int lo_b = __shfl(lo, pos), hi_b = __shfl(hi, pos);
-      if (a >= n_act && a < n_act + cnt) {
-        v_e = c0 + pos;
-        v_p0 = lo_b;
-        v_m = hi_b - lo_b;
-      }
-      n_act += cnt;
-    }
-  }
+  // Active experts, found by every wave on its own (no barrier): lane g
+  // receives expert a = sub + kSlots g, the a-th expert with rows (expert
+  // order), with its first row and row count.
+  int v_e, v_p0, v_m;
+  const int n_act = active_experts<NCH, kSlots>(p.offsets, p.E, sub, v_e, v_p0, v_m);
 
-  // Items of this wave: (expert a = sub + 4 g, block j) for g < n_mine, j < nkw.
+  // Items of this wave: (expert a = sub + kSlots g, block j) for g < n_mine, j < nkw.
   const int nkw = (nb - kw + 3) / 4;
-  const int n_mine = n_act > sub ? (n_act - sub + 3) / 4 : 0;
+  const int n_mine = n_act > sub ? (n_act - sub + kSlots - 1) / kSlots : 0;
   const int n_items = n_mine * nkw;
   auto uni = [](int v, int l) { return __builtin_amdgcn_readlane(v, l); };
-  // Lane i: the weight scale of item i (loaded before the weight window).
+  // Lane i: the weight scale of item i, read by readlane at item i (its
+  // load is issued before the weight window and waited for with it).
+  float wsv;
   {
     const int g = lane / max(nkw, 1), j = lane - g * max(nkw, 1);
     const int e_g = __shfl(v_e, min(g, 63));
-    const float wsv = lane < n_items ? p.s[((int64_t)e_g * (p.N / kBlock) + n0 / kBlock) * nb + kw + 4 * j] : 0.0f;
-    wsc[wave][lane] = wsv;
+    wsv = lane < n_items ? p.s[((int64_t)e_g * (p.N / kBlock) + n0 / kBlock) * nb + kw + 4 * j] : 0.0f;
   }
   v8i wbuf[W][NT];
   // Item it (clamped into the list; a wave without items loads expert 0's
@@ -184,7 +213,7 @@ __global__ __launch_bounds__(kDcThreads) void ffn_decode_down_combine_kernel(Dow
         const int g = it / nkw, j = it - g * nkw;
         const int p0 = uni(v_p0, g), m = uni(v_m, g);
         const int bk = kw + 4 * j;
-        const float ws = wsc[wave][it];
+        const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wsv), it));
         // A rows beyond the expert's m rows read a valid row; their outputs are never kept.
         const v8i afrag = load_v8i_ksplit(qh + (p0 + min(r, m - 1)) * p.K + bk * kBlock + kq * 16);
         float sa[4];
@@ -240,7 +269,7 @@ __global__ __launch_bounds__(kDcThreads) void ffn_decode_down_combine_kernel(Dow
 // True when the fused down + combine takes this batch.
 bool decode_down_combine_fits(const moe_dims_t& d, int32_t T) {
   return T >= 1 && T <= kDcMaxTokens && (int64_t)T * d.topk <= kDcMaxRows && d.inter <= kDcMaxK &&
-         d.n_experts <= kDcThreads && d.hidden % 32 == 0;
+         d.n_experts <= kDcMaxExperts && d.hidden % 32 == 0;
 }
 
 // y = down(h) of every active expert combined per token into out (bf16 [T, H]).
@@ -254,10 +283,17 @@ moe_status_t run_ffn_decode_down_combine(const moe_dims_t& d, int32_t T, const f
   a.h = h; a.offsets = offsets; a.E = d.n_experts;
   a.w = w_down; a.s = s_down; a.N = d.hidden; a.K = d.inter;
   a.dest_row = dest_row; a.topk_w = topk_w; a.topk = d.topk; a.tokens = T; a.out = out;
-  // Two h row blocks per lane group ahead of the weight window (they fit in
-  // registers beside it); any others are loaded after it.
-  MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<2, 2, 4>), dim3((unsigned)(d.hidden / 32)),
-             dim3(kDcThreads), 0, stream, a);
+  // 16 columns and 8 waves (two expert slots x four K parts) per workgroup:
+  // two workgroups fit on a CU (94 VGPRs, 39 KB of LDS), so all H / 16 of
+  // them are resident at once on all CUs (at H = 7168: 448 on 256 CUs; 224
+  // workgroups of 32 columns left 32 CUs idle).  Four h row blocks per lane
+  // group go out ahead of the weight window; any others follow it.
+  if (d.n_experts <= 256)
+    MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<1, 4, 4, 1, 8>),
+               dim3((unsigned)(d.hidden / 16)), dim3(512), 0, stream, a);
+  else
+    MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<1, 4, 4, kDcMaxExperts / 256, 8>),
+               dim3((unsigned)(d.hidden / 16)), dim3(512), 0, stream, a);
   return check_launch("ffn_decode_down_combine");
 }
 

@@ -153,6 +153,8 @@ def test_fused_layer_deepseek_decode_equals_four_calls(moe, deepseek_layer, name
     (256, 128, 1, 1, 3, "decode"),        # a single expert
     (256, 128, 1, 1, 300, "prefill"),
     (256, 128, 1024, 32, 2, "decode"),    # E = 1024, k = 32: the widest sort
+    (256, 128, 1024, 16, 1, "decode"),    # E = 1024, T * k = 16: fused down + combine over four 256-expert chunks
+    (256, 128, 300, 8, 2, "decode"),      # E = 300: fused down + combine, a partial second chunk
     (256, 128, 1024, 32, 40, "prefill"),
     (384, 128, 8, 2, 9, "decode"),        # H a multiple of 128 but not of 256 (decode only)
     (8448, 256, 4, 2, 40, "prefill"),     # K = 8448 > 8192: row scales beyond one 16-load batch
