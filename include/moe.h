@@ -241,8 +241,12 @@ moe_status_t moe_combine(const float* y_rows, const int32_t* dest_row, const flo
  * from device memory), in fewer launches:
  *   T <= 256: quantization and the slot sort run as one launch;
  *   DECODE regime with T * k <= 16 and I <= 2048: the down projection and
- *   the combine run as one launch (a workgroup computes 32 output columns
- *   for every active expert and combines them per token in LDS).
+ *   the combine run as one launch (a workgroup computes 16 output columns
+ *   for every active expert and combines them per token in LDS);
+ *   DECODE regime with T = 1, k <= 16, I <= 2048 and H <= 8192: two launches
+ *   and no sort (one token's slots are distinct experts): the gate/up launch
+ *   quantizes the token row itself and takes slot j's expert from topk_ids,
+ *   writing h row j; the down + combine launch reads the same ids.
  * x_bf16: device [T, H] bf16 bits; topk_ids: device int32 [T, k];
  * topk_w: device fp32 [T, k]; weight stacks as in moe_expert_ffn (packed);
  * out_bf16: device [T, H] bf16 bits; dev_status: optional device int32

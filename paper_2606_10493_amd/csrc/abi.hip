@@ -41,10 +41,18 @@ moe_status_t run_ffn_decode_gateup(const moe_dims_t& d, int32_t T, const uint8_t
                                    const float* s_gate, const uint8_t* w_up, const float* s_up, float* h,
                                    hipStream_t stream);
 
+bool decode_one_token_fits(const moe_dims_t& d);
+moe_status_t run_ffn_decode_gateup_one_token(const moe_dims_t& d, const uint16_t* x, const int32_t* topk_ids,
+                                             int32_t* dev_status, const uint8_t* w_gate, const float* s_gate,
+                                             const uint8_t* w_up, const float* s_up, float* h, hipStream_t stream);
+
 bool decode_down_combine_fits(const moe_dims_t& d, int32_t T);
 moe_status_t run_ffn_decode_down_combine(const moe_dims_t& d, int32_t T, const float* h, const int32_t* offsets,
                                          const uint8_t* w_down, const float* s_down, const int32_t* dest_row,
                                          const float* topk_w, uint16_t* out, hipStream_t stream);
+moe_status_t run_ffn_decode_down_combine_one_token(const moe_dims_t& d, const float* h, const int32_t* topk_ids,
+                                                   const uint8_t* w_down, const float* s_down, const float* topk_w,
+                                                   uint16_t* out, hipStream_t stream);
 
 moe_status_t launch_layer_prologue(const uint16_t* x, int32_t T, int32_t H, const int32_t* topk_ids, int32_t k,
                                    int32_t E, uint8_t* qx, float* sx, int32_t* offsets, int32_t* sorted_src,
@@ -249,6 +257,17 @@ extern "C" moe_status_t moe_ffn_layer(moe_dims_t d, int32_t T, moe_regime_t regi
   int32_t* dest_row = reinterpret_cast<int32_t*>(b + L.dest_row);
   float* y = reinterpret_cast<float*>(b + L.y);
   const size_t R = (size_t)T * d.topk;
+
+  if (rg == MOE_REGIME_DECODE && T == 1 && decode_down_combine_fits(d, T) && decode_one_token_fits(d)) {
+    // One token: two launches and no prologue.  Gate/up quantizes the row
+    // and reads the expert ids itself (row j of h is slot j); the down
+    // projection and the combine follow in one launch.  The results are
+    // bit-identical to the sorted path below.
+    float* h = reinterpret_cast<float*>(b + L.ffn);
+    st = run_ffn_decode_gateup_one_token(d, x_bf16, topk_ids, dev_status, w_gate, s_gate, w_up, s_up, h, stream);
+    if (st != MOE_OK) return st;
+    return run_ffn_decode_down_combine_one_token(d, h, topk_ids, w_down, s_down, topk_w, out_bf16, stream);
+  }
 
   // Quantize and sort: one launch for a single chunk of tokens.
   if (T <= 256) {

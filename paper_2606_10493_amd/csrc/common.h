@@ -161,14 +161,16 @@ __device__ __forceinline__ float silu_mul_fast(float g, float u) {
 }
 
 // Eight consecutive values of a row as fp32 (one 16-byte load of bf16, two of fp32).
-__device__ __forceinline__ void load8_f32(const uint16_t* p, float (&v)[8]) {
-  const uint4 raw = *reinterpret_cast<const uint4*>(p);
+__device__ __forceinline__ void bf16x8_to_f32(const uint4 raw, float (&v)[8]) {
   const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     v[2 * i] = bf16_to_f32(w[i] & 0xffffu);
     v[2 * i + 1] = bf16_to_f32(w[i] >> 16);
   }
+}
+__device__ __forceinline__ void load8_f32(const uint16_t* p, float (&v)[8]) {
+  bf16x8_to_f32(*reinterpret_cast<const uint4*>(p), v);
 }
 __device__ __forceinline__ void load8_f32(const float* p, float (&v)[8]) {
   const float4 a = *reinterpret_cast<const float4*>(p);
@@ -182,6 +184,18 @@ __device__ __forceinline__ void load8_f32(const float* p, float (&v)[8]) {
 // (lane sub of the group: columns 8 sub .. 8 sub + 7).  The block amax is
 // reduced over the 16 lanes, s = amax / 448, and the lane writes its 8
 // codes; lane 0 of the group writes s.
+// The arithmetic of one group: this lane's 8 values -> 8 codes, the group's
+// scale returned (every lane of the 16 calls it together).
+__device__ __forceinline__ float quant_group8(const float (&v)[8], uint2& codes) {
+  float amax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
+#pragma unroll
+  for (int m = 8; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
+  const float sc = amax / kE4M3Max;
+  codes = make_uint2(quantize4_e4m3(v[0], v[1], v[2], v[3], sc), quantize4_e4m3(v[4], v[5], v[6], v[7], sc));
+  return sc;
+}
 template <typename InT>
 __device__ __forceinline__ void quant_row_group(const InT* __restrict__ x, int64_t g, int sub, int groups_per_row,
                                                 uint8_t* __restrict__ q, float* __restrict__ s) {
@@ -190,15 +204,9 @@ __device__ __forceinline__ void quant_row_group(const InT* __restrict__ x, int64
   const int64_t idx = row * (int64_t)groups_per_row * kBlock + col;
   float v[8];
   load8_f32(x + idx, v);
-  float amax = 0.0f;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
-#pragma unroll
-  for (int m = 8; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
-  const float sc = amax / kE4M3Max;
-  const uint32_t lo = quantize4_e4m3(v[0], v[1], v[2], v[3], sc);
-  const uint32_t hi = quantize4_e4m3(v[4], v[5], v[6], v[7], sc);
-  *reinterpret_cast<uint2*>(q + idx) = make_uint2(lo, hi);
+  uint2 codes;
+  const float sc = quant_group8(v, codes);
+  *reinterpret_cast<uint2*>(q + idx) = codes;
   if (sub == 0) s[g] = sc;
 }
 

@@ -39,6 +39,13 @@
 // to the block sum.  h is written in bf16 and is the down projection's
 // activation.
 //
+// X1 (one token, no layer prologue): the gate/up kernel quantizes the bf16
+// token row into LDS itself (the rule of moe_quant_act, once per workgroup,
+// after its first weight block is issued) and takes slot j's expert straight
+// from topk_ids: the k slots of one token are distinct experts, so no sort is
+// needed, and row j of h is slot j.  Workgroup 0 reports bad ids as the sort
+// would; a slot with a bad id gets no row.
+//
 // GATEUP: the tile holds the same 16*NT rows of W_gate and W_up, and the
 // epilogue writes h = SiLU(G) * U in fp32 (bf16 with A16).  Down: h is quantized per row per
 // 128 (QH: in this kernel's prologue, for at most kQhRows rows per expert;
@@ -65,6 +72,9 @@ struct DecodeArgs {
   uint16_t* out16;            // A16 GATEUP: bf16 h [rows, N] (out unused)
   const float* hf;            // QH: fp32 h rows [rows, K] quantized in the prologue
   int m_lo, m_hi;             // the launch covers the experts with m_lo <= rows <= m_hi
+  const uint16_t* x16;        // X1: bf16 activations of the one token [K], quantized in the kernel
+  const int32_t* ids;         // X1: the token's topk expert ids; row j of out is slot j
+  int32_t* dev_status;        // X1: MOE_DEV_* bits OR-ed in for bad ids (workgroup 0), or NULL
 };
 
 namespace {
@@ -72,6 +82,8 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kQhRows = 4;    // QH: rows of h quantized in the down kernel's prologue
 constexpr int kQhMaxK = 2048; // QH: 16 lane groups x 128 columns
+constexpr int kX1MaxK = 8192; // X1: the token row in LDS, 4 passes of 16 lane groups x 128 columns
+constexpr int kX1Passes = kX1MaxK / kBlock / (256 / 16);
 
 // The a-th expert whose row count lies in [m_lo, m_hi] (or -1), the number
 // of such experts and the expert's row range, found by one wave with ballots.  The offsets of 256
@@ -128,10 +140,11 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(int d0, int d1) {
   return bf16x8{a[0], a[1], b[0], b[1], c[0], c[1], e[0], e[1]};
 }
 
-template <int MT, int NT, bool GATEUP, bool QH, int U, bool A16 = false>
+template <int MT, int NT, bool GATEUP, bool QH, int U, bool A16 = false, bool X1 = false>
 __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   static_assert(!QH || (!GATEUP && MT == 1), "QH is the down projection with at most 16 rows");
   static_assert(!(A16 && QH), "W8A16 reads bf16 h rows directly");
+  static_assert(!X1 || (GATEUP && MT == 1 && !A16), "X1 is the one-token gate/up");
   static_assert(!GATEUP || NT == 1, "a GATEUP tile is 16 rows of W_gate and of W_up");
   constexpr bool kSplit = GATEUP && MT == 1;  // one matrix per wave (waves 0, 1 gate; 2, 3 up)
   constexpr int G = (GATEUP && !kSplit) ? 2 : 1;  // weight matrices per wave
@@ -139,6 +152,8 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   __shared__ float red[(kWaves - 1) * kPer * 64];
   __shared__ __attribute__((aligned(16))) uint8_t qh_lds[QH ? kQhRows * kQhMaxK : 16];
   __shared__ float sh_lds[QH ? kQhRows * (kQhMaxK / kBlock) : 1];
+  __shared__ __attribute__((aligned(16))) uint8_t qx_lds[X1 ? kX1MaxK : 16];
+  __shared__ float sx_lds[X1 ? kX1MaxK / kBlock : 1];
 
   const int nb = p.K / kBlock;
   const int lane = threadIdx.x & 63;
@@ -159,11 +174,49 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   const uint8_t* wfirst_mat = up_wave ? p.w1 : p.w0;
   const float* sfirst_mat = up_wave ? p.s1 : p.s0;
 
-  ExpertRef ref = find_expert(p.offsets, p.E, blockIdx.x / tiles, p.m_lo, p.m_hi);
+  // X1: the token's bf16 row goes out first, 8 values per lane of each
+  // 16-lane group of a 128-column block (blocks past the last load the last
+  // again), to be quantized into LDS once the first weights are in flight.
+  uint4 xraw[X1 ? kX1Passes : 1];
+  if constexpr (X1) {
+#pragma unroll
+    for (int q = 0; q < kX1Passes; ++q) {
+      const int g = min((int)(threadIdx.x >> 4) + q * 16, nb - 1);
+      xraw[q] = *reinterpret_cast<const uint4*>(p.x16 + g * kBlock + (threadIdx.x & 15) * 8);
+    }
+  }
+  // X1: item a * tiles + t is slot a's expert (one row, row a of out), with
+  // no sort: the slots of one token are distinct experts.  A slot whose id
+  // lies outside [0, E) or repeats an earlier slot's has no row (m = 0), as
+  // the sort leaves such slots out; workgroup 0 reports them.
+  auto slot_ref = [&](int64_t a) {
+    const int idv = lane < p.topk ? p.ids[lane] : -1;
+    const int e = __shfl(idv, (int)a);
+    const bool dup = __ballot(lane < a && idv == e) != 0ull;
+    const bool ok = e >= 0 && e < p.E && !dup;
+    return ExpertRef{ok ? e : -1, p.topk, (int)a, ok ? 1 : 0};
+  };
+  if constexpr (X1) {
+    if (blockIdx.x == 0 && wave == 0) {
+      const int idv = lane < p.topk ? p.ids[lane] : 0;
+      uint32_t err = 0;
+      bool dup = false;
+      for (int i = 0; i < p.topk; ++i) {
+        const int o = __shfl(idv, i);
+        dup |= i < lane && o == idv;
+      }
+      if (lane < p.topk) err = (idv < 0 || idv >= p.E) ? MOE_DEV_BAD_EXPERT_ID : dup ? MOE_DEV_DUP_EXPERT_ID : 0u;
+      for (int m = 32; m >= 1; m >>= 1) err |= (uint32_t)__shfl_xor((int)err, m, 64);
+      if (p.dev_status && err && lane == 0) atomicOr(p.dev_status, (int)err);
+    }
+  }
+  bool x_done = false;  // X1: qx_lds holds the token row
+
+  ExpertRef ref = X1 ? slot_ref(blockIdx.x / tiles) : find_expert(p.offsets, p.E, blockIdx.x / tiles, p.m_lo, p.m_hi);
   const int64_t items = (int64_t)ref.n_active * tiles;
 
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
-    if (item != blockIdx.x) ref = find_expert(p.offsets, p.E, item / tiles, p.m_lo, p.m_hi);
+    if (item != blockIdx.x) ref = X1 ? slot_ref(item / tiles) : find_expert(p.offsets, p.E, item / tiles, p.m_lo, p.m_hi);
     const int e = ref.e;
     const int n0 = (int)(item % tiles) * 16 * NT;
     const int p0 = ref.p0;
@@ -208,7 +261,7 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       };
       int ta[MT], ts[MT][4];
       int raw[MT][5];
-      if (!QH) {
+      if (!QH && !X1) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -244,7 +297,28 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
       v8i wfirst[G][NT];
       if (nkw > 0) load_w(kb0, wfirst);
       __builtin_amdgcn_sched_barrier(0);
-      if (!QH) {
+      if (X1) {  // the one token row: A row 0, scale row 0
+        ta[0] = r == 0 ? 0 : -1;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ts[0][i] = (kq == 0 && i == 0) ? 0 : -1;
+        if (!x_done) {
+          // The token row per 128 -> e4m3 in LDS (the rule of moe_quant_act).
+#pragma unroll
+          for (int q = 0; q < kX1Passes; ++q) {
+            const int g = (int)(threadIdx.x >> 4) + q * 16;
+            if (g < nb) {  // whole 16-lane groups
+              float v[8];
+              bf16x8_to_f32(xraw[q], v);
+              uint2 codes;
+              const float sc = quant_group8(v, codes);
+              *reinterpret_cast<uint2*>(qx_lds + g * kBlock + (threadIdx.x & 15) * 8) = codes;
+              if ((threadIdx.x & 15) == 0) sx_lds[g] = sc;
+            }
+          }
+          __syncthreads();
+          x_done = true;
+        }
+      } else if (!QH) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -297,6 +371,10 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
             const int row = 4 * kq + i;
             sa[0][i] = row < kQhRows ? sh_lds[row * (kQhMaxK / kBlock) + bk] : 0.0f;
           }
+        } else if (X1) {
+          afrag[0] = ta[0] >= 0 ? load_v8i_ksplit(qx_lds + bk * kBlock + kq * 16) : v8i{0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) sa[0][i] = ts[0][i] >= 0 ? sx_lds[bk] : 0.0f;
         } else if (!A16) {
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
@@ -435,13 +513,14 @@ __global__ __launch_bounds__(256) void ffn_decode_kernel(DecodeArgs p) {
   }
 }
 
-template <int MT, int NT, bool GATEUP, bool QH, int U, bool A16 = false>
+template <int MT, int NT, bool GATEUP, bool QH, int U, bool A16 = false, bool X1 = false>
 moe_status_t launch_decode(const DecodeArgs& a, int64_t max_items, hipStream_t stream) {
   const int64_t grid = max_items < 2048 ? max_items : 2048;
   if (grid <= 0) return MOE_OK;
   const char* name = A16 ? (GATEUP ? "ffn_decode_w8a16_gateup" : "ffn_decode_w8a16_down")
                          : (GATEUP ? "ffn_decode_gateup" : "ffn_decode_down");
-  MOE_LAUNCH(name, (ffn_decode_kernel<MT, NT, GATEUP, QH, U, A16>), dim3((unsigned)grid), dim3(256), 0, stream, a);
+  MOE_LAUNCH(name, (ffn_decode_kernel<MT, NT, GATEUP, QH, U, A16, X1>), dim3((unsigned)grid), dim3(256), 0, stream,
+             a);
   return check_launch(name);
 }
 
@@ -495,6 +574,27 @@ moe_status_t run_ffn_decode_gateup(const moe_dims_t& d, int32_t T, const uint8_t
   g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
   g.N = d.inter; g.K = d.hidden; g.out = h;
   return launch_by_rows<1, true, false, 3, 2>(g, T, R, d.inter / 16, stream);
+}
+
+// One token without the layer prologue: the gate/up GEMV quantizes the bf16
+// row and takes slot j's expert from topk_ids itself (no sort: one token's
+// slots are distinct experts); h row j belongs to slot j, and a slot with a
+// bad id has no row.  Needs K = H <= kX1MaxK; callers check
+// decode_one_token_fits.
+bool decode_one_token_fits(const moe_dims_t& d) { return d.hidden <= kX1MaxK; }
+
+moe_status_t run_ffn_decode_gateup_one_token(const moe_dims_t& d, const uint16_t* x, const int32_t* topk_ids,
+                                             int32_t* dev_status, const uint8_t* w_gate, const float* s_gate,
+                                             const uint8_t* w_up, const float* s_up, float* h, hipStream_t stream) {
+  moe_status_t st0 = decode_shape_check(d);
+  if (st0 != MOE_OK) return st0;
+  if (!decode_one_token_fits(d))
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "one-token decode: H=%d > %d", d.hidden, kX1MaxK);
+  DecodeArgs g{};
+  g.x16 = x; g.ids = topk_ids; g.dev_status = dev_status; g.topk = d.topk; g.a_rows = 1; g.E = d.n_experts;
+  g.w0 = w_gate; g.s0 = s_gate; g.w1 = w_up; g.s1 = s_up;
+  g.N = d.inter; g.K = d.hidden; g.out = h;
+  return launch_decode<1, 1, true, false, 3, false, true>(g, (int64_t)d.topk * (d.inter / 16), stream);
 }
 
 // Decode-regime FFN: gate/up -> h (fp32) -> quantize h -> down.

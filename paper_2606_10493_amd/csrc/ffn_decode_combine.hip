@@ -45,6 +45,7 @@ struct DownCombineArgs {
   const float* topk_w;      // [T * k]
   int topk, tokens;
   uint16_t* out;            // bf16 [T, N]
+  const int32_t* ids;       // SLOT1 (T = 1): the token's expert ids; h row j is slot j (offsets, dest_row unused)
 };
 
 // The active experts (those with rows) of slot `sub`: the a-th active
@@ -100,11 +101,48 @@ __device__ __forceinline__ int active_experts(const int32_t* __restrict__ offset
   return n_act;
 }
 
+// One token (SLOT1): the same lanes as active_experts, from the token's ids
+// in slot order: slot j is expert ids[j] with one row, row j, when the id
+// lies in [0, E) and no earlier slot has it (the slots the sort keeps).
+// Returns the number of such slots.
+template <int SLOTS>
+__device__ __forceinline__ int active_slots(const int32_t* __restrict__ ids, int k, int E, int sub, int& v_e,
+                                            int& v_p0, int& v_m) {
+  const int lane = threadIdx.x & 63;
+  const int idv = lane < k ? ids[lane] : -1;
+  bool dup = false;
+  for (int i = 0; i < k; ++i) {
+    const int o = __shfl(idv, i);
+    dup |= i < lane && o == idv;
+  }
+  const bool on = lane < k && idv >= 0 && idv < E && !dup;
+  const unsigned long long bal = __ballot(on);
+  const int rank = (int)__builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
+  unsigned long long want = __ballot(on && rank >= sub && ((rank - sub) & (SLOTS - 1)) == 0);
+  v_e = 0;
+  v_p0 = 0;
+  v_m = 0;
+  int found = 0;
+  while (want != 0ull) {
+    const int pos = __ffsll((long long)want) - 1;
+    const int e = __builtin_amdgcn_readlane(idv, pos);
+    if (lane == found) {
+      v_e = e;
+      v_p0 = pos;
+      v_m = 1;
+    }
+    ++found;
+    want &= want - 1ull;
+  }
+  return __popcll(bal);
+}
+
 // NT: 16-column operands per workgroup; HQ: h row blocks per 16-lane group
 // loaded before the weight window (the rest, if R * K / 128 > 64 HQ, are
 // loaded after it); W: items in the weight window; NCH: 256-expert chunks
-// of the offsets (E <= 256 NCH); WAVES: 4 K parts x WAVES / 4 expert slots.
-template <int NT, int HQ, int W, int NCH, int WAVES>
+// of the offsets (E <= 256 NCH); WAVES: 4 K parts x WAVES / 4 expert slots;
+// SLOT1: one token, experts from p.ids in slot order (active_slots).
+template <int NT, int HQ, int W, int NCH, int WAVES, bool SLOT1 = false>
 __global__ __launch_bounds__(64 * WAVES) void ffn_decode_down_combine_kernel(DownCombineArgs p) {
   constexpr int kCols = 16 * NT;
   constexpr int kDcThreads = 64 * WAVES;
@@ -114,6 +152,7 @@ __global__ __launch_bounds__(64 * WAVES) void ffn_decode_down_combine_kernel(Dow
   __shared__ float sh[kDcMaxRows * (kDcMaxK / kBlock)];
   __shared__ float part[4 * kDcMaxRows * kCols];  // [K part][expert row][column]
   __shared__ __attribute__((aligned(16))) float yl[kDcMaxRows * kCols];
+  __shared__ int32_t dest_id[SLOT1 ? kDcMaxRows : 1];  // SLOT1: slot j's row is row j
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -140,7 +179,8 @@ __global__ __launch_bounds__(64 * WAVES) void ffn_decode_down_combine_kernel(Dow
   // receives expert a = sub + kSlots g, the a-th expert with rows (expert
   // order), with its first row and row count.
   int v_e, v_p0, v_m;
-  const int n_act = active_experts<NCH, kSlots>(p.offsets, p.E, sub, v_e, v_p0, v_m);
+  const int n_act = SLOT1 ? active_slots<kSlots>(p.ids, p.topk, p.E, sub, v_e, v_p0, v_m)
+                          : active_experts<NCH, kSlots>(p.offsets, p.E, sub, v_e, v_p0, v_m);
 
   // Items of this wave: (expert a = sub + kSlots g, block j) for g < n_mine, j < nkw.
   const int nkw = (nb - kw + 3) / 4;
@@ -200,6 +240,7 @@ __global__ __launch_bounds__(64 * WAVES) void ffn_decode_down_combine_kernel(Dow
   // Partials start at zero: a wave without K blocks (K < 512) adds +0.0, as
   // the decode down kernel's does.
   for (int i = tid; i < 4 * kDcMaxRows * kCols; i += kDcThreads) part[i] = 0.0f;
+  if (SLOT1 && tid < kDcMaxRows) dest_id[tid] = tid;
   __syncthreads();
 
   v4f acc[NT];
@@ -260,7 +301,8 @@ __global__ __launch_bounds__(64 * WAVES) void ffn_decode_down_combine_kernel(Dow
     const int t = idx / kPerTok;
     const int c = (idx - t * kPerTok) * 8;
     *reinterpret_cast<uint4*>(p.out + (int64_t)t * p.N + n0 + c) =
-        combine8_of([&](int64_t row) { return yl + row * kCols + c; }, p.dest_row, p.topk_w, p.topk, t);
+        combine8_of([&](int64_t row) { return yl + row * kCols + c; }, SLOT1 ? dest_id : p.dest_row, p.topk_w,
+                    p.topk, t);
   }
 }
 
@@ -294,6 +336,24 @@ moe_status_t run_ffn_decode_down_combine(const moe_dims_t& d, int32_t T, const f
   else
     MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<1, 4, 4, kDcMaxExperts / 256, 8>),
                dim3((unsigned)(d.hidden / 16)), dim3(512), 0, stream, a);
+  return check_launch("ffn_decode_down_combine");
+}
+
+// One token (T = 1, k <= 16): as run_ffn_decode_down_combine with h row j
+// belonging to slot j (run_ffn_decode_gateup_one_token's rows) and the
+// experts taken from topk_ids.
+moe_status_t run_ffn_decode_down_combine_one_token(const moe_dims_t& d, const float* h, const int32_t* topk_ids,
+                                                   const uint8_t* w_down, const float* s_down, const float* topk_w,
+                                                   uint16_t* out, hipStream_t stream) {
+  if (!decode_down_combine_fits(d, 1))
+    return fail(MOE_ERR_UNSUPPORTED_SHAPE, "decode down+combine: k=%d (max %d), I=%d (max %d)", d.topk, kDcMaxRows,
+                d.inter, kDcMaxK);
+  DownCombineArgs a{};
+  a.h = h; a.ids = topk_ids; a.E = d.n_experts;
+  a.w = w_down; a.s = s_down; a.N = d.hidden; a.K = d.inter;
+  a.topk_w = topk_w; a.topk = d.topk; a.tokens = 1; a.out = out;
+  MOE_LAUNCH("ffn_decode_down_combine", (ffn_decode_down_combine_kernel<1, 4, 4, 1, 8, true>),
+             dim3((unsigned)(d.hidden / 16)), dim3(512), 0, stream, a);
   return check_launch("ffn_decode_down_combine");
 }
 

@@ -116,6 +116,27 @@ def test_fused_layer_reports_bad_ids(moe, regime, tokens):
     assert np.array_equal(a.out.cpu().numpy()[good], b.out.cpu().numpy()[good])
 
 
+@pytest.mark.parametrize("bad_kind", ["range", "dup", "both"])
+def test_one_token_layer_reports_bad_ids(moe, bad_kind):
+    """One token (no sort launch): an id outside [0, E) and an id repeated in
+    the token's top-k set the same dev_status bits as the sort does."""
+    w, x, ids, wts = _layer_inputs(512, 256, 16, 4, 1, "uniform", seed=8)
+    ids = ids.copy()
+    if bad_kind in ("range", "both"):
+        ids[0, 1] = 16 if bad_kind == "range" else -3
+    if bad_kind in ("dup", "both"):
+        ids[0, 3] = ids[0, 0]
+    wg, wu, wd = synth.weights_host(w)
+    dweights = quantize_weights_gpu(moe, wg, wu, wd)
+    a = _run(moe, w, x, ids, wts, dweights, moe.MOE_REGIME_DECODE, fused=True)
+    b = _run(moe, w, x, ids, wts, dweights, moe.MOE_REGIME_DECODE, fused=False)
+    st = int(a.dev_status.item())
+    assert st == int(b.dev_status.item())
+    want = {"range": moe.MOE_DEV_BAD_EXPERT_ID, "dup": moe.MOE_DEV_DUP_EXPERT_ID,
+            "both": moe.MOE_DEV_BAD_EXPERT_ID | moe.MOE_DEV_DUP_EXPERT_ID}[bad_kind]
+    assert st == want
+
+
 def test_fused_layer_zero_tokens_and_small_workspace(moe):
     w, x, ids, wts = _layer_inputs(256, 128, 8, 2, 4, "uniform")
     wg, wu, wd = synth.weights_host(w)
@@ -155,6 +176,10 @@ def test_fused_layer_deepseek_decode_equals_four_calls(moe, deepseek_layer, name
     (256, 128, 1024, 32, 2, "decode"),    # E = 1024, k = 32: the widest sort
     (256, 128, 1024, 16, 1, "decode"),    # E = 1024, T * k = 16: fused down + combine over four 256-expert chunks
     (256, 128, 300, 8, 2, "decode"),      # E = 300: fused down + combine, a partial second chunk
+    (256, 128, 32, 16, 1, "decode"),      # one token, k = 16: the most slots of the one-token path
+    (8192, 256, 8, 4, 1, "decode"),       # one token at the largest H the one-token path takes
+    (8320, 256, 8, 4, 1, "decode"),       # one token with H > 8192: through the sort
+    (128, 128, 4, 2, 1, "decode"),        # one token, one K block: a gate/up wave without blocks
     (256, 128, 1024, 32, 40, "prefill"),
     (384, 128, 8, 2, 9, "decode"),        # H a multiple of 128 but not of 256 (decode only)
     (8448, 256, 4, 2, 40, "prefill"),     # K = 8448 > 8192: row scales beyond one 16-load batch
