@@ -156,6 +156,28 @@ def algorithmic(w, ids):
     }
 
 
+def prefill_gemm_bytes(w, ids, groups):
+    """Algorithmic HBM bytes of the prefill GEMM launches of one layer call,
+    one launch pair per group [e0, e1) of experts: gate/up reads the group's
+    active experts' W_gate, W_up and scales once, each token row (qx + sx)
+    with a slot in the group once, and writes qh + sh of the group's routed
+    rows; down reads the active experts' W_down and scales and those qh + sh
+    rows once, and writes the rows' fp32 outputs."""
+    import numpy as np
+    h, i = w.hidden, w.inter
+    sc_gu = 2 * (i // 128) * (h // 128) * 4
+    sc_d = (h // 128) * (i // 128) * 4
+    gu = dn = 0
+    for e0, e1 in groups:
+        m = (ids >= e0) & (ids < e1)
+        rows = int(m.sum())
+        toks = int(m.any(axis=1).sum())
+        act = int(np.unique(ids[m]).size)
+        gu += act * (2 * i * h + sc_gu) + toks * (h + (h // 128) * 4) + rows * (i + (i // 128) * 4)
+        dn += act * (h * i + sc_d) + rows * (i + (i // 128) * 4) + rows * h * 4
+    return gu, dn
+
+
 def profile_steps(moe, torch, step, n_steps, per_step):
     """Kernel durations of n_steps steps from the library's launch events:
     {name: (launches, total ms)}."""
@@ -219,16 +241,29 @@ def decode_roofline(alg, kern, steps, workload):
                            "us_per_step": round(us, 2)}}
 
 
-def prefill_roofline(flops_total, kern, dom, workload, launches_note=""):
-    """A prefill GEMM kernel against dense FP8 MFMA: algorithmic FLOPs per launch
-    over its mean launch duration."""
+def prefill_roofline(flops_total, bytes_total, kern, dom, workload, launches_note=""):
+    """A prefill GEMM kernel against its roofline: algorithmic FLOPs and HBM
+    bytes per launch over its mean launch duration.  The bound is the larger
+    of FLOPs at the dense FP8 MFMA peak and bytes at the HBM peak, i.e. the
+    side of the ridge point (5.0 PFLOP/s / 8 TB/s = 625 FLOP/B) the launch's
+    arithmetic intensity falls on: an expert with a few hundred rows (8192
+    tokens over 256 experts) reads more weight bytes than its MFMAs can hide,
+    an expert group with thousands of rows (the 32768-token streamed layer)
+    does not.  Both fractions are reported."""
     n, tot_ms = kern[dom]
     avg_us = 1000.0 * tot_ms / n
-    per_launch = flops_total / n
-    achieved = per_launch / (avg_us * 1e-6) / 1e12
-    return {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": FP8_PEAK_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4), "traffic": measured_traffic(workload, dom),
-            "per_launch": {"launches": n, "algorithmic_flops": round(per_launch), "avg_us": round(avg_us, 2),
+    flops = flops_total / n
+    nbytes = bytes_total / n
+    tflops = flops / (avg_us * 1e-6) / 1e12
+    gbs = nbytes / (avg_us * 1e-6) / 1e9
+    mfma = flops / (FP8_PEAK_TFLOPS * 1e12) >= nbytes / (HBM_PEAK_GBS * 1e9)
+    achieved, peak, unit = (tflops, FP8_PEAK_TFLOPS, "TFLOP/s") if mfma else (gbs, HBM_PEAK_GBS, "GB/s")
+    return {"kernel": dom, "bound": "mfma" if mfma else "hbm", "achieved": round(achieved, 1), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 4), "traffic": measured_traffic(workload, dom),
+            "per_launch": {"launches": n, "algorithmic_flops": round(flops), "algorithmic_bytes": round(nbytes),
+                           "flop_per_byte": round(flops / nbytes, 1), "avg_us": round(avg_us, 2),
+                           "TFLOPs": round(tflops, 1), "frac_of_fp8_peak": round(tflops / FP8_PEAK_TFLOPS, 4),
+                           "GBps": round(gbs, 1), "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
                            **({"note": launches_note} if launches_note else {})}}
 
 
@@ -258,8 +293,11 @@ def resident_summary(moe, torch, synth, cache, extra, steps, warmup, layers_n, f
         res["roofline"] = decode_roofline(alg, kern, steps, base_name)
         res["layer_frac_hbm"] = round(alg["layer_weight_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
     else:
-        res["roofline"] = prefill_roofline(alg["gateup_flops"] * steps, kern, "ffn_prefill_gateup", base_name)
-        res["roofline_down"] = prefill_roofline(alg["down_flops"] * steps, kern, "ffn_prefill_down", base_name)
+        gu_b, dn_b = prefill_gemm_bytes(w, ids, [(0, w.n_experts)])
+        res["roofline"] = prefill_roofline(alg["gateup_flops"] * steps, gu_b * steps, kern, "ffn_prefill_gateup",
+                                           base_name)
+        res["roofline_down"] = prefill_roofline(alg["down_flops"] * steps, dn_b * steps, kern, "ffn_prefill_down",
+                                                base_name)
         res["layer_TFLOPs"] = round((alg["gateup_flops"] + alg["down_flops"]) / (ms * 1e-3) / 1e12, 1)
     return res
 
@@ -546,7 +584,8 @@ def main_resident(args, moe, torch, synth, cache, steps, warmup, layers_n):
     if decode:
         roof = decode_roofline(alg, kern, steps, args.workload)
     else:
-        roof = prefill_roofline(alg["gateup_flops"] * steps, kern, "ffn_prefill_gateup", args.workload)
+        gu_b, _ = prefill_gemm_bytes(w, ids, [(0, w.n_experts)])
+        roof = prefill_roofline(alg["gateup_flops"] * steps, gu_b * steps, kern, "ffn_prefill_gateup", args.workload)
     layer_gbs = alg["layer_weight_bytes"] / (ms * 1e-3) / 1e9
     layer_tflops = (alg["gateup_flops"] + alg["down_flops"]) / (ms * 1e-3) / 1e12
     res = {
@@ -565,6 +604,22 @@ def main_resident(args, moe, torch, synth, cache, steps, warmup, layers_n):
     return res, w, x, ids, wts
 
 
+def streamed_gemm_bytes(moe, w, ids_all, n_layers):
+    """prefill_gemm_bytes of every layer call of a streamed step, with the
+    expert groups of the call's launches taken from the ring schedule the
+    library executes (moe_stream_schedule)."""
+    dims = moe.MoeDims(w.hidden, w.inter, w.n_experts, w.topk)
+    slots = w.ring_slots or w.n_experts
+    ops, _ = moe.moe_stream_schedule(dims, w.tokens, w.chunk_tokens, slots)
+    groups = [(a, a + b) for op, a, b, _c in ops if op == moe.MOE_SOP_LAUNCH]
+    gu = dn = 0
+    for layer in range(n_layers):
+        g, d = prefill_gemm_bytes(w, ids_all[layer * w.tokens:(layer + 1) * w.tokens], groups)
+        gu += g
+        dn += d
+    return gu, dn
+
+
 def main_streamed(args, moe, torch, synth, cache, steps, warmup):
     w, ids, wts, x, ms, copy_ms, h2d_bytes, kern, per_layer = time_streamed(moe, torch, synth, cache, args.workload,
                                                                             steps, warmup)
@@ -578,8 +633,11 @@ def main_streamed(args, moe, torch, synth, cache, steps, warmup):
     if os.environ.get("HSA_ENABLE_SDMA") == "0":
         note += ("; with shader copies the copy kernels share the compute units with the expert kernels, so "
                  "these launch durations include waiting for them")
-    roof = prefill_roofline(alg["gateup_flops"] * steps, kern, "ffn_prefill_gateup", args.workload, note)
-    roof_dn = prefill_roofline(alg["down_flops"] * steps, kern, "ffn_prefill_down", args.workload, note)
+    gu_b, dn_b = streamed_gemm_bytes(moe, w, ids, n_layers)
+    roof = prefill_roofline(alg["gateup_flops"] * steps, gu_b * steps, kern, "ffn_prefill_gateup", args.workload,
+                            note)
+    roof_dn = prefill_roofline(alg["down_flops"] * steps, dn_b * steps, kern, "ffn_prefill_down", args.workload,
+                               note)
     res = {
         "metric": METRIC, "value": round(w.tokens / (ms / 1000.0), 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": steps, "warmup": warmup, "ms_per_step": round(ms, 3), "higher_is_better": True,
