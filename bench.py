@@ -552,11 +552,24 @@ def main():
             kus = time_router(moe, torch, synth, w, r_steps, r_warm)
             also["router"] = {"tokens": w.tokens, "kernel_us": kus}
             if kus.get("router_logits"):
-                # logits = x W_r^T: 2 T H E FLOPs of bf16 MFMA (the selection is latency-bound and small)
-                tf = 2.0 * w.tokens * w.hidden * w.n_experts / (kus["router_logits"] * 1e-6) / 1e12
-                also["router"]["roofline"] = {"kernel": "router_logits", "bound": "mfma", "achieved": round(tf, 1),
-                                              "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                                              "frac": round(tf / BF16_PEAK_TFLOPS, 4), "traffic": None}
+                # logits = x W_r^T: 2 T H E FLOPs of bf16 MFMA over the bf16 hidden states and router weight
+                # read once and the fp32 logits written once (the selection is latency-bound and small).  The
+                # bound is the side of the bf16 ridge point (2.5 PFLOP/s / 8 TB/s = 312.5 FLOP/B) the
+                # intensity falls on: about E = 256 FLOP/B, so HBM.
+                t, h, e = w.tokens, w.hidden, w.n_experts
+                flops = 2.0 * t * h * e
+                nbytes = 2.0 * t * h + 2.0 * e * h + 4.0 * t * e
+                sec = kus["router_logits"] * 1e-6
+                tf, gbs = flops / sec / 1e12, nbytes / sec / 1e9
+                mfma = flops / (BF16_PEAK_TFLOPS * 1e12) >= nbytes / (HBM_PEAK_GBS * 1e9)
+                ach, peak, unit = (tf, BF16_PEAK_TFLOPS, "TFLOP/s") if mfma else (gbs, HBM_PEAK_GBS, "GB/s")
+                also["router"]["roofline"] = {
+                    "kernel": "router_logits", "bound": "mfma" if mfma else "hbm", "achieved": round(ach, 1),
+                    "peak": peak, "unit": unit, "frac": round(ach / peak, 4), "traffic": None,
+                    "per_launch": {"algorithmic_flops": round(flops), "algorithmic_bytes": round(nbytes),
+                                   "flop_per_byte": round(flops / nbytes, 1), "us": kus["router_logits"],
+                                   "TFLOPs": round(tf, 1), "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
+                                   "GBps": round(gbs, 1), "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}}
             continue
         base = extra[:-len("_w8a16")] if extra.endswith("_w8a16") else extra
         if synth.WORKLOADS[base].chunk_tokens:

@@ -91,11 +91,14 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
 // supplies K bytes [16 kq, 16 kq + 16) and [64 + 16 kq, 80 + 16 kq) of the
 // block.  A and B share it, so each dot product runs over the whole block;
 // the instruction's internal order of K does not matter.
-// The E8M0 block scales of the instruction are left at 127 (= 1.0); the fp32
-// scales are applied to the result.
+// The instruction's own E8M0 block scales are not used: with both scale
+// operands 0 the compiler emits the unscaled v_mfma_f32_16x16x128_f8f6f4
+// (format 0 = e4m3 for both operands), one 8-byte instruction instead of the
+// scaled form's 16-byte pair of a scale load and the MFMA.  The fp32 scales
+// are applied to the result.
 __device__ __forceinline__ v4f mfma_f8_16x16x128(const v8i& a, const v8i& b) {
   const v4f zero = {0.f, 0.f, 0.f, 0.f};
-  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, zero, 0, 0, 0, 127, 0, 127);
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, zero, 0, 0, 0, 0, 0, 0);
 }
 
 // Packed weight layout (moe_pack_weight): a [rows, K] e4m3 matrix is stored

@@ -181,7 +181,9 @@ size_t tiles_desc_offset(int64_t n_units) { return 2 * tiles_index_bytes(n_units
 __device__ __forceinline__ int swz(int row, int c) { return row * kLdsRow + ((c ^ ((row >> 1) & 7)) << 4); }
 
 __device__ __forceinline__ v16f mfma_f8_32x32x64(const v8i& a, const v8i& b, const v16f& c) {
-  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
+  // Scale operands 0: the compiler emits the unscaled v_mfma_f32_32x32x64_f8f6f4
+  // (e4m3 operands, no block scales; see mfma_f8_16x16x128).
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
 // The tile of work item `item`: expert u owns items [mtile_start[u],
