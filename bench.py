@@ -45,33 +45,38 @@ DEFAULT_ALSO = "prefill8k,decode64_zipf,decode4,decode1,decode1_w8a16,router"
 # HBM bytes moved by a kernel, from rocprofv3 FETCH_SIZE and WRITE_SIZE runs
 # scaled by a plain 1 GiB copy (FETCH x2.000, WRITE x1.000), recorded in the
 # profiles/ summaries of each workload.  Valid only while the kernel's source
-# file is the one measured (sha256 prefix).  Decode entries are per step (all
-# launches of the kernel in a step), prefill entries per launch (the mean over
-# the launches of a step), as the rooflines that carry them.
+# file and the shared device header are the ones measured (sha256 prefix of
+# the two files' bytes, source first).  Decode entries are per step (all
+# launches of the kernel in a step), prefill entries per launch (the mean
+# over the launches of a step), as the rooflines that carry them.
 _DEC, _PRE = "paper_2606_10493_amd/csrc/ffn_decode.hip", "paper_2606_10493_amd/csrc/ffn_prefill.hip"
+_COMMON = "paper_2606_10493_amd/csrc/common.h"
+_DH, _PH = "cb7c22470036695c", "8d7be0b2719ce263"
 TRAFFIC = {
-    ("decode1", "ffn_decode_gateup"): {"bytes": 235721651, "source": _DEC, "sha256_prefix": "39bd3a7be7eb6d58"},
-    ("decode64_zipf", "ffn_decode_gateup"): {"bytes": 4603759047, "source": _DEC, "sha256_prefix": "39bd3a7be7eb6d58"},
-    ("decode4", "ffn_decode_gateup"): {"bytes": 942042780, "source": _DEC, "sha256_prefix": "39bd3a7be7eb6d58"},
-    ("decode1_w8a16", "ffn_decode_w8a16_gateup"): {"bytes": 235617550, "source": _DEC,
-                                                   "sha256_prefix": "39bd3a7be7eb6d58"},
-    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9697626778, "source": _PRE, "sha256_prefix": "7fb3d6681d45a9dc"},
-    ("prefill8k", "ffn_prefill_down"): {"bytes": 6157209830, "source": _PRE, "sha256_prefix": "7fb3d6681d45a9dc"},
-    ("prefill32k_streamed", "ffn_prefill_gateup"): {"bytes": 1366489044, "source": _PRE,
-                                                    "sha256_prefix": "7fb3d6681d45a9dc"},
-    ("prefill32k_streamed", "ffn_prefill_down"): {"bytes": 1098404608, "source": _PRE,
-                                                  "sha256_prefix": "7fb3d6681d45a9dc"},
+    ("decode1", "ffn_decode_gateup"): {"bytes": 235721523, "source": _DEC, "sha256_prefix": _DH},
+    ("decode64_zipf", "ffn_decode_gateup"): {"bytes": 4603754906, "source": _DEC, "sha256_prefix": _DH},
+    ("decode4", "ffn_decode_gateup"): {"bytes": 942054400, "source": _DEC, "sha256_prefix": _DH},
+    ("decode1_w8a16", "ffn_decode_w8a16_gateup"): {"bytes": 235617690, "source": _DEC, "sha256_prefix": _DH},
+    ("prefill8k", "ffn_prefill_gateup"): {"bytes": 9711002009, "source": _PRE, "sha256_prefix": _PH},
+    ("prefill8k", "ffn_prefill_down"): {"bytes": 6169021849, "source": _PRE, "sha256_prefix": _PH},
+    ("prefill32k_streamed", "ffn_prefill_gateup"): {"bytes": 1360592077, "source": _PRE, "sha256_prefix": _PH},
+    ("prefill32k_streamed", "ffn_prefill_down"): {"bytes": 1098833100, "source": _PRE, "sha256_prefix": _PH},
 }
 
 
-def measured_traffic(workload, kernel):
+def source_hash(source):
     import hashlib
+    h = hashlib.sha256()
+    for f in (source, _COMMON):
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
     t = TRAFFIC.get((workload, kernel))
-    if not t:
+    if not t or source_hash(t["source"]) != t["sha256_prefix"]:
         return None
-    with open(os.path.join(ROOT, t["source"]), "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest()[:16] != t["sha256_prefix"]:
-            return None
     return t["bytes"]
 
 
