@@ -160,10 +160,10 @@ def deepseek_layer(moe):
 
 @pytest.mark.parametrize("name", ["decode1", "decode2", "decode4", "decode64_zipf"])
 def test_fused_layer_deepseek_decode_equals_four_calls(moe, deepseek_layer, name):
-    """At H = 7168 the fused down + combine (one token, and two tokens through
-    the sort) runs 28-column windows, each crossing 16-row groups of W_down
-    and some a 128-row scale block; the four calls run the 16-column down
-    kernel and the combine."""
+    """The DeepSeek-V3 layer in one call equals the four calls bit for bit:
+    at one token the two-launch path (gate/up with its own quantization and
+    no sort, then the fused down + combine), at two tokens the sort with the
+    fused down + combine (T * k = 16), beyond it the separate kernels."""
     import dataclasses
     w = (dataclasses.replace(synth.WORKLOADS["decode4"], name="decode2", tokens=2) if name == "decode2"
          else synth.WORKLOADS[name])
